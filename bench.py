@@ -1,0 +1,172 @@
+#!/usr/bin/env python3
+"""Throughput of the OmniMem per-chunk KV-cache compression step on one MI355X.
+
+One step = the four stages of the C ABI (importance score, redundancy,
+AVBA allocation, select + compact) over one synthetic working set whose
+inputs are already resident in HBM.  The metric is KV tokens entering the
+step per second, summed over layers.  Prints one JSON line.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "KV tokens compressed/sec per layer-step; % MFMA peak (score+Gram), % HBM (top-k+compact)"
+PEAK_HBM_GBS = 8000.0                                   # MI355X HBM3E
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}       # dense MFMA
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="qwen7b-layer-6144")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+def algorithmic_work(layers, budgets, causal=True):
+    """Per-launch algorithmic units of each kernel (all layers in one launch)."""
+    score_flops = gram_flops = 0
+    compact_bytes = topk_bytes = 0
+    for lay, (mv, ma) in zip(layers, budgets):
+        h_q, c, d = lay["q"].shape
+        h_kv, n, _ = lay["k"].shape
+        nc = lay["n_cache"]
+        elt = 2 if lay["dtype"] == "bf16" else 4
+        pairs = c * nc + c * (c + 1) // 2 if causal else c * n
+        score_flops += 2 * d * h_q * pairs
+        for mu in (0, 1):
+            k = int((lay["modality"] == mu).sum())
+            gram_flops += h_kv * k * (k - 1) * d          # k(k-1)/2 pairs x 2d
+        m = int(mv) + int(ma)
+        compact_bytes += 2 * 2 * h_kv * m * d * elt          # K and V rows, read + write
+        topk_bytes += h_kv * n * (4 + 4) + n + 4 * h_kv * m  # a, s, modality in; idx out
+    return {"lse_pass": ("mfma", score_flops), "colsum_pass": ("mfma", score_flops),
+            "gram_max": ("mfma", gram_flops), "gather_compact": ("hbm", compact_bytes),
+            "psi_topk": ("hbm", topk_bytes)}
+
+
+def cpu_baseline(layers, spec):
+    """The oracle, as it stands, on one layer of the same workload."""
+    import numpy as np
+    import threadpoolctl
+
+    from oracle import omnimem_oracle as orc
+    lay = dict(layers[0])
+    for key in ("q", "k", "v"):
+        lay[key] = lay[key].astype(np.float64)
+    per_layer_budget = spec["total_budget"] // spec["n_layers"]
+    t0 = time.perf_counter()
+    orc.compression_step([lay], per_layer_budget)
+    dt = time.perf_counter() - t0
+    threads = max([x["num_threads"] for x in threadpoolctl.threadpool_info() if x["user_api"] == "blas"] or [1])
+    n = lay["k"].shape[1]
+    return {"value": n / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"one layer ({n} tokens) of the same workload through the whole numpy fp64 oracle step, "
+                      f"{dt:.1f} s wall; BLAS threads as cores (exp/sort single-threaded)"}
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the step is per layer and KV head; sharding is described in the design notes)",
+              file=sys.stderr)
+        sys.exit(1)
+    import numpy as np
+    import torch
+
+    from paper_2606_07577_amd import synth
+    from paper_2606_07577_amd.step import DeviceStep
+
+    spec = synth.WORKLOADS[args.workload]
+    layers = synth.make_workload(args.workload)
+    step = DeviceStep(layers, spec["total_budget"])
+    stream = torch.cuda.current_stream()
+    print(f"[bench] workload {args.workload}: inputs resident, warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step.run(stream)
+    torch.cuda.synchronize()
+
+    # Timed region: K whole steps, nothing else.
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        step.run(stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    tokens = sum(int(l["k"].shape[1]) for l in layers)
+    value = tokens / (ms / 1e3)
+    print(f"[bench] {ms:.4f} ms/step, {value:.4g} tokens/s", file=sys.stderr, flush=True)
+
+    # Same K steps again with per-kernel HIP events on the launch stream.
+    step.ctx.omnimem_profile(True)
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        step.run(stream)
+    torch.cuda.synchronize()
+    kernels = step.ctx.omnimem_profile_report()
+    step.ctx.omnimem_profile(False)
+    budgets = step.budgets.cpu().numpy()
+    work = algorithmic_work(layers, budgets)
+    dtype = layers[0]["dtype"]
+    per_kernel = {}
+    for name, (launches, total_ms) in kernels.items():
+        avg_ms = total_ms / max(launches, 1)
+        entry = {"avg_us": round(avg_ms * 1e3, 3), "launches": launches}
+        if name in work:
+            bound, units = work[name]
+            if bound == "mfma":
+                ach = units / (avg_ms / 1e3) / 1e12
+                entry.update(bound="mfma", achieved=ach, unit="TFLOP/s", frac=ach / PEAK_MFMA_TFLOPS[dtype])
+            else:
+                ach = units / (avg_ms / 1e3) / 1e9
+                entry.update(bound="hbm", achieved=ach, unit="GB/s", frac=ach / PEAK_HBM_GBS)
+        per_kernel[name] = entry
+    dominant = max((n for n in per_kernel if n in work), key=lambda n: per_kernel[n]["avg_us"])
+    dk = per_kernel[dominant]
+    peak = PEAK_MFMA_TFLOPS[dtype] if dk["bound"] == "mfma" else PEAK_HBM_GBS
+    roofline = {"bound": dk["bound"], "achieved": round(dk["achieved"], 3), "peak": peak, "unit": dk["unit"],
+                "frac": round(dk["frac"], 4), "traffic": None, "kernel": dominant,
+                "units_per_launch": work[dominant][1], "avg_launch_us": dk["avg_us"]}
+
+    def stage_frac(names, peak_units, scale):
+        t = sum(per_kernel[n]["avg_us"] for n in names if n in per_kernel) / 1e6
+        u = sum(work[n][1] for n in names)
+        return round(u / t / scale / peak_units, 4) if t > 0 else None
+
+    fractions = {
+        "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_max"], PEAK_MFMA_TFLOPS[dtype], 1e12),
+        "hbm_frac_topk_compact": stage_frac(["psi_topk", "gather_compact"], PEAK_HBM_GBS, 1e9),
+    }
+    base = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        base = cpu_baseline(layers, spec)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
+                   "kv_heads": spec["h_kv"], "head_dim": spec["d"],
+                   "cache": spec["n_cache_v"] + spec["n_cache_a"],
+                   "chunk": spec["n_frames"] * (spec["frame_v"] + spec["frame_a"]),
+                   "budget": spec["total_budget"]},
+        "roofline": roofline, "fractions": fractions, "kernels": per_kernel, "cpu_baseline": base,
+    }
+    print(json.dumps(out))
+    step.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,200 @@
+/*
+ * omnimem.h -- C ABI of the OmniMem per-chunk KV-cache compression step on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: OmniMem, "Perturbation-aware Memory Compression for Streaming
+ * Audio-Visual LLMs" (arXiv 2606.07577), Sec. 3.  After a chunk has been
+ * prefilled, each layer's working set is its retained visual and audio
+ * caches followed by the chunk's new KV pairs (Eq. 3).  The step
+ *
+ *   1. scores every working-set row by accumulated chunk attention (Eq. 6),
+ *   2. scores its redundancy by value-vector cosine similarity (Eq. 7),
+ *   3. derives per-layer and per-modality budgets from normalised attention
+ *      entropy and mean cosine (AVBA, Eqs. 9-14),
+ *   4. keeps the top-M rows per modality by psi = a^lambda (1 - s) (Eq. 8,
+ *      Eqs. 4-5) and compacts them into the next caches (Eq. 2).
+ *
+ * The four calls below are those four stages.  They are independent: a
+ * caller may supply its own a, s or budgets to any later stage.
+ *
+ * Conventions shared by every call
+ *  - All tensor pointers are DEVICE pointers owned by the caller, except the
+ *    `layers` descriptor array, which is a HOST array of cfg.n_layers
+ *    entries that is copied before the call returns.
+ *  - Every call validates its arguments on the host first; on failure it
+ *    returns a nonzero status, launches nothing and sets the text that
+ *    omnimem_last_error() returns.
+ *  - Work is enqueued asynchronously on `stream`; outputs are valid once the
+ *    stream has reached the call's end.  Calls on one context must not run
+ *    concurrently (one context per stream).
+ *  - No call allocates device memory after omnimem_create().
+ *  - Working-set layout of layer l, KV head g (Eq. 3): row j of k, v at
+ *    k + g*kv_head_stride + j*kv_row_stride (elements), head_dim contiguous
+ *    elements per row.  Rows 0 .. n_cache-1 are the retained caches, rows
+ *    n_cache .. n_cache+n_chunk-1 the chunk in time order.  modality[j] is 0
+ *    (visual) or 1 (audio) for every row.
+ *  - Query head h reads KV head h / (n_q_heads / n_kv_heads) (grouped-query
+ *    attention).  Chunk query i of head h is at q + h*q_head_stride +
+ *    i*q_row_stride.
+ *  - Per-token outputs a, s and idx are [n_layers][n_kv_heads][max_tokens]
+ *    row-major; entries past layer l's N = n_cache + n_chunk are untouched.
+ *  - Scores, statistics and log-sum-exp values are always fp32.
+ */
+#ifndef OMNIMEM_H
+#define OMNIMEM_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OMNIMEM_OK = 0,
+  OMNIMEM_ERR_INVALID_ARG = 1,  /* null pointer, bad size, bad stride, overlap  */
+  OMNIMEM_ERR_UNSUPPORTED = 2,  /* head_dim other than 64 or 128, dtype, ...    */
+  OMNIMEM_ERR_INFEASIBLE = 3,   /* per-layer minimum budgets exceed the total   */
+  OMNIMEM_ERR_CAPACITY = 4,     /* sizes beyond those given to omnimem_create   */
+  OMNIMEM_ERR_HIP = 5           /* a HIP runtime error (text in last_error)     */
+} omnimem_status;
+
+typedef enum { OMNIMEM_BF16 = 0, OMNIMEM_F32 = 1 } omnimem_dtype;
+
+/* Redundancy source of Eq. (7).  SIM_MAX: s_k = max cosine between row k
+ * and any other row of the same (layer, KV head, modality).  SIM_ADJ: the
+ * mean cosine with the previous and next row of the same modality (Eq. 7
+ * as printed; one neighbour at either end, 0 for a lone row). */
+typedef enum { OMNIMEM_SIM_MAX = 0, OMNIMEM_SIM_ADJ = 1 } omnimem_sim;
+
+typedef struct {
+  int32_t n_layers;      /* L                                                 */
+  int32_t n_q_heads;     /* H_q                                               */
+  int32_t n_kv_heads;    /* H_kv; must divide H_q                              */
+  int32_t head_dim;      /* d: 64 or 128                                       */
+  int32_t dtype;         /* omnimem_dtype of q, k, v, k_out, v_out             */
+  float lambda;          /* Eq. (8) exponent; paper default 0.02 (Sec. 4.3)    */
+  float ratio_r;         /* Eqs. (11)-(12) prior visual:audio ratio; 5         */
+  float temperature;     /* Eq. (14) T; 0.2                                    */
+  float b_min_frac;      /* per-layer budget >= ceil(b_min_frac*B_tot/L)       */
+  float b_max_frac;      /* per-layer budget <= floor(b_max_frac*B_tot/L)      */
+  int32_t causal;        /* 1: chunk row n_cache+t is visible to query i iff t <= i */
+  int32_t sim;           /* omnimem_sim                                        */
+  int32_t sim_on_keys;   /* 0: cosine of values (Sec. 3.1), 1: of keys         */
+  int64_t max_tokens;    /* capacity: largest N = n_cache + n_chunk of a layer */
+  int64_t max_chunk;     /* capacity: largest n_chunk of a layer               */
+} omnimem_config;
+
+typedef struct {
+  const void* q;            /* [H_q][n_chunk][d] chunk queries                */
+  int64_t q_head_stride;    /* elements between query heads                   */
+  int64_t q_row_stride;     /* elements between chunk queries                 */
+  const void* k;            /* [H_kv][N][d] working-set keys (Eq. 3)           */
+  const void* v;            /* [H_kv][N][d] working-set values                 */
+  int64_t kv_head_stride;   /* elements, shared by k and v                    */
+  int64_t kv_row_stride;    /* elements, shared by k and v                    */
+  const uint8_t* modality;  /* [N]: 0 visual, 1 audio                         */
+  int64_t n_cache;          /* retained rows at the front of the working set  */
+  int64_t n_chunk;          /* chunk rows (and chunk queries) at the back     */
+  float sm_scale;           /* softmax scale of Eq. (1); 0 -> 1/sqrt(d)        */
+  const float* lse;         /* optional [H_q][n_chunk] fp32 log-sum-exp of the
+                               chunk attention rows (e.g. from the prefill);
+                               NULL -> computed by omnimem_score               */
+  void* k_out;              /* [H_kv][M_l][d] next keys   (select_compact)    */
+  void* v_out;              /* [H_kv][M_l][d] next values (select_compact)    */
+  int64_t out_head_stride;  /* elements, shared by k_out and v_out            */
+  int64_t out_row_stride;   /* elements, shared by k_out and v_out            */
+} omnimem_layer;
+
+typedef struct omnimem_ctx omnimem_ctx;
+
+/* Fill *cfg with the paper's defaults (lambda 0.02, r 5, T 0.2; Sec. 3.2 and
+ * Sec. 4.3), b_min_frac 0.5, b_max_frac 2, causal, SIM_MAX on values, bf16.
+ * Sizes are left 0. */
+void omnimem_config_default(omnimem_config* cfg);
+
+/* Create a context on the current HIP device.  Allocates every workspace
+ * buffer for cfg's capacities.  On success *out owns them until
+ * omnimem_destroy.  Errors: INVALID_ARG (null, nonpositive sizes, H_kv not
+ * dividing H_q), UNSUPPORTED (head_dim, dtype), HIP (allocation failed). */
+omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out);
+
+/* Wait for the context's outstanding work, free its workspace and the
+ * context.  NULL is accepted. */
+omnimem_status omnimem_destroy(omnimem_ctx* ctx);
+
+/* Text of the last error on this context ("" if none).  Valid until the next
+ * call on the context.  ctx NULL -> text of the last failed omnimem_create. */
+const char* omnimem_last_error(const omnimem_ctx* ctx);
+
+/* Eq. (6): a[l][g][j] = sum over query heads h of KV head g and chunk queries
+ * i of A_{h,i,j}, A the softmax over visible rows of sm_scale <q_{h,i}, k_{g,j}>
+ * (Eq. 1: one softmax over both caches and the chunk).  Each layer's lse is
+ * taken from the descriptor when given, else computed.
+ *   a       [L][H_kv][max_tokens] fp32, written for j < N_l.
+ *   lse_out optional [L][H_q][max_chunk] fp32: the log-sum-exp per chunk query
+ *           that was used (copied from the descriptor when given).  */
+omnimem_status omnimem_score(omnimem_ctx* ctx, const omnimem_layer* layers, float* a,
+                             float* lse_out, hipStream_t stream);
+
+/* Eq. (7): s[l][g][j] = redundancy of row j among the rows of its modality
+ * in KV head g, from cfg.sim and cfg.sim_on_keys.  Cosine similarity is 0
+ * when either vector is zero and is clamped to [-1, 1]; a modality with a
+ * single row gives s = 0.
+ *   s [L][H_kv][max_tokens] fp32, written for j < N_l. */
+omnimem_status omnimem_redundancy(omnimem_ctx* ctx, const omnimem_layer* layers, float* s,
+                                  hipStream_t stream);
+
+/* AVBA, Eqs. (9)-(14): per layer, normalised attention entropy per KV head
+ * (averaged over heads) and mean redundancy over visual rows, audio rows and
+ * all rows give C_v, C_a (Eqs. 9-10) and C^(l) (Eq. 13, normalised by ln N).
+ * Layer shares x_l = clamp(kappa*B_tot*softmax(C/T)_l, lo_l, hi_l) with the
+ * kappa making sum x_l = B_tot, lo_l = min(ceil(b_min_frac*B_tot/L), N_l),
+ * hi_l = min(floor(b_max_frac*B_tot/L), N_l) (every layer keeps hi_l when
+ * sum hi_l <= B_tot).  Integer B_l by largest remainder (ties to the lower
+ * layer).  M_v = clamp(floor(w_v*B_l + 1/2), max(0, B_l - K_a), min(K_v, B_l))
+ * with w_v from Eq. (11), M_a = B_l - M_v.  Computed in fp64 on the device.
+ *   a, s     [L][H_kv][max_tokens] fp32 inputs.
+ *   budgets  [L][2] int32 output (M_v, M_a).
+ *   stats    optional [L][10] fp32 output: Hn_v, Hn_a, Hn_l, sbar_v, sbar_a,
+ *            sbar_l, C_v, C_a, C_l, w_v.
+ * Errors: INFEASIBLE when sum_l lo_l > total_budget (checked on the host). */
+omnimem_status omnimem_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a,
+                                const float* s, int64_t total_budget, int32_t* budgets,
+                                float* stats, hipStream_t stream);
+
+/* Eqs. (4)-(5), (8): per (layer, KV head, modality) keep the M rows with the
+ * largest psi = a^lambda (1 - s) (0^lambda = 0; ties to the lower row), in
+ * ascending row order, visual block first; then k_out[g][i] = k[g][idx[g][i]]
+ * and the same for v, for i < M_v + M_a.  The next step's modality mask is
+ * M_v zeros followed by M_a ones.
+ *   a, s     [L][H_kv][max_tokens] fp32; budgets [L][2] int32 (device).
+ *   idx      optional [L][H_kv][max_tokens] int32 output of the kept rows.
+ * k_out / v_out must not overlap k / v (ping-pong the cache buffers); the
+ * caller sizes them for the budgets it passes.  Budgets are read on the
+ * device and clamped to [0, K_mu]. */
+omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* layers,
+                                      const float* a, const float* s, const int32_t* budgets,
+                                      int32_t* idx, hipStream_t stream);
+
+/* Kernel timing for measurement.  While on, every kernel the context
+ * launches is bracketed by two HIP events recorded on its launch stream
+ * (up to 16384 launches are kept; later ones are not recorded). */
+omnimem_status omnimem_profile(omnimem_ctx* ctx, int32_t on);
+
+typedef struct {
+  char name[32];       /* kernel name                                       */
+  int32_t launches;    /* recorded launches                                 */
+  double total_ms;     /* summed event-to-event time of those launches      */
+} omnimem_kernel_time;
+
+/* Wait for the recorded launches, write up to `capacity` per-kernel totals
+ * (in first-launch order) and their number to *count, and clear the record. */
+omnimem_status omnimem_profile_report(omnimem_ctx* ctx, omnimem_kernel_time* out, int32_t capacity,
+                                      int32_t* count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OMNIMEM_H */

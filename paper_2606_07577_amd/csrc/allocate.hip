@@ -1,0 +1,216 @@
+// Audio-Visual Budget Allocation (AVBA, Sec. 3.2 of the OmniMem paper).
+//
+//  avba_partials  per (layer, KV head): fp64 sums over visual and audio
+//                 rows of a, a ln a and s (the inputs of Eqs. 9, 10, 13).
+//  avba_allocate  one workgroup: normalised entropies and mean cosines,
+//                 compressibilities C_v, C_a, C^(l), the split w_v (Eq. 11),
+//                 layer shares B_tot softmax(C^(l)/T) (Eq. 14) clamped to
+//                 [B_min, B_max] with the sum kept (water-filling on the
+//                 scale kappa), largest-remainder integer budgets and the
+//                 per-modality split.  All in fp64.
+#include "common.h"
+
+namespace omnimem {
+
+namespace {
+
+constexpr int kStatSets = 2;  // visual, audio (the layer set is their union)
+
+__device__ inline double block_sum(double v, double* scratch) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) scratch[wave] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += scratch[w];
+  return t;
+}
+
+// stat_part[l][g][set][0..3] = {sum a, sum a ln a, sum s, count}
+__global__ __launch_bounds__(256) void avba_partials(const LayerDesc* __restrict__ layers, Dims dm,
+                                                     const float* __restrict__ a, const float* __restrict__ s,
+                                                     double* __restrict__ part) {
+  const int l = blockIdx.y, g = blockIdx.x;
+  const LayerDesc Ld = layers[l];
+  const int N = Ld.n;
+  const float* ag = a + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
+  const float* sg = s + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
+  double acc[kStatSets][4] = {};
+  for (int j = threadIdx.x; j < N; j += blockDim.x) {
+    const int mu = Ld.mod[j] ? 1 : 0;
+    const double x = ag[j];
+    acc[mu][0] += x;
+    acc[mu][1] += x > 0.0 ? x * log(x) : 0.0;
+    acc[mu][2] += sg[j];
+    acc[mu][3] += 1.0;
+  }
+  __shared__ double scratch[16];
+  double* out = part + (((int64_t)l * dm.Hkv + g) * kStatSets) * 4;
+  for (int mu = 0; mu < kStatSets; ++mu)
+    for (int q = 0; q < 4; ++q) {
+      const double t = block_sum(acc[mu][q], scratch);
+      if (threadIdx.x == 0) out[mu * 4 + q] = t;
+    }
+}
+
+// Normalised entropy of x / sum x over K entries from sum x and sum x ln x:
+// H = ln S - (sum x ln x) / S, divided by ln K; 0 when K <= 1 or S == 0.
+__device__ inline double norm_entropy(double sum, double xlogx, double count) {
+  if (count <= 1.0 || sum <= 0.0) return 0.0;
+  return (log(sum) - xlogx / sum) / log(count);
+}
+
+constexpr int kMaxLayers = 1024;
+
+__global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict__ layers, Dims dm,
+                                                     const double* __restrict__ part, int64_t total,
+                                                     float ratio_r, float temperature, float bmin_frac,
+                                                     float bmax_frac, int32_t* __restrict__ budgets,
+                                                     float* __restrict__ stats) {
+  __shared__ double c_l[kMaxLayers], w_v[kMaxLayers], p[kMaxLayers], x[kMaxLayers];
+  __shared__ int n_l[kMaxLayers], k_v[kMaxLayers], lo[kMaxLayers], hi[kMaxLayers], b_l[kMaxLayers];
+  __shared__ double s_kappa;
+  const int L = dm.L;
+  const double B = (double)total;
+  const double T = (double)temperature;
+  const double r = (double)ratio_r;
+
+  // --- per-layer statistics (Eqs. 9, 10, 13) ---
+  for (int l = threadIdx.x; l < L; l += blockDim.x) {
+    double hv = 0.0, ha = 0.0, hl = 0.0, sv = 0.0, sa = 0.0, cnt_v = 0.0, cnt_a = 0.0;
+    for (int g = 0; g < dm.Hkv; ++g) {
+      const double* P = part + (((int64_t)l * dm.Hkv + g) * kStatSets) * 4;
+      hv += norm_entropy(P[0], P[1], P[3]);
+      ha += norm_entropy(P[4], P[5], P[7]);
+      hl += norm_entropy(P[0] + P[4], P[1] + P[5], P[3] + P[7]);
+      sv += P[2];
+      sa += P[6];
+      cnt_v = P[3];
+      cnt_a = P[7];
+    }
+    hv /= dm.Hkv; ha /= dm.Hkv; hl /= dm.Hkv;
+    const double sbar_v = cnt_v > 0.0 ? sv / (dm.Hkv * cnt_v) : 0.0;
+    const double sbar_a = cnt_a > 0.0 ? sa / (dm.Hkv * cnt_a) : 0.0;
+    const double sbar_l = (cnt_v + cnt_a) > 0.0 ? (sv + sa) / (dm.Hkv * (cnt_v + cnt_a)) : 0.0;
+    const double cv = hv * (1.0 - sbar_v), ca = ha * (1.0 - sbar_a), cl = hl * (1.0 - sbar_l);
+    const double den = cv * r + ca;
+    const double wv = den > 0.0 ? cv * r / den : r / (r + 1.0);
+    c_l[l] = cl;
+    w_v[l] = wv;
+    n_l[l] = layers[l].n;
+    k_v[l] = (int)cnt_v;
+    if (stats) {
+      float* o = stats + (int64_t)l * 10;
+      o[0] = (float)hv; o[1] = (float)ha; o[2] = (float)hl;
+      o[3] = (float)sbar_v; o[4] = (float)sbar_a; o[5] = (float)sbar_l;
+      o[6] = (float)cv; o[7] = (float)ca; o[8] = (float)cl; o[9] = (float)wv;
+    }
+  }
+  __syncthreads();
+
+  // --- Eq. (14): softmax over layers of C / T, bounds ---
+  if (threadIdx.x == 0) {
+    double mx = -INFINITY;
+    for (int l = 0; l < L; ++l) mx = fmax(mx, c_l[l] / T);
+    double sum = 0.0;
+    for (int l = 0; l < L; ++l) { p[l] = exp(c_l[l] / T - mx); sum += p[l]; }
+    for (int l = 0; l < L; ++l) p[l] /= sum;
+  }
+  const int lo_base = (int)ceil(((double)bmin_frac * B) / L);
+  const int hi_base = (int)floor(((double)bmax_frac * B) / L);
+  for (int l = threadIdx.x; l < L; l += blockDim.x) {
+    lo[l] = min(lo_base, n_l[l]);
+    hi[l] = min(hi_base, n_l[l]);
+  }
+  __syncthreads();
+  double sum_hi = 0.0;
+  for (int l = 0; l < L; ++l) sum_hi += hi[l];
+
+  if (sum_hi <= B) {
+    for (int l = threadIdx.x; l < L; l += blockDim.x) { x[l] = hi[l]; b_l[l] = hi[l]; }
+    __syncthreads();
+  } else {
+    // --- water-fill: kappa with sum_l clamp(kappa B p_l, lo_l, hi_l) = B ---
+    // Breakpoints kappa = lo_l / (B p_l) and hi_l / (B p_l); f is linear in
+    // between.  Thread 0 walks the sorted breakpoints (2L values).
+    if (threadIdx.x == 0) {
+      auto f = [&](double kap) {
+        double t = 0.0;
+        for (int l = 0; l < L; ++l) t += fmin(fmax(kap * B * p[l], (double)lo[l]), (double)hi[l]);
+        return t;
+      };
+      // walk the distinct breakpoints in increasing order
+      double prev_k = 0.0, prev_f = 0.0, kap = 0.0, last = -INFINITY;
+      bool have_prev = false;
+      for (;;) {
+        double kb = INFINITY;  // smallest breakpoint above `last`
+        for (int l = 0; l < L; ++l) {
+          if (!(p[l] > 0.0)) continue;
+          const double c0 = lo[l] / (B * p[l]), c1 = hi[l] / (B * p[l]);
+          if (c0 > last && c0 < kb) kb = c0;
+          if (c1 > last && c1 < kb) kb = c1;
+        }
+        if (kb == INFINITY) break;
+        const double fk = f(kb);
+        if (fk >= B) {
+          kap = have_prev ? prev_k + (B - prev_f) * (kb - prev_k) / (fk - prev_f) : kb;
+          break;
+        }
+        prev_k = kb;
+        prev_f = fk;
+        have_prev = true;
+        last = kb;
+      }
+      s_kappa = kap;
+    }
+    __syncthreads();
+    const double kap = s_kappa;
+    for (int l = threadIdx.x; l < L; l += blockDim.x) {
+      x[l] = fmin(fmax(kap * B * p[l], (double)lo[l]), (double)hi[l]);
+      b_l[l] = (int)floor(x[l]);
+    }
+    __syncthreads();
+    // --- largest remainder: leftover units to the largest fractional parts
+    // among layers below their upper bound, ties to the lower layer ---
+    double fl_sum = 0.0;
+    for (int l = 0; l < L; ++l) fl_sum += b_l[l];
+    const int leftover = (int)(B - fl_sum);
+    __syncthreads();
+    for (int l = threadIdx.x; l < L; l += blockDim.x) {
+      if (b_l[l] >= hi[l]) continue;
+      const double fr = x[l] - floor(x[l]);
+      int rank = 0;
+      for (int m = 0; m < L; ++m) {
+        if (m == l || floor(x[m]) >= hi[m]) continue;
+        const double fm = x[m] - floor(x[m]);
+        if (fm > fr || (fm == fr && m < l)) ++rank;
+      }
+      if (rank < leftover) b_l[l] += 1;
+    }
+    __syncthreads();
+  }
+
+  // --- per-modality split (Eqs. 11-12) ---
+  for (int l = threadIdx.x; l < L; l += blockDim.x) {
+    const int bl = b_l[l];
+    const int kv = k_v[l], ka = n_l[l] - k_v[l];
+    int mv = (int)floor(w_v[l] * bl + 0.5);
+    mv = min(max(mv, max(0, bl - ka)), min(kv, bl));
+    budgets[2 * l] = mv;
+    budgets[2 * l + 1] = bl - mv;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
+                           const float* s, int64_t total, float ratio_r, float temperature, float bmin_frac,
+                           float bmax_frac, int32_t* budgets, float* stats, hipStream_t st) {
+  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st, avba_partials<<<dim3(dm.Hkv, dm.L), 256, 0, st>>>(desc, dm, a, s, ws.stat_part));
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, total, ratio_r,
+                                   temperature, bmin_frac, bmax_frac, budgets, stats));
+  return hipGetLastError();
+}
+
+}  // namespace omnimem

@@ -1,0 +1,448 @@
+// Host side of the C ABI in include/omnimem.h: argument validation,
+// workspace ownership, descriptor upload and the launch sequence of each
+// stage.  No device memory is allocated after omnimem_create.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/omnimem.h"
+#include "common.h"
+
+using namespace omnimem;
+
+namespace {
+
+constexpr int kSlots = 16;        // descriptor ring depth
+constexpr int kProfEvents = 2 * 16384;
+constexpr int kMaxLayers = 1024;  // bound of the allocation kernel's tables
+
+std::string g_create_error;
+
+}  // namespace
+
+namespace omnimem {
+// Launch timing: an event pool and the (kernel, begin event) of each launch.
+struct Profiler {
+  std::vector<hipEvent_t> pool;
+  int used = 0;
+  std::vector<int> kernel;   // per recorded launch
+  std::vector<int> first;    // index of its begin event; end event is first + 1
+  bool open = false;
+};
+
+void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
+  if (begin) {
+    if (p->used + 2 > (int)p->pool.size()) return;
+    if (hipEventRecord(p->pool[p->used], st) != hipSuccess) return;
+    p->kernel.push_back(kid);
+    p->first.push_back(p->used);
+    p->used += 2;
+    p->open = true;
+  } else if (p->open) {
+    (void)hipEventRecord(p->pool[p->first.back() + 1], st);
+    p->open = false;
+  }
+}
+}  // namespace omnimem
+
+static const char* kKernelNames[K_COUNT] = {
+    "lse_pass", "colsum_pass", "head_sum", "modality_lists", "gram_plan", "inv_norms", "fill_int",
+    "gram_max", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact"};
+
+struct omnimem_ctx {
+  omnimem_config cfg;
+  Dims dm;
+  int device = 0;
+  Workspace ws{};
+  LayerDesc* pinned = nullptr;          // host ring [kSlots][L]
+  hipEvent_t ev[kSlots] = {};
+  bool ev_used[kSlots] = {};
+  int next_slot = 0;
+  int last_slot = -1;                   // slot holding the last uploaded table
+  std::vector<LayerDesc> last_table;
+  std::string err;
+  std::vector<void*> allocations;
+  Profiler prof;
+};
+
+namespace {
+
+omnimem_status fail(omnimem_ctx* ctx, omnimem_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (ctx) ctx->err = buf; else g_create_error = buf;
+  return st;
+}
+
+omnimem_status hip_fail(omnimem_ctx* ctx, hipError_t e, const char* where) {
+  return fail(ctx, OMNIMEM_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+size_t elt_size(const omnimem_config& c) { return c.dtype == OMNIMEM_BF16 ? 2 : 4; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Byte range [lo, hi) covered by a [heads][rows][d] strided tensor.
+void extent(const void* base, int64_t heads, int64_t rows, int64_t hs, int64_t rs, int64_t d, size_t esz,
+            uintptr_t* lo, uintptr_t* hi) {
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+  const int64_t last = (heads - 1) * hs + (rows - 1) * rs + d;
+  *lo = b;
+  *hi = b + (uintptr_t)(last * (int64_t)esz);
+}
+
+bool overlaps(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a0 < b1 && b0 < a1; }
+
+enum Need { NEED_Q = 1, NEED_K = 2, NEED_V = 4, NEED_OUT = 8 };
+
+omnimem_status validate(omnimem_ctx* ctx, const omnimem_layer* layers, int need) {
+  if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
+  if (!layers) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null layer array");
+  const omnimem_config& c = ctx->cfg;
+  const int64_t d = c.head_dim;
+  const size_t esz = elt_size(c);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const omnimem_layer& L = layers[l];
+    const int64_t n = L.n_cache + L.n_chunk;
+    if (L.n_cache < 0 || L.n_chunk < 0 || n < 1)
+      return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: need n_cache >= 0, n_chunk >= 0, N >= 1", l);
+    if (n > c.max_tokens || L.n_chunk > c.max_chunk)
+      return fail(ctx, OMNIMEM_ERR_CAPACITY, "layer %d: N=%lld or n_chunk=%lld beyond the context's capacity", l,
+                  (long long)n, (long long)L.n_chunk);
+    if (!L.modality) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: null modality", l);
+    if (!std::isfinite(L.sm_scale)) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: sm_scale not finite", l);
+    if ((need & NEED_Q)) {
+      if (!L.q) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: null q", l);
+      if (!aligned16(L.q) || L.q_row_stride < d || L.q_head_stride < 0 || (L.q_row_stride * esz) % 16 ||
+          (L.q_head_stride * esz) % 16)
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: q must be 16-byte aligned with row stride >= d and "
+                    "strides of whole 16-byte units", l);
+      if (L.lse && (reinterpret_cast<uintptr_t>(L.lse) & 3u))
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: lse not 4-byte aligned", l);
+    }
+    const bool need_k = need & NEED_K, need_v = need & NEED_V;
+    if ((need_k && !L.k) || (need_v && !L.v)) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: null k or v", l);
+    if (need_k || need_v) {
+      if ((L.k && !aligned16(L.k)) || (L.v && !aligned16(L.v)) || L.kv_row_stride < d || L.kv_head_stride < 0 ||
+          (L.kv_row_stride * esz) % 16 || (L.kv_head_stride * esz) % 16)
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k/v must be 16-byte aligned with row stride >= d and "
+                    "strides of whole 16-byte units", l);
+    }
+    if (need & NEED_OUT) {
+      if (!L.k_out || !L.v_out) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: null k_out or v_out", l);
+      if (!aligned16(L.k_out) || !aligned16(L.v_out) || (L.out_row_stride * esz) % 16 ||
+          (L.out_head_stride * esz) % 16)
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: outputs must be 16-byte aligned, strides of whole "
+                    "16-byte units", l);
+      const int64_t H = c.n_kv_heads;
+      const bool head_major = L.out_row_stride >= d && (H == 1 || L.out_head_stride >= n * L.out_row_stride);
+      const bool row_major = L.out_head_stride >= d && L.out_row_stride >= H * L.out_head_stride;
+      if (!head_major && !row_major)
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k_out/v_out must hold H_kv x N rows of d without "
+                    "overlap", l);
+      uintptr_t k0, k1, v0, v1, o0, o1, p0, p1;
+      extent(L.k, H, n, L.kv_head_stride, L.kv_row_stride, d, esz, &k0, &k1);
+      extent(L.v, H, n, L.kv_head_stride, L.kv_row_stride, d, esz, &v0, &v1);
+      extent(L.k_out, H, n, L.out_head_stride, L.out_row_stride, d, esz, &o0, &o1);
+      extent(L.v_out, H, n, L.out_head_stride, L.out_row_stride, d, esz, &p0, &p1);
+      if (overlaps(o0, o1, k0, k1) || overlaps(o0, o1, v0, v1) || overlaps(p0, p1, k0, k1) ||
+          overlaps(p0, p1, v0, v1) || overlaps(o0, o1, p0, p1))
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k_out/v_out overlap k, v or each other", l);
+    }
+  }
+  return OMNIMEM_OK;
+}
+
+// Copy the descriptor table to the device unless it equals the last one.
+omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t st, const LayerDesc** dev) {
+  const int L = ctx->cfg.n_layers;
+  const double log2e = 1.4426950408889634;
+  std::vector<LayerDesc> t(L);
+  for (int l = 0; l < L; ++l) {
+    const omnimem_layer& s = layers[l];
+    LayerDesc& x = t[l];
+    std::memset(&x, 0, sizeof x);
+    x.q = s.q; x.k = s.k; x.v = s.v; x.mod = s.modality; x.lse_in = s.lse;
+    x.k_out = s.k_out; x.v_out = s.v_out;
+    x.q_hs = s.q_head_stride; x.q_rs = s.q_row_stride;
+    x.kv_hs = s.kv_head_stride; x.kv_rs = s.kv_row_stride;
+    x.out_hs = s.out_head_stride; x.out_rs = s.out_row_stride;
+    x.n_cache = (int32_t)s.n_cache; x.n_chunk = (int32_t)s.n_chunk; x.n = (int32_t)(s.n_cache + s.n_chunk);
+    const double scale = s.sm_scale != 0.0f ? (double)s.sm_scale : 1.0 / std::sqrt((double)ctx->cfg.head_dim);
+    x.scale_log2 = (float)(scale * log2e);
+  }
+  if (ctx->last_slot >= 0 && ctx->last_table.size() == t.size() &&
+      std::memcmp(ctx->last_table.data(), t.data(), sizeof(LayerDesc) * L) == 0) {
+    *dev = ctx->ws.desc + (size_t)ctx->last_slot * L;
+    return OMNIMEM_OK;
+  }
+  const int slot = ctx->next_slot;
+  if (ctx->ev_used[slot]) {
+    hipError_t e = hipEventSynchronize(ctx->ev[slot]);
+    if (e != hipSuccess) return hip_fail(ctx, e, "descriptor ring wait");
+  }
+  LayerDesc* host = ctx->pinned + (size_t)slot * L;
+  std::memcpy(host, t.data(), sizeof(LayerDesc) * L);
+  LayerDesc* d = ctx->ws.desc + (size_t)slot * L;
+  hipError_t e = hipMemcpyAsync(d, host, sizeof(LayerDesc) * L, hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return hip_fail(ctx, e, "descriptor upload");
+  ctx->last_slot = slot;
+  ctx->last_table = t;
+  ctx->next_slot = (slot + 1) % kSlots;
+  *dev = d;
+  return OMNIMEM_OK;
+}
+
+// Mark the slot in use by this call's work.
+omnimem_status finish(omnimem_ctx* ctx, hipError_t launch_err, hipStream_t st, const char* what) {
+  if (launch_err != hipSuccess) return hip_fail(ctx, launch_err, what);
+  const int slot = ctx->last_slot;
+  hipError_t e = hipEventRecord(ctx->ev[slot], st);
+  if (e != hipSuccess) return hip_fail(ctx, e, "event record");
+  ctx->ev_used[slot] = true;
+  ctx->err.clear();
+  return OMNIMEM_OK;
+}
+
+omnimem_status set_device(omnimem_ctx* ctx) {
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  e = hipGetLastError();  // an earlier asynchronous fault surfaces here
+  if (e != hipSuccess) return hip_fail(ctx, e, "earlier device error");
+  return OMNIMEM_OK;
+}
+
+template <typename T>
+hipError_t dalloc(omnimem_ctx* ctx, T** p, size_t count) {
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, std::max<size_t>(count * sizeof(T), 256));
+  if (e == hipSuccess) ctx->allocations.push_back(q);
+  *p = static_cast<T*>(q);
+  return e;
+}
+
+int64_t plan_F(int64_t n) {
+  const int64_t q = n / kGramStrip, r = n % kGramStrip;
+  return kGramStrip * q * (q + 1) / 2 + r * (q + 1);
+}
+
+}  // namespace
+
+extern "C" {
+
+void omnimem_config_default(omnimem_config* c) {
+  if (!c) return;
+  std::memset(c, 0, sizeof *c);
+  c->dtype = OMNIMEM_BF16;
+  c->lambda = 0.02f;
+  c->ratio_r = 5.0f;
+  c->temperature = 0.2f;
+  c->b_min_frac = 0.5f;
+  c->b_max_frac = 2.0f;
+  c->causal = 1;
+  c->sim = OMNIMEM_SIM_MAX;
+  c->sim_on_keys = 0;
+}
+
+omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
+  if (!cfg || !out) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  const omnimem_config& c = *cfg;
+  if (c.n_layers < 1 || c.n_layers > kMaxLayers || c.n_q_heads < 1 || c.n_kv_heads < 1 ||
+      c.n_q_heads % c.n_kv_heads != 0 || c.max_tokens < 1 || c.max_chunk < 0 || c.max_chunk > c.max_tokens ||
+      c.max_tokens > (int64_t)1 << 30)
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "bad sizes: need 1 <= n_layers <= %d, H_kv | H_q, "
+                "0 <= max_chunk <= max_tokens <= 2^30", kMaxLayers);
+  if (c.head_dim != 64 && c.head_dim != 128)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "head_dim %d: supported 64 and 128", c.head_dim);
+  if (c.dtype != OMNIMEM_BF16 && c.dtype != OMNIMEM_F32)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "dtype %d", c.dtype);
+  if (c.sim != OMNIMEM_SIM_MAX && c.sim != OMNIMEM_SIM_ADJ)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "sim %d", c.sim);
+  if (!std::isfinite(c.lambda) || c.lambda < 0.0f || !(c.ratio_r > 0.0f) || !(c.temperature > 0.0f) ||
+      !(c.b_min_frac >= 0.0f) || !(c.b_max_frac >= c.b_min_frac) || !std::isfinite(c.b_max_frac))
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "need lambda >= 0, r > 0, T > 0, 0 <= b_min_frac <= b_max_frac");
+
+  omnimem_ctx* ctx = new omnimem_ctx();
+  ctx->cfg = c;
+  hipError_t e = hipGetDevice(&ctx->device);
+  if (e != hipSuccess) { delete ctx; return fail(nullptr, OMNIMEM_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e)); }
+  Dims& dm = ctx->dm;
+  dm.L = c.n_layers; dm.Hq = c.n_q_heads; dm.Hkv = c.n_kv_heads; dm.G = c.n_q_heads / c.n_kv_heads;
+  dm.d = c.head_dim; dm.max_tokens = c.max_tokens; dm.max_chunk = std::max<int64_t>(c.max_chunk, 1);
+  dm.causal = c.causal ? 1 : 0;
+  const size_t L = c.n_layers, Hq = c.n_q_heads, Hkv = c.n_kv_heads, T = c.max_tokens, Cm = dm.max_chunk;
+  const int64_t tblocks = (c.max_tokens + kGramTile - 1) / kGramTile;
+  Workspace& ws = ctx->ws;
+  ws.items_cap = (int64_t)L * Hkv * plan_F(tblocks + 1);
+  if ((e = dalloc(ctx, &ws.desc, (size_t)kSlots * L)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.lse, L * Hq * Cm)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.part, L * Hq * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.pos, L * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.rank, L * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.counts, L * 2)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.inv_norm, L * Hkv * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.best, L * Hkv * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.items, (size_t)ws.items_cap)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.n_items, 1)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.stat_part, L * Hkv * 2 * 4)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.idx, L * Hkv * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.keys, L * Hkv * T)) != hipSuccess) {
+    omnimem_destroy(ctx);
+    return fail(nullptr, OMNIMEM_ERR_HIP, "workspace allocation: %s", hipGetErrorString(e));
+  }
+  void* pinned = nullptr;
+  if ((e = hipHostMalloc(&pinned, sizeof(LayerDesc) * kSlots * L, hipHostMallocDefault)) != hipSuccess) {
+    omnimem_destroy(ctx);
+    return fail(nullptr, OMNIMEM_ERR_HIP, "pinned descriptor ring: %s", hipGetErrorString(e));
+  }
+  ctx->pinned = static_cast<LayerDesc*>(pinned);
+  for (int i = 0; i < kSlots; ++i) {
+    if ((e = hipEventCreateWithFlags(&ctx->ev[i], hipEventDisableTiming)) != hipSuccess) {
+      omnimem_destroy(ctx);
+      return fail(nullptr, OMNIMEM_ERR_HIP, "event: %s", hipGetErrorString(e));
+    }
+  }
+  *out = ctx;
+  return OMNIMEM_OK;
+}
+
+omnimem_status omnimem_destroy(omnimem_ctx* ctx) {
+  if (!ctx) return OMNIMEM_OK;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  for (void* p : ctx->allocations) (void)hipFree(p);
+  if (ctx->pinned) (void)hipHostFree(ctx->pinned);
+  for (int i = 0; i < kSlots; ++i)
+    if (ctx->ev[i]) (void)hipEventDestroy(ctx->ev[i]);
+  for (hipEvent_t e : ctx->prof.pool) (void)hipEventDestroy(e);
+  delete ctx;
+  return OMNIMEM_OK;
+}
+
+const char* omnimem_last_error(const omnimem_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+omnimem_status omnimem_score(omnimem_ctx* ctx, const omnimem_layer* layers, float* a, float* lse_out,
+                             hipStream_t stream) {
+  omnimem_status st = validate(ctx, layers, NEED_Q | NEED_K);
+  if (st != OMNIMEM_OK) return st;
+  if (!a) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a");
+  if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
+  const LayerDesc* dev = nullptr;
+  if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
+  float* lse_buf = lse_out ? lse_out : ctx->ws.lse;
+  return finish(ctx, launch_score(ctx->dm, ctx->cfg.dtype, dev, ctx->ws, lse_buf, a, 1, stream), stream,
+                "omnimem_score launch");
+}
+
+omnimem_status omnimem_redundancy(omnimem_ctx* ctx, const omnimem_layer* layers, float* s, hipStream_t stream) {
+  if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
+  omnimem_status st = validate(ctx, layers, ctx->cfg.sim_on_keys ? NEED_K : NEED_V);
+  if (st != OMNIMEM_OK) return st;
+  if (!s) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null s");
+  if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
+  const LayerDesc* dev = nullptr;
+  if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
+  return finish(ctx, launch_redundancy(ctx->dm, ctx->cfg.dtype, ctx->cfg.sim, ctx->cfg.sim_on_keys, dev, ctx->ws,
+                                       s, stream),
+                stream, "omnimem_redundancy launch");
+}
+
+omnimem_status omnimem_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,
+                                int64_t total_budget, int32_t* budgets, float* stats, hipStream_t stream) {
+  omnimem_status st = validate(ctx, layers, 0);
+  if (st != OMNIMEM_OK) return st;
+  if (!a || !s || !budgets) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a, s or budgets");
+  const omnimem_config& c = ctx->cfg;
+  if (total_budget < 0 || total_budget > ((int64_t)1 << 40))
+    return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "total budget %lld out of range", (long long)total_budget);
+  const int64_t lo_base = (int64_t)std::ceil(((double)c.b_min_frac * (double)total_budget) / c.n_layers);
+  int64_t sum_lo = 0;
+  for (int l = 0; l < c.n_layers; ++l) sum_lo += std::min<int64_t>(lo_base, layers[l].n_cache + layers[l].n_chunk);
+  if (sum_lo > total_budget)
+    return fail(ctx, OMNIMEM_ERR_INFEASIBLE, "per-layer minimum budgets sum to %lld > total %lld",
+                (long long)sum_lo, (long long)total_budget);
+  if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
+  const LayerDesc* dev = nullptr;
+  if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
+  return finish(ctx, launch_allocate(ctx->dm, dev, ctx->ws, a, s, total_budget, c.ratio_r, c.temperature,
+                                     c.b_min_frac, c.b_max_frac, budgets, stats, stream),
+                stream, "omnimem_allocate launch");
+}
+
+omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,
+                                      const int32_t* budgets, int32_t* idx, hipStream_t stream) {
+  omnimem_status st = validate(ctx, layers, NEED_K | NEED_V | NEED_OUT);
+  if (st != OMNIMEM_OK) return st;
+  if (!a || !s || !budgets) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a, s or budgets");
+  if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
+  const LayerDesc* dev = nullptr;
+  if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
+  return finish(ctx, launch_select_compact(ctx->dm, ctx->cfg.dtype, ctx->cfg.lambda, dev, ctx->ws, a, s, budgets,
+                                           idx, stream),
+                stream, "omnimem_select_compact launch");
+}
+
+omnimem_status omnimem_profile(omnimem_ctx* ctx, int32_t on) {
+  if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
+  omnimem_status st = set_device(ctx);
+  if (st != OMNIMEM_OK) return st;
+  if (on && ctx->prof.pool.empty()) {
+    ctx->prof.pool.resize(kProfEvents);
+    for (auto& e : ctx->prof.pool) {
+      hipError_t err = hipEventCreate(&e);
+      if (err != hipSuccess) return hip_fail(ctx, err, "profiling events");
+    }
+  }
+  ctx->ws.prof = on ? &ctx->prof : nullptr;
+  return OMNIMEM_OK;
+}
+
+omnimem_status omnimem_profile_report(omnimem_ctx* ctx, omnimem_kernel_time* out, int32_t capacity,
+                                      int32_t* count) {
+  if (!ctx || (!out && capacity > 0) || !count) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null argument");
+  omnimem_status st = set_device(ctx);
+  if (st != OMNIMEM_OK) return st;
+  Profiler& p = ctx->prof;
+  double total[K_COUNT] = {};
+  int n[K_COUNT] = {};
+  int order[K_COUNT];
+  int n_kinds = 0;
+  for (size_t i = 0; i < p.kernel.size(); ++i) {
+    hipError_t e = hipEventSynchronize(p.pool[p.first[i] + 1]);
+    if (e != hipSuccess) return hip_fail(ctx, e, "profile wait");
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, p.pool[p.first[i]], p.pool[p.first[i] + 1]);
+    if (e != hipSuccess) return hip_fail(ctx, e, "profile elapsed time");
+    const int k = p.kernel[i];
+    if (n[k] == 0) order[n_kinds++] = k;
+    n[k] += 1;
+    total[k] += ms;
+  }
+  const int m = std::min<int>(n_kinds, std::max<int32_t>(capacity, 0));
+  for (int i = 0; i < m; ++i) {
+    const int k = order[i];
+    std::memset(&out[i], 0, sizeof out[i]);
+    std::snprintf(out[i].name, sizeof out[i].name, "%s", kKernelNames[k]);
+    out[i].launches = n[k];
+    out[i].total_ms = total[k];
+  }
+  *count = m;
+  p.kernel.clear();
+  p.first.clear();
+  p.used = 0;
+  p.open = false;
+  return OMNIMEM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,177 @@
+// Internal declarations shared by the library's HIP translation units.
+// Target: gfx950 (CDNA4) only: 64-lane wavefronts, MFMA 32x32 tiles.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace omnimem {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Device copy of one layer's working-set descriptor.  Strides in elements.
+struct LayerDesc {
+  const void* q;
+  const void* k;
+  const void* v;
+  const uint8_t* mod;
+  const float* lse_in;   // caller-supplied log-sum-exp [H_q][n_chunk] or null
+  void* k_out;
+  void* v_out;
+  int64_t q_hs, q_rs;
+  int64_t kv_hs, kv_rs;
+  int64_t out_hs, out_rs;
+  int32_t n_cache, n_chunk, n;
+  float scale_log2;      // softmax scale times log2(e)
+};
+
+// Sizes fixed for a context.
+struct Dims {
+  int L, Hq, Hkv, G, d;
+  int64_t max_tokens, max_chunk;
+  int causal;
+};
+
+// ---------------------------------------------------------------------------
+// MFMA operand traits.  A 32x32 output tile D[M][N] += A[M][k] B[k][N] is
+// computed in k-steps; lane l supplies row (l & 31) of A (and column (l & 31)
+// of B), holding PER_LANE consecutive k-elements starting at
+// ks*KSTEP + (l >> 5)*PER_LANE.  The output element held in accumulator
+// register r of lane l is D[(r >> 2)*8 + (l >> 5)*4 + (r & 3)][l & 31].
+// ---------------------------------------------------------------------------
+template <typename T> struct Mfma;
+
+template <> struct Mfma<uint16_t> {  // bf16 storage, v_mfma_f32_32x32x16_bf16
+  static constexpr int KSTEP = 16;
+  static constexpr int PER_LANE = 8;
+  using frag = bf16x8;
+  __device__ static inline floatx16 mma(frag a, frag b, floatx16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline frag load(const uint16_t* p) {
+    return *reinterpret_cast<const frag*>(p);
+  }
+  __device__ static inline frag zero() { return frag{}; }
+};
+
+template <> struct Mfma<float> {  // fp32, v_mfma_f32_32x32x2_f32
+  static constexpr int KSTEP = 2;
+  static constexpr int PER_LANE = 1;
+  using frag = float;
+  __device__ static inline floatx16 mma(frag a, frag b, floatx16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline frag load(const float* p) { return *p; }
+  __device__ static inline frag zero() { return 0.0f; }
+};
+
+// Row of the 32x32 output tile held by accumulator register r of lane l.
+__device__ inline int acc_row(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }
+
+// LDS row padding: 16 bytes keeps ds_read_b128 of consecutive rows on
+// different banks.
+template <typename T> constexpr int lds_pad() { return 16 / (int)sizeof(T); }
+
+// Copy `rows` rows of D elements from global (row r at src + r*row_stride)
+// into an LDS tile with row stride D + pad; rows at or past `valid` are
+// zero-filled.  Every thread of the block takes part.
+template <typename T, int D>
+__device__ inline void stage_rows(T* lds, const T* src, int64_t row_stride, int rows, int valid) {
+  constexpr int CPR = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
+  constexpr int LD = D + lds_pad<T>();
+  for (int c = threadIdx.x; c < rows * CPR; c += blockDim.x) {
+    const int r = c / CPR, x = c % CPR;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (r < valid) val = *reinterpret_cast<const uint4*>(src + (int64_t)r * row_stride + x * (16 / sizeof(T)));
+    *reinterpret_cast<uint4*>(lds + r * LD + x * (16 / sizeof(T))) = val;
+  }
+}
+
+// Same, with an explicit row list (gathered rows).
+template <typename T, int D>
+__device__ inline void stage_rows_gather(T* lds, const T* base, int64_t row_stride, const int* rows_idx,
+                                         int rows, int valid) {
+  constexpr int CPR = D * (int)sizeof(T) / 16;
+  constexpr int LD = D + lds_pad<T>();
+  for (int c = threadIdx.x; c < rows * CPR; c += blockDim.x) {
+    const int r = c / CPR, x = c % CPR;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (r < valid) val = *reinterpret_cast<const uint4*>(base + (int64_t)rows_idx[r] * row_stride + x * (16 / sizeof(T)));
+    *reinterpret_cast<uint4*>(lds + r * LD + x * (16 / sizeof(T))) = val;
+  }
+}
+
+// Order-preserving map float -> int32 (signed compare), an involution.
+__device__ inline int ord_f32(float f) {
+  int i = __float_as_int(f);
+  return i ^ ((i >> 31) & 0x7fffffff);
+}
+__device__ inline float unord_f32(int i) { return __int_as_float(i ^ ((i >> 31) & 0x7fffffff)); }
+
+constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
+
+// ---------------------------------------------------------------------------
+// Optional launch timing (see omnimem_profile).
+// ---------------------------------------------------------------------------
+enum KernelId {
+  K_LSE, K_COLSUM, K_HEADSUM, K_LISTS, K_PLAN, K_NORMS, K_FILL, K_GRAM, K_GRAM_FINISH, K_ADJ,
+  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_COUNT
+};
+struct Profiler;
+void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
+
+// Launch `stmt` bracketed by profiler events when profiling is on.
+#define OMNIMEM_LAUNCH(ws, kid, st, ...)                 \
+  do {                                                   \
+    if ((ws).prof) prof_mark((ws).prof, (kid), (st), true); \
+    __VA_ARGS__;                                         \
+    if ((ws).prof) prof_mark((ws).prof, (kid), (st), false); \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// Workspace owned by a context (device pointers), sized at creation.
+// ---------------------------------------------------------------------------
+struct Workspace {
+  LayerDesc* desc;        // [slots][L]
+  float* lse;             // [L][Hq][max_chunk]
+  float* part;            // [L][Hq][max_tokens] per-query-head column sums
+  int* pos;               // [L][max_tokens]  visual rows then audio rows
+  int* rank;              // [L][max_tokens]  rank of row j inside its modality
+  int* counts;            // [L][2]           K_v, K_a
+  float* inv_norm;        // [L][Hkv][max_tokens]
+  int* best;              // [L][Hkv][max_tokens] ord_f32 of the best cosine
+  int4* items;            // Gram work items
+  int* n_items;           // [1]
+  int64_t items_cap;
+  double* stat_part;      // [L][Hkv][3][4]
+  int* eff;               // [L][2] budgets as applied by select
+  int* idx;               // [L][Hkv][max_tokens] fallback for the idx output
+  uint32_t* keys;         // [L][Hkv][max_tokens]
+  Profiler* prof;         // null unless timing is on
+};
+
+// Launchers (each returns hipGetLastError() after its launches).
+hipError_t launch_score(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws,
+                        float* lse_buf, float* a, int need_lse, hipStream_t st);
+hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
+                             const Workspace& ws, float* s, hipStream_t st);
+hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, hipStream_t st);
+hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspace& ws,
+                           const float* a, const float* s, int64_t total, float ratio_r,
+                           float temperature, float bmin_frac, float bmax_frac, int32_t* budgets,
+                           float* stats, hipStream_t st);
+hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, const LayerDesc* desc,
+                                 const Workspace& ws, const float* a, const float* s,
+                                 const int32_t* budgets, int32_t* idx, hipStream_t st);
+
+constexpr int kGramTile = 128;   // rows per Gram block
+constexpr int kGramStrip = 4;    // J blocks per work item
+
+}  // namespace omnimem

@@ -1,0 +1,210 @@
+"""Thin ctypes binding of libomnimem.so (the C ABI in include/omnimem.h).
+
+Argument marshalling only: every stage of the compression step runs in the
+library's HIP kernels.  torch tensors serve as device buffers and streams.
+There is no fallback: if the library is missing or fails to load, every
+call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libomnimem.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_INFEASIBLE, ERR_CAPACITY, ERR_HIP = range(6)
+BF16, F32 = 0, 1
+SIM_MAX, SIM_ADJ = 0, 1
+
+EXPORTED = [
+    "omnimem_config_default", "omnimem_create", "omnimem_destroy", "omnimem_last_error",
+    "omnimem_score", "omnimem_redundancy", "omnimem_allocate", "omnimem_select_compact",
+    "omnimem_profile", "omnimem_profile_report",
+]
+
+
+class OmnimemError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"omnimem status {status}: {message}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("lambda_", ctypes.c_float),
+        ("ratio_r", ctypes.c_float), ("temperature", ctypes.c_float), ("b_min_frac", ctypes.c_float),
+        ("b_max_frac", ctypes.c_float), ("causal", ctypes.c_int32), ("sim", ctypes.c_int32),
+        ("sim_on_keys", ctypes.c_int32), ("max_tokens", ctypes.c_int64), ("max_chunk", ctypes.c_int64),
+    ]
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [
+        ("q", ctypes.c_void_p), ("q_head_stride", ctypes.c_int64), ("q_row_stride", ctypes.c_int64),
+        ("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("kv_head_stride", ctypes.c_int64),
+        ("kv_row_stride", ctypes.c_int64), ("modality", ctypes.c_void_p), ("n_cache", ctypes.c_int64),
+        ("n_chunk", ctypes.c_int64), ("sm_scale", ctypes.c_float), ("lse", ctypes.c_void_p),
+        ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p), ("out_head_stride", ctypes.c_int64),
+        ("out_row_stride", ctypes.c_int64),
+    ]
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
+
+
+_lib = None
+
+
+def load_library(path=LIB_PATH):
+    """Load libomnimem.so; raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2606_07577_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    lib.omnimem_config_default.argtypes = [ctypes.POINTER(Config)]
+    lib.omnimem_config_default.restype = None
+    lib.omnimem_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(vp)]
+    lib.omnimem_create.restype = i32
+    lib.omnimem_destroy.argtypes = [vp]
+    lib.omnimem_destroy.restype = i32
+    lib.omnimem_last_error.argtypes = [vp]
+    lib.omnimem_last_error.restype = ctypes.c_char_p
+    lib.omnimem_score.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, vp]
+    lib.omnimem_score.restype = i32
+    lib.omnimem_redundancy.argtypes = [vp, ctypes.POINTER(Layer), vp, vp]
+    lib.omnimem_redundancy.restype = i32
+    lib.omnimem_allocate.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, i64, vp, vp, vp]
+    lib.omnimem_allocate.restype = i32
+    lib.omnimem_select_compact.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, vp, vp, vp]
+    lib.omnimem_select_compact.restype = i32
+    lib.omnimem_profile.argtypes = [vp, ctypes.c_int32]
+    lib.omnimem_profile.restype = i32
+    lib.omnimem_profile_report.argtypes = [vp, ctypes.POINTER(KernelTime), ctypes.c_int32,
+                                           ctypes.POINTER(ctypes.c_int32)]
+    lib.omnimem_profile_report.restype = i32
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("device tensors (torch, cuda) are required")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def make_layer(q, k, v, modality, n_cache, sm_scale=0.0, lse=None, k_out=None, v_out=None):
+    """Descriptor of one layer's working set from device tensors.
+
+    q [H_q, C, d]; k, v [H_kv, N, d]; modality uint8 [N]; optional lse
+    [H_q, C] fp32; optional k_out, v_out [H_kv, >=N, d] (same strides).
+    """
+    if k.stride() != v.stride():
+        raise ValueError("k and v must share strides")
+    if k_out is not None and (v_out is None or k_out.stride() != v_out.stride()):
+        raise ValueError("k_out and v_out must both be given with equal strides")
+    if modality.dtype != torch.uint8:
+        raise TypeError("modality must be uint8")
+    n = k.shape[1]
+    lay = Layer()
+    lay.q = _ptr(q)
+    lay.q_head_stride, lay.q_row_stride = (q.stride(0), q.stride(1)) if q is not None else (0, 0)
+    lay.k, lay.v = _ptr(k), _ptr(v)
+    lay.kv_head_stride, lay.kv_row_stride = k.stride(0), k.stride(1)
+    lay.modality = _ptr(modality)
+    lay.n_cache = int(n_cache)
+    lay.n_chunk = int(n - n_cache)
+    lay.sm_scale = float(sm_scale)
+    lay.lse = _ptr(lse)
+    if k_out is not None:
+        lay.k_out, lay.v_out = _ptr(k_out), _ptr(v_out)
+        lay.out_head_stride, lay.out_row_stride = k_out.stride(0), k_out.stride(1)
+    return lay
+
+
+class Context:
+    """An omnimem_ctx: workspace for the given capacities on the current device."""
+
+    def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, max_tokens, max_chunk,
+                 dtype=BF16, **options):
+        lib = load_library()
+        cfg = Config()
+        lib.omnimem_config_default(ctypes.byref(cfg))
+        cfg.n_layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim = n_layers, n_q_heads, n_kv_heads, head_dim
+        cfg.dtype, cfg.max_tokens, cfg.max_chunk = dtype, max_tokens, max_chunk
+        for key, val in options.items():
+            setattr(cfg, "lambda_" if key == "lam" else key, val)
+        self.cfg = cfg
+        self._lib = lib
+        handle = ctypes.c_void_p()
+        st = lib.omnimem_create(ctypes.byref(cfg), ctypes.byref(handle))
+        if st != OK:
+            raise OmnimemError(st, lib.omnimem_last_error(None).decode())
+        self.handle = handle
+
+    def _check(self, st):
+        if st != OK:
+            raise OmnimemError(st, self._lib.omnimem_last_error(self.handle).decode())
+
+    def _layers(self, layers):
+        if len(layers) != self.cfg.n_layers:
+            raise ValueError(f"expected {self.cfg.n_layers} layer descriptors")
+        arr = (Layer * len(layers))(*layers)
+        return arr
+
+    def close(self):
+        if self.handle:
+            self._lib.omnimem_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # The four stages of the C ABI, same names.
+    def omnimem_score(self, layers, a, lse_out=None, stream=None):
+        self._check(self._lib.omnimem_score(self.handle, self._layers(layers), _ptr(a), _ptr(lse_out),
+                                            _stream(stream)))
+
+    def omnimem_redundancy(self, layers, s, stream=None):
+        self._check(self._lib.omnimem_redundancy(self.handle, self._layers(layers), _ptr(s), _stream(stream)))
+
+    def omnimem_allocate(self, layers, a, s, total_budget, budgets, stats=None, stream=None):
+        self._check(self._lib.omnimem_allocate(self.handle, self._layers(layers), _ptr(a), _ptr(s),
+                                               int(total_budget), _ptr(budgets), _ptr(stats), _stream(stream)))
+
+    def omnimem_select_compact(self, layers, a, s, budgets, idx=None, stream=None):
+        self._check(self._lib.omnimem_select_compact(self.handle, self._layers(layers), _ptr(a), _ptr(s),
+                                                     _ptr(budgets), _ptr(idx), _stream(stream)))
+
+
+    def omnimem_profile(self, on):
+        self._check(self._lib.omnimem_profile(self.handle, int(bool(on))))
+
+    def omnimem_profile_report(self):
+        """{kernel name: (launches, total milliseconds)} of the recorded launches."""
+        buf = (KernelTime * 32)()
+        n = ctypes.c_int32()
+        self._check(self._lib.omnimem_profile_report(self.handle, buf, 32, ctypes.byref(n)))
+        return {buf[i].name.decode(): (buf[i].launches, buf[i].total_ms) for i in range(n.value)}
+
+
+def default_scale(head_dim):
+    return 1.0 / math.sqrt(head_dim)

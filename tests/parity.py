@@ -1,0 +1,99 @@
+"""Comparison rules between the HIP path and the oracle.
+
+Tolerances (bf16/fp32 inputs, fp32 accumulation on the GPU, fp64 oracle):
+  a, lse, normalised entropy, C, w:  |d| <= 1e-3 |ref| + 1e-6 mean|ref|
+  s:                                 |d| <= 1e-3 |ref| + 1e-5
+Integer work (budgets from identical inputs, gathers) is bit-exact.  Kept
+index sets are bit-exact where the oracle's psi margin at the M-th boundary
+exceeds 1e-3 relative; otherwise every kept row must have psi >= psi_(M)
+(1 - 1e-3) and every dropped row psi <= psi_(M) (1 + 1e-3).
+"""
+import numpy as np
+
+from oracle import omnimem_oracle as om
+
+# The library's configuration values are fp32; the oracle takes the same
+# numbers widened to fp64.
+LAMBDA = float(np.float32(om.DEFAULT_LAMBDA))
+TEMPERATURE = float(np.float32(om.DEFAULT_T))
+RATIO = float(np.float32(om.DEFAULT_R))
+REL = 1e-3
+
+
+def assert_close_a(got, ref, what="a"):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    tol = REL * np.abs(ref) + 1e-6 * np.abs(ref).mean()
+    bad = np.abs(got - ref) > tol
+    if bad.any():
+        i = np.argmax(np.abs(got - ref) - tol)
+        raise AssertionError(f"{what}: {bad.sum()} of {bad.size} beyond tolerance; worst at flat {i}: "
+                             f"got {got.flat[i]!r} ref {ref.flat[i]!r}")
+
+
+def assert_close_s(got, ref, what="s"):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    tol = REL * np.abs(ref) + 1e-5
+    bad = np.abs(got - ref) > tol
+    if bad.any():
+        i = np.argmax(np.abs(got - ref) - tol)
+        raise AssertionError(f"{what}: {bad.sum()} of {bad.size} beyond tolerance; worst at flat {i}: "
+                             f"got {got.flat[i]!r} ref {ref.flat[i]!r}")
+
+
+def check_selection(idx_row, psi_row, modality, m_v, m_a, rel=REL):
+    """One KV head: GPU kept rows vs the oracle's psi.  Returns #exact blocks."""
+    modality = np.asarray(modality)
+    exact = 0
+    for mu, lo, hi in ((0, 0, m_v), (1, m_v, m_v + m_a)):
+        got = np.asarray(idx_row[lo:hi], dtype=np.int64)
+        m = hi - lo
+        pos = om.segment_positions(modality, mu)
+        assert len(got) == m
+        if m:
+            assert (np.diff(got) > 0).all(), "kept rows not ascending"
+            assert (modality[got] == mu).all(), "kept row of the wrong modality"
+        order = sorted(pos.tolist(), key=lambda p: (-psi_row[p], p))
+        ref = np.sort(np.array(order[:m], dtype=np.int64))
+        if m == 0 or m == len(pos):
+            np.testing.assert_array_equal(got, ref)
+            exact += 1
+            continue
+        psi_m, psi_next = psi_row[order[m - 1]], psi_row[order[m]]
+        margin = (psi_m - psi_next) / psi_m if psi_m > 0 else 0.0
+        if margin > rel:
+            np.testing.assert_array_equal(got, ref)
+            exact += 1
+        else:
+            kept = set(got.tolist())
+            dropped = [p for p in pos.tolist() if p not in kept]
+            assert all(psi_row[p] >= psi_m * (1 - rel) for p in kept)
+            assert all(psi_row[p] <= psi_m * (1 + rel) for p in dropped)
+    return exact
+
+
+def oracle_allocation(a_list, s_list, layers, total_budget, bmin=om.DEFAULT_BMIN_FRAC,
+                      bmax=om.DEFAULT_BMAX_FRAC, temperature=TEMPERATURE, r=RATIO):
+    """Oracle stats, shares and (M_v, M_a) per layer from given a, s."""
+    stats = [om.avba_statistics(a, s, l["modality"]) for a, s, l in zip(a_list, s_list, layers)]
+    n_tok = [len(l["modality"]) for l in layers]
+    shares = om.layer_shares([st["C_l"] for st in stats], n_tok, total_budget, temperature, bmin, bmax)
+    b_l = om.integer_budgets(shares, n_tok, total_budget, bmin, bmax)
+    budgets = []
+    for st, b, l in zip(stats, b_l, layers):
+        mod = np.asarray(l["modality"])
+        w_v, _ = om.modality_weights(st["C_v"], st["C_a"], r)
+        st["w_v"] = w_v
+        budgets.append(om.split_budget(int(b), w_v, int((mod == 0).sum()), int((mod == 1).sum())))
+    return stats, shares, np.array(budgets, dtype=np.int64)
+
+
+STAT_KEYS = ["H_v", "H_a", "H_l", "sbar_v", "sbar_a", "sbar_l", "C_v", "C_a", "C_l", "w_v"]
+
+
+def as_f64(layer):
+    out = dict(layer)
+    for key in ("q", "k", "v"):
+        out[key] = np.asarray(layer[key], dtype=np.float64)
+    return out

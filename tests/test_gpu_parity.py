@@ -1,0 +1,336 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Each stage is checked on its own ("teacher-forced": the GPU stage gets the
+oracle's inputs where a stage has inputs) and the whole chain free-running.
+Small workloads are compared element by element; the full-size Qwen-7B
+shaped layer (6144 tokens) likewise; the 28-layer and 40960-token workloads
+on sampled queries/keys/rows the oracle computes one by one, plus
+properties that hold at any size.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import omnimem_oracle as om
+from paper_2606_07577_amd import omnimem, synth
+from paper_2606_07577_amd.step import DeviceStep
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _sync():
+    torch.cuda.synchronize()
+
+
+class Case:
+    """Run every stage of one workload on the GPU and keep host copies."""
+
+    def __init__(self, layers, budget, **opts):
+        self.layers = layers
+        self.budget = budget
+        self.opts = opts
+        self.step = st = DeviceStep(layers, budget, **opts)
+        st.score(lse_out=True)
+        st.redundancy()
+        st.allocate()
+        st.select_compact()
+        _sync()
+        L = len(layers)
+        self.lse = [st.host("lse", l) for l in range(L)]
+        self.a = [st.host("a", l) for l in range(L)]
+        self.s = [st.host("s", l) for l in range(L)]
+        self.budgets = st.budgets.cpu().numpy().astype(np.int64)
+        self.stats = st.stats.cpu().numpy()
+        self.idx = [st.host("idx", l) for l in range(L)]
+        self.k_out = [st.k_out[l].float().cpu().numpy() for l in range(L)]
+        self.v_out = [st.v_out[l].float().cpu().numpy() for l in range(L)]
+        self.layers64 = [P.as_f64(x) for x in layers]
+
+    @property
+    def causal(self):
+        return bool(self.opts.get("causal", 1))
+
+    @property
+    def mode(self):
+        return "adj" if self.opts.get("sim", omnimem.SIM_MAX) == omnimem.SIM_ADJ else "max"
+
+
+def ragged_layers(n_layers=1, d=128, dtype="bf16", seed=100, caches=((200, 77),), frames=(3, 41, 13),
+                  h_q=8, h_kv=2):
+    out = []
+    for l in range(n_layers):
+        cv, ca = caches[l % len(caches)]
+        out.append(synth.make_layer([seed, l], h_q=h_q, h_kv=h_kv, d=d, n_cache_v=cv, n_cache_a=ca,
+                                    n_frames=frames[0], frame_v=frames[1], frame_a=frames[2],
+                                    dup_frac=0.3, head_scale=(0.5, 2.0), dtype=dtype,
+                                    sm_scale=1.0 / ((0.5 + l) * math.sqrt(d))))
+    return out
+
+
+_cache = {}
+
+
+def get_case(name):
+    if name in _cache:
+        return _cache[name]
+    if name == "tiny-f32":
+        case = Case(synth.make_workload("tiny-f32-640"), 256)
+    elif name == "qwen-layer":
+        case = Case(synth.make_workload("qwen7b-layer-6144"), 4096)
+    elif name == "ragged-bf16":
+        case = Case(ragged_layers(), 300)
+    elif name == "ragged-bf16-d64":
+        case = Case(ragged_layers(d=64, seed=101), 250)
+    elif name == "ragged-3layer":
+        case = Case(ragged_layers(3, seed=102, caches=((200, 77), (333, 111), (64, 17))), 3 * 260)
+    elif name == "ragged-adj-noncausal":
+        case = Case(ragged_layers(seed=103), 300, sim=omnimem.SIM_ADJ, causal=0)
+    else:
+        raise KeyError(name)
+    _cache[name] = case
+    return case
+
+
+FULL_CASES = ["tiny-f32", "ragged-bf16", "ragged-bf16-d64", "ragged-3layer", "ragged-adj-noncausal",
+              "qwen-layer"]
+
+
+@pytest.mark.parametrize("name", FULL_CASES)
+def test_lse_and_importance(name):
+    c = get_case(name)
+    for l, lay in enumerate(c.layers64):
+        lse = om.attention_lse(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], c.causal)
+        P.assert_close_a(c.lse[l], lse, f"lse layer {l}")
+        a = om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], c.causal, lse=lse)
+        P.assert_close_a(c.a[l], a, f"a layer {l}")
+        group = lay["q"].shape[0] // lay["k"].shape[0]
+        np.testing.assert_allclose(c.a[l].sum(axis=1, dtype=np.float64), group * lay["q"].shape[1], rtol=1e-4)
+
+
+@pytest.mark.parametrize("name", FULL_CASES)
+def test_redundancy(name):
+    c = get_case(name)
+    for l, lay in enumerate(c.layers64):
+        s = om.redundancy(lay["v"], lay["modality"], c.mode)
+        P.assert_close_s(c.s[l], s, f"s layer {l}")
+
+
+@pytest.mark.parametrize("name", FULL_CASES)
+def test_allocate_teacher_forced(name):
+    # The GPU allocation from the oracle's own a and s (rounded to fp32, the
+    # ABI's type) must give the oracle's integer budgets exactly.
+    c = get_case(name)
+    a_ref, s_ref = [], []
+    for lay in c.layers64:
+        a_ref.append(om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], c.causal)
+                     .astype(np.float32))
+        s_ref.append(om.redundancy(lay["v"], lay["modality"], c.mode).astype(np.float32))
+    st = c.step
+    a_dev, s_dev = st.to_device_f32(a_ref), st.to_device_f32(s_ref)
+    budgets = torch.zeros_like(st.budgets)
+    stats = torch.zeros_like(st.stats)
+    st.ctx.omnimem_allocate(st.descs, a_dev, s_dev, c.budget, budgets, stats)
+    _sync()
+    ref_stats, shares, ref_budgets = P.oracle_allocation(
+        [x.astype(np.float64) for x in a_ref], [x.astype(np.float64) for x in s_ref], c.layers, c.budget)
+    np.testing.assert_array_equal(budgets.cpu().numpy(), ref_budgets)
+    got = stats.cpu().numpy()
+    for l, rs in enumerate(ref_stats):
+        P.assert_close_a(got[l], [rs[k] for k in P.STAT_KEYS], f"stats layer {l}")
+    total = sum(min(n, c.budget) for n in [len(x["modality"]) for x in c.layers])
+    assert ref_budgets.sum() == min(c.budget, total)
+
+
+@pytest.mark.parametrize("name", FULL_CASES)
+def test_select_compact_teacher_forced(name):
+    c = get_case(name)
+    st = c.step
+    L = len(c.layers)
+    a_ref, s_ref = [], []
+    for lay in c.layers64:
+        a_ref.append(om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], c.causal)
+                     .astype(np.float32))
+        s_ref.append(om.redundancy(lay["v"], lay["modality"], c.mode).astype(np.float32))
+    _, _, budgets = P.oracle_allocation([x.astype(np.float64) for x in a_ref],
+                                        [x.astype(np.float64) for x in s_ref], c.layers, c.budget)
+    st.ctx.omnimem_select_compact(st.descs, st.to_device_f32(a_ref), st.to_device_f32(s_ref),
+                                  torch.from_numpy(budgets.astype(np.int32)).to(st.device), st.idx)
+    _sync()
+    for l in range(L):
+        mv, ma = budgets[l]
+        psi = om.retention_score(a_ref[l].astype(np.float64), s_ref[l].astype(np.float64), P.LAMBDA)
+        idx = st.host("idx", l)[:, : mv + ma]
+        for g in range(st.h_kv):
+            P.check_selection(idx[g], psi[g], c.layers[l]["modality"], mv, ma)
+        k_out = st.k_out[l].float().cpu().numpy()
+        v_out = st.v_out[l].float().cpu().numpy()
+        for g in range(st.h_kv):
+            np.testing.assert_array_equal(k_out[g, : mv + ma], c.layers[l]["k"][g, idx[g]])
+            np.testing.assert_array_equal(v_out[g, : mv + ma], c.layers[l]["v"][g, idx[g]])
+
+
+@pytest.mark.parametrize("name", FULL_CASES)
+def test_chain_free_running(name):
+    # The GPU's own a, s -> budgets -> kept rows; budgets close to the
+    # oracle's, the kept rows a valid top-M of the oracle's psi under the
+    # GPU's budgets, and the compacted caches exactly the kept rows.
+    c = get_case(name)
+    a_o, s_o = [], []
+    for lay in c.layers64:
+        a_o.append(om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], c.causal))
+        s_o.append(om.redundancy(lay["v"], lay["modality"], c.mode))
+    _, _, ref_budgets = P.oracle_allocation(a_o, s_o, c.layers, c.budget)
+    assert c.budgets.sum() == ref_budgets.sum()
+    assert np.abs(c.budgets - ref_budgets).max() <= max(1, int(2e-3 * ref_budgets.max()))
+    for l, lay in enumerate(c.layers):
+        mv, ma = c.budgets[l]
+        psi = om.retention_score(a_o[l], s_o[l], P.LAMBDA)
+        for g in range(c.step.h_kv):
+            row = c.idx[l][g, : mv + ma]
+            P.check_selection(row, psi[g], lay["modality"], mv, ma, rel=5e-3)
+            np.testing.assert_array_equal(c.k_out[l][g, : mv + ma], lay["k"][g, row])
+            np.testing.assert_array_equal(c.v_out[l][g, : mv + ma], lay["v"][g, row])
+
+
+def test_determinism_bitwise():
+    c = get_case("ragged-3layer")
+    st = c.step
+    st.run()
+    _sync()
+    again = [st.host("a", l) for l in range(3)], [st.host("s", l) for l in range(3)]
+    for l in range(3):
+        np.testing.assert_array_equal(again[0][l], c.a[l])
+        np.testing.assert_array_equal(again[1][l], c.s[l])
+    np.testing.assert_array_equal(st.budgets.cpu().numpy(), c.budgets)
+    for l in range(3):
+        np.testing.assert_array_equal(st.host("idx", l), c.idx[l])
+
+
+def test_caller_supplied_lse_matches_computed():
+    c = get_case("ragged-bf16")
+    layers = c.layers
+    step = DeviceStep(layers, 300)
+    lse = [torch.from_numpy(c.lse[0]).contiguous().cuda()]
+    step.set_lse_inputs(lse)
+    step.score(lse_out=True)
+    _sync()
+    np.testing.assert_array_equal(step.host("lse", 0), c.lse[0])
+    np.testing.assert_array_equal(step.host("a", 0), c.a[0])
+    step.close()
+
+
+# ---------------------------------------------------------------------------
+# Large workloads: sampled outputs and properties
+# ---------------------------------------------------------------------------
+
+def _sampled_checks(c, l, rng, n_q=48, n_k=96, n_s=96):
+    lay = c.layers64[l]
+    C = lay["q"].shape[1]
+    N = lay["k"].shape[1]
+    qs = np.sort(rng.choice(C, size=min(n_q, C), replace=False))
+    qs[0], qs[-1] = 0, C - 1
+    lse_ref = om.attention_lse(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True, queries=qs)
+    P.assert_close_a(c.lse[l][:, qs], lse_ref, f"lse layer {l} (sampled)")
+    ks = np.sort(rng.choice(N, size=min(n_k, N), replace=False))
+    ks[0], ks[-1] = 0, N - 1
+    a_ref = om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True,
+                                    lse=c.lse[l].astype(np.float64), keys=ks)
+    P.assert_close_a(c.a[l][:, ks], a_ref, f"a layer {l} (sampled keys, GPU lse)")
+    group = lay["q"].shape[0] // lay["k"].shape[0]
+    np.testing.assert_allclose(c.a[l].sum(axis=1, dtype=np.float64), group * C, rtol=1e-4)
+    rows = np.sort(rng.choice(N, size=min(n_s, N), replace=False))
+    s_ref = om.redundancy(lay["v"], lay["modality"], "max", rows=rows)
+    P.assert_close_s(c.s[l][:, rows], s_ref, f"s layer {l} (sampled rows)")
+
+
+def _allocation_and_selection_from_gpu_scores(c):
+    a64 = [x.astype(np.float64) for x in c.a]
+    s64 = [x.astype(np.float64) for x in c.s]
+    _, _, ref_budgets = P.oracle_allocation(a64, s64, c.layers, c.budget)
+    np.testing.assert_array_equal(c.budgets, ref_budgets)
+    for l, lay in enumerate(c.layers):
+        mv, ma = c.budgets[l]
+        psi = om.retention_score(a64[l], s64[l], P.LAMBDA)
+        for g in range(c.step.h_kv):
+            row = c.idx[l][g, : mv + ma]
+            P.check_selection(row, psi[g], lay["modality"], mv, ma)
+            np.testing.assert_array_equal(c.k_out[l][g, : mv + ma], lay["k"][g, row])
+            np.testing.assert_array_equal(c.v_out[l][g, : mv + ma], lay["v"][g, row])
+
+
+def test_28_layer_workload_sampled():
+    layers = synth.make_workload("qwen7b-28layer-6144")
+    c = Case(layers, 28 * 4096)
+    rng = np.random.default_rng(7)
+    for l in (0, 13, 27):
+        _sampled_checks(c, l, rng)
+    assert c.budgets.sum() == 28 * 4096
+    _allocation_and_selection_from_gpu_scores(c)
+    c.step.close()
+
+
+def test_long_cache_workload_sampled():
+    layers = synth.make_workload("qwen7b-longcache-40960")
+    c = Case(layers, 32768)
+    _sampled_checks(c, 0, np.random.default_rng(8))
+    assert c.budgets.sum() == 32768
+    _allocation_and_selection_from_gpu_scores(c)
+    c.step.close()
+
+
+# ---------------------------------------------------------------------------
+# Degenerate cases and argument validation
+# ---------------------------------------------------------------------------
+
+def test_visual_only_layer_and_budget_beyond_tokens():
+    layers = ragged_layers(seed=104, caches=((150, 0),), frames=(2, 30, 0))
+    c = Case(layers, 1000)   # more budget than the 210 rows: keep everything
+    assert c.budgets.tolist() == [[210, 0]]
+    np.testing.assert_array_equal(c.idx[0][:, :210], np.tile(np.arange(210), (2, 1)))
+    lay = c.layers64[0]
+    P.assert_close_s(c.s[0], om.redundancy(lay["v"], lay["modality"], "max"))
+    c.step.close()
+
+
+def test_exact_duplicates_and_zero_rows():
+    layers = ragged_layers(seed=105)
+    lay = layers[0]
+    lay["v"][:, 5] = lay["v"][:, 9]        # exact twins
+    lay["v"][:, 11] = 0.0                  # zero vector: cosine 0 with everything
+    c = Case(layers, 300)
+    assert (c.s[0][:, [5, 9]] == 1.0).all()
+    P.assert_close_s(c.s[0], om.redundancy(P.as_f64(lay)["v"], lay["modality"], "max"))
+    c.step.close()
+
+
+def test_validation_errors():
+    layers = ragged_layers(seed=106)
+    st = DeviceStep(layers, 300)
+    with pytest.raises(omnimem.OmnimemError) as e:
+        st.ctx.omnimem_allocate(st.descs, st.a, st.s, -1, st.budgets)
+    assert e.value.status == omnimem.ERR_INVALID_ARG
+    with pytest.raises(omnimem.OmnimemError) as e:
+        omnimem.Context(1, 8, 3, 128, 1024, 512)
+    assert e.value.status == omnimem.ERR_INVALID_ARG
+    with pytest.raises(omnimem.OmnimemError) as e:
+        omnimem.Context(1, 8, 2, 96, 1024, 512)
+    assert e.value.status == omnimem.ERR_UNSUPPORTED
+    small = omnimem.Context(1, 8, 2, 128, 100, 50)
+    with pytest.raises(omnimem.OmnimemError) as e:
+        small.omnimem_score(st.descs, st.a)
+    assert e.value.status == omnimem.ERR_CAPACITY
+    small.close()
+    bad = omnimem.make_layer(st.q[0], st.k[0], st.v[0], st.mod[0], st.n_cache[0], 0.0, None,
+                             st.k[0], st.v_out[0])  # output aliases the input
+    with pytest.raises(omnimem.OmnimemError) as e:
+        st.ctx.omnimem_select_compact([bad], st.a, st.s, st.budgets, st.idx)
+    assert e.value.status == omnimem.ERR_INVALID_ARG
+    tight = omnimem.Context(1, 8, 2, 128, st.max_tokens, st.max_chunk, b_min_frac=1.5, b_max_frac=2.0)
+    with pytest.raises(omnimem.OmnimemError) as e:
+        tight.omnimem_allocate(st.descs, st.a, st.s, 100, st.budgets)
+    assert e.value.status == omnimem.ERR_INFEASIBLE
+    tight.close()
+    st.close()
