@@ -16,42 +16,51 @@ namespace {
 
 constexpr int kStatSets = 2;  // visual, audio (the layer set is their union)
 
-__device__ inline double block_sum(double v, double* scratch) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) scratch[wave] = v;
-  __syncthreads();
-  double t = 0.0;
-  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += scratch[w];
-  return t;
+
+constexpr int kPartThreads = 256;
+constexpr int kPartRows = 512;   // rows per partial-sum workgroup
+
+__host__ __device__ inline int part_chunks(const Dims& dm) {
+  return (int)((dm.max_tokens + kPartRows - 1) / kPartRows);
 }
 
-// stat_part[l][g][set][0..3] = {sum a, sum a ln a, sum s, count}
-__global__ __launch_bounds__(256) void avba_partials(const LayerDesc* __restrict__ layers, Dims dm,
-                                                     const float* __restrict__ a, const float* __restrict__ s,
-                                                     double* __restrict__ part) {
-  const int l = blockIdx.y, g = blockIdx.x;
-  const LayerDesc Ld = layers[l];
-  const int N = Ld.n;
+// stat_part[l][g][chunk][set][0..3] = {sum a, sum a ln a, sum s, count}
+// over the visual (set 0) and audio (set 1) rows of one chunk of layer l,
+// KV head g.
+__global__ __launch_bounds__(kPartThreads) void avba_partials(const LayerDesc* __restrict__ layers, Dims dm,
+                                                              const float* __restrict__ a,
+                                                              const float* __restrict__ s,
+                                                              double* __restrict__ part) {
+  const int l = blockIdx.z, g = blockIdx.y, chunk = blockIdx.x;
+  const int N = layers[l].n;
+  const uint8_t* mod = layers[l].mod;
   const float* ag = a + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
   const float* sg = s + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
-  double acc[kStatSets][4] = {};
-  for (int j = threadIdx.x; j < N; j += blockDim.x) {
-    const int mu = Ld.mod[j] ? 1 : 0;
+  double acc[kStatSets * 4] = {};
+  const int j1 = min(N, (chunk + 1) * kPartRows);
+  for (int j = chunk * kPartRows + threadIdx.x; j < j1; j += blockDim.x) {
+    const int o = mod[j] ? 4 : 0;
     const double x = ag[j];
-    acc[mu][0] += x;
-    acc[mu][1] += x > 0.0 ? x * log(x) : 0.0;
-    acc[mu][2] += sg[j];
-    acc[mu][3] += 1.0;
+    acc[o + 0] += x;
+    acc[o + 1] += x > 0.0 ? x * log(x) : 0.0;
+    acc[o + 2] += sg[j];
+    acc[o + 3] += 1.0;
   }
-  __shared__ double scratch[16];
-  double* out = part + (((int64_t)l * dm.Hkv + g) * kStatSets) * 4;
-  for (int mu = 0; mu < kStatSets; ++mu)
-    for (int q = 0; q < 4; ++q) {
-      const double t = block_sum(acc[mu][q], scratch);
-      if (threadIdx.x == 0) out[mu * 4 + q] = t;
-    }
+  // all eight sums reduced together: wave shuffles, then one LDS round
+  __shared__ double wsum[kPartThreads / 64][kStatSets * 4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int q = 0; q < kStatSets * 4; ++q) {
+    double v = acc[q];
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0) wsum[wave][q] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < kStatSets * 4) {
+    double t = 0.0;
+    for (int w = 0; w < kPartThreads / 64; ++w) t += wsum[w][threadIdx.x];
+    part[(((int64_t)l * dm.Hkv + g) * part_chunks(dm) + chunk) * kStatSets * 4 + threadIdx.x] = t;
+  }
 }
 
 // Normalised entropy of x / sum x over K entries from sum x and sum x ln x:
@@ -62,6 +71,7 @@ __device__ inline double norm_entropy(double sum, double xlogx, double count) {
 }
 
 constexpr int kMaxLayers = 1024;
+constexpr int kMaxSums = 2048;   // L * H_kv * 8 partial sums kept in LDS
 
 __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict__ layers, Dims dm,
                                                      const double* __restrict__ part, int64_t total,
@@ -71,16 +81,28 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
   __shared__ double c_l[kMaxLayers], w_v[kMaxLayers], p[kMaxLayers], x[kMaxLayers];
   __shared__ int n_l[kMaxLayers], k_v[kMaxLayers], lo[kMaxLayers], hi[kMaxLayers], b_l[kMaxLayers];
   __shared__ double s_kappa;
+  __shared__ double sums[kMaxSums];
   const int L = dm.L;
   const double B = (double)total;
   const double T = (double)temperature;
   const double r = (double)ratio_r;
 
+  // --- chunk partials summed per (layer, head, quantity), in chunk order ---
+  const int nchunk = part_chunks(dm);
+  for (int x = threadIdx.x; x < L * dm.Hkv * kStatSets * 4; x += blockDim.x) {
+    const int lg = x / (kStatSets * 4), q = x % (kStatSets * 4);
+    const double* src = part + (int64_t)lg * nchunk * kStatSets * 4 + q;
+    double t = 0.0;
+    for (int c = 0; c < nchunk; ++c) t += src[c * kStatSets * 4];
+    sums[x] = t;
+  }
+  __syncthreads();
+
   // --- per-layer statistics (Eqs. 9, 10, 13) ---
   for (int l = threadIdx.x; l < L; l += blockDim.x) {
     double hv = 0.0, ha = 0.0, hl = 0.0, sv = 0.0, sa = 0.0, cnt_v = 0.0, cnt_a = 0.0;
     for (int g = 0; g < dm.Hkv; ++g) {
-      const double* P = part + (((int64_t)l * dm.Hkv + g) * kStatSets) * 4;
+      const double* P = sums + (l * dm.Hkv + g) * kStatSets * 4;
       hv += norm_entropy(P[0], P[1], P[3]);
       ha += norm_entropy(P[4], P[5], P[7]);
       hl += norm_entropy(P[0] + P[4], P[1] + P[5], P[3] + P[7]);
@@ -204,10 +226,14 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
 
 }  // namespace
 
+int allocate_part_chunks(const Dims& dm) { return part_chunks(dm); }
+
 hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
                            const float* s, int64_t total, float ratio_r, float temperature, float bmin_frac,
                            float bmax_frac, int32_t* budgets, float* stats, hipStream_t st) {
-  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st, avba_partials<<<dim3(dm.Hkv, dm.L), 256, 0, st>>>(desc, dm, a, s, ws.stat_part));
+  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st,
+                 avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
+                                                                                            ws.stat_part));
   OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, total, ratio_r,
                                    temperature, bmin_frac, bmax_frac, budgets, stats));
   return hipGetLastError();

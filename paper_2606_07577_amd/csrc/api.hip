@@ -50,8 +50,7 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 }  // namespace omnimem
 
 static const char* kKernelNames[K_COUNT] = {
-    "lse_pass", "colsum_pass", "head_sum", "modality_lists", "gram_plan", "inv_norms", "fill_int",
-    "gram_max", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact"};
+    "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "inv_norms", "gram_max", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -260,6 +259,9 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       c.max_tokens > (int64_t)1 << 30)
     return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "bad sizes: need 1 <= n_layers <= %d, H_kv | H_q, "
                 "0 <= max_chunk <= max_tokens <= 2^30", kMaxLayers);
+  if ((int64_t)c.n_layers * c.n_kv_heads > 256)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "n_layers * n_kv_heads = %d: at most 256 supported",
+                c.n_layers * c.n_kv_heads);
   if (c.head_dim != 64 && c.head_dim != 128)
     return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "head_dim %d: supported 64 and 128", c.head_dim);
   if (c.dtype != OMNIMEM_BF16 && c.dtype != OMNIMEM_F32)
@@ -278,21 +280,23 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
   dm.L = c.n_layers; dm.Hq = c.n_q_heads; dm.Hkv = c.n_kv_heads; dm.G = c.n_q_heads / c.n_kv_heads;
   dm.d = c.head_dim; dm.max_tokens = c.max_tokens; dm.max_chunk = std::max<int64_t>(c.max_chunk, 1);
   dm.causal = c.causal ? 1 : 0;
+  choose_key_ranges(&dm);
   const size_t L = c.n_layers, Hq = c.n_q_heads, Hkv = c.n_kv_heads, T = c.max_tokens, Cm = dm.max_chunk;
   const int64_t tblocks = (c.max_tokens + kGramTile - 1) / kGramTile;
   Workspace& ws = ctx->ws;
-  ws.items_cap = (int64_t)L * Hkv * plan_F(tblocks + 1);
+  ws.items_per_layer = (int64_t)Hkv * plan_F(tblocks + 1);
   if ((e = dalloc(ctx, &ws.desc, (size_t)kSlots * L)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.lse, L * Hq * Cm)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.part, L * Hq * T)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.pos, L * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.lse_part, L * Hq * (size_t)dm.n_kr * Cm)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.lse2, L * Hq * Cm)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.part, L * Hq * (size_t)dm.n_qc * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.pos, L * 2 * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.rank, L * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.counts, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.inv_norm, L * Hkv * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.best, L * Hkv * T)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.items, (size_t)ws.items_cap)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.n_items, 1)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.stat_part, L * Hkv * 2 * 4)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.items, L * (size_t)ws.items_per_layer)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.n_items, L)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.stat_part, L * Hkv * (size_t)allocate_part_chunks(dm) * 2 * 4)) != hipSuccess ||
       (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.idx, L * Hkv * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.keys, L * Hkv * T)) != hipSuccess) {
@@ -340,8 +344,7 @@ omnimem_status omnimem_score(omnimem_ctx* ctx, const omnimem_layer* layers, floa
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
-  float* lse_buf = lse_out ? lse_out : ctx->ws.lse;
-  return finish(ctx, launch_score(ctx->dm, ctx->cfg.dtype, dev, ctx->ws, lse_buf, a, 1, stream), stream,
+  return finish(ctx, launch_score(ctx->dm, ctx->cfg.dtype, dev, ctx->ws, lse_out, a, 0, stream), stream,
                 "omnimem_score launch");
 }
 

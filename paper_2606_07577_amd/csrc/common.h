@@ -37,7 +37,28 @@ struct Dims {
   int L, Hq, Hkv, G, d;
   int64_t max_tokens, max_chunk;
   int causal;
+  int krange;   // keys per range of the LSE pass (multiple of 64)
+  int n_kr;     // ranges covering max_tokens
+  int qchunk;   // queries per slice of the column-sum pass (multiple of 64)
+  int n_qc;     // slices covering max_chunk
 };
+
+// Loads through the global address space.  Pointers read from a
+// descriptor are generic; a generic (flat) load also counts against the LDS
+// wait counter, which would make every LDS wait wait for HBM as well.
+template <typename T>
+__device__ inline T gload(const void* p) {
+  typedef const __attribute__((address_space(1))) T global_t;
+  return *(global_t*)(p);
+}
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ inline uint4 gload16(const void* p) {
+  const u32x4 v = gload<u32x4>(p);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// Index of the calling wavefront in its workgroup, as a scalar.
+__device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
 // ---------------------------------------------------------------------------
 // MFMA operand traits.  A 32x32 output tile D[M][N] += A[M][k] B[k][N] is
@@ -58,6 +79,7 @@ template <> struct Mfma<uint16_t> {  // bf16 storage, v_mfma_f32_32x32x16_bf16
   __device__ static inline frag load(const uint16_t* p) {
     return *reinterpret_cast<const frag*>(p);
   }
+  __device__ static inline frag gload(const uint16_t* p) { return omnimem::gload<frag>(p); }
   __device__ static inline frag zero() { return frag{}; }
 };
 
@@ -69,6 +91,7 @@ template <> struct Mfma<float> {  // fp32, v_mfma_f32_32x32x2_f32
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
   __device__ static inline frag load(const float* p) { return *p; }
+  __device__ static inline frag gload(const float* p) { return omnimem::gload<float>(p); }
   __device__ static inline frag zero() { return 0.0f; }
 };
 
@@ -89,7 +112,7 @@ __device__ inline void stage_rows(T* lds, const T* src, int64_t row_stride, int 
   for (int c = threadIdx.x; c < rows * CPR; c += blockDim.x) {
     const int r = c / CPR, x = c % CPR;
     uint4 val = make_uint4(0, 0, 0, 0);
-    if (r < valid) val = *reinterpret_cast<const uint4*>(src + (int64_t)r * row_stride + x * (16 / sizeof(T)));
+    if (r < valid) val = gload16(src + (int64_t)r * row_stride + x * (16 / sizeof(T)));
     *reinterpret_cast<uint4*>(lds + r * LD + x * (16 / sizeof(T))) = val;
   }
 }
@@ -103,7 +126,7 @@ __device__ inline void stage_rows_gather(T* lds, const T* base, int64_t row_stri
   for (int c = threadIdx.x; c < rows * CPR; c += blockDim.x) {
     const int r = c / CPR, x = c % CPR;
     uint4 val = make_uint4(0, 0, 0, 0);
-    if (r < valid) val = *reinterpret_cast<const uint4*>(base + (int64_t)rows_idx[r] * row_stride + x * (16 / sizeof(T)));
+    if (r < valid) val = gload16(base + (int64_t)rows_idx[r] * row_stride + x * (16 / sizeof(T)));
     *reinterpret_cast<uint4*>(lds + r * LD + x * (16 / sizeof(T))) = val;
   }
 }
@@ -121,7 +144,7 @@ constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
 // Optional launch timing (see omnimem_profile).
 // ---------------------------------------------------------------------------
 enum KernelId {
-  K_LSE, K_COLSUM, K_HEADSUM, K_LISTS, K_PLAN, K_NORMS, K_FILL, K_GRAM, K_GRAM_FINISH, K_ADJ,
+  K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
   K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_COUNT
 };
 struct Profiler;
@@ -140,17 +163,18 @@ void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
 // ---------------------------------------------------------------------------
 struct Workspace {
   LayerDesc* desc;        // [slots][L]
-  float* lse;             // [L][Hq][max_chunk]
-  float* part;            // [L][Hq][max_tokens] per-query-head column sums
-  int* pos;               // [L][max_tokens]  visual rows then audio rows
+  float2* lse_part;       // [L][Hq][n_kr][max_chunk] running (max, sum) in log2 units
+  float* lse2;            // [L][Hq][max_chunk] merged normaliser, log2 units
+  float* part;            // [L][Hq][n_qc][max_tokens] column sums per query head and slice
+  int* pos;               // [L][2][max_tokens] visual rows, audio rows (ascending)
   int* rank;              // [L][max_tokens]  rank of row j inside its modality
   int* counts;            // [L][2]           K_v, K_a
   float* inv_norm;        // [L][Hkv][max_tokens]
   int* best;              // [L][Hkv][max_tokens] ord_f32 of the best cosine
-  int4* items;            // Gram work items
-  int* n_items;           // [1]
-  int64_t items_cap;
-  double* stat_part;      // [L][Hkv][3][4]
+  int4* items;            // [L][items_per_layer] Gram work items (seg, I, J0, J1)
+  int* n_items;           // [L] items used in each layer's slot range
+  int64_t items_per_layer;
+  double* stat_part;      // [L][Hkv][chunks][2][4]
   int* eff;               // [L][2] budgets as applied by select
   int* idx;               // [L][Hkv][max_tokens] fallback for the idx output
   uint32_t* keys;         // [L][Hkv][max_tokens]
@@ -159,10 +183,12 @@ struct Workspace {
 
 // Launchers (each returns hipGetLastError() after its launches).
 hipError_t launch_score(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws,
-                        float* lse_buf, float* a, int need_lse, hipStream_t st);
+                        float* lse_out, float* a, int unused, hipStream_t st);
+void choose_key_ranges(Dims* dm);
+int allocate_part_chunks(const Dims& dm);
 hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
                              const Workspace& ws, float* s, hipStream_t st);
-hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, hipStream_t st);
+hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, int make_plan, hipStream_t st);
 hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspace& ws,
                            const float* a, const float* s, int64_t total, float ratio_r,
                            float temperature, float bmin_frac, float bmax_frac, int32_t* budgets,
@@ -172,6 +198,7 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, const 
                                  const int32_t* budgets, int32_t* idx, hipStream_t st);
 
 constexpr int kGramTile = 128;   // rows per Gram block
+
 constexpr int kGramStrip = 4;    // J blocks per work item
 
 }  // namespace omnimem

@@ -18,55 +18,83 @@ namespace omnimem {
 namespace {
 
 // --- modality lists --------------------------------------------------------
-// Per layer: pos[0 .. K_v) = visual rows ascending, pos[K_v .. N) = audio
-// rows ascending; rank[j] = index of row j inside its modality's list.
+// Per layer: pos[l][0][0 .. K_v) = visual rows ascending, pos[l][1][0 .. K_a)
+// = audio rows ascending; rank[j] = index of row j inside its modality's
+// list.  One pass, 16 rows per thread.
+constexpr int kListPer = 16;
+
+__device__ inline int64_t plan_F(int64_t n);
+
 __global__ __launch_bounds__(1024) void modality_lists(const LayerDesc* __restrict__ layers, Dims dm,
                                                       int* __restrict__ pos, int* __restrict__ rank,
-                                                      int* __restrict__ counts) {
+                                                      int* __restrict__ counts, int4* __restrict__ items,
+                                                      int* __restrict__ n_items, int64_t items_per_layer,
+                                                      int make_plan) {
   const int l = blockIdx.x;
-  const LayerDesc Ld = layers[l];
-  const int N = Ld.n;
-  const uint8_t* mod = Ld.mod;
+  const int N = layers[l].n;
+  const uint8_t* mod = layers[l].mod;
   __shared__ int wave_tot[16];
-  __shared__ int s_total;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
-
-  // total visual rows
-  int cnt = 0;
-  for (int j = threadIdx.x; j < N; j += blockDim.x) cnt += (mod[j] == 0);
-  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
-  if (lane == 0) wave_tot[wave] = cnt;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int t = 0;
-    for (int w = 0; w < nwaves; ++w) t += wave_tot[w];
-    s_total = t;
-  }
-  __syncthreads();
-  const int kv = s_total;
-  int* P = pos + (int64_t)l * dm.max_tokens;
+  int* Pv = pos + (int64_t)(2 * l) * dm.max_tokens;
+  int* Pa = Pv + dm.max_tokens;
   int* R = rank + (int64_t)l * dm.max_tokens;
-  int base = 0;  // visual rows before the current tile
-  for (int t0 = 0; t0 < N; t0 += blockDim.x) {
-    const int j = t0 + threadIdx.x;
-    const bool vis = j < N && mod[j] == 0;
-    const unsigned long long bal = __ballot(vis);
-    const int before = __popcll(bal & ((1ull << lane) - 1ull));
-    __syncthreads();
-    if (lane == 0) wave_tot[wave] = __popcll(bal);
-    __syncthreads();
-    int wbase = base;
-    for (int w = 0; w < wave; ++w) wbase += wave_tot[w];
-    if (j < N) {
-      const int rv = wbase + before;   // visual rows before j
-      if (vis) { P[rv] = j; R[j] = rv; }
-      else { const int ra = j - rv; P[kv + ra] = j; R[j] = ra; }
+  int carry = 0;  // visual rows before the current span
+  for (int base = 0; base < N; base += (int)blockDim.x * kListPer) {
+    const int j0 = base + (int)threadIdx.x * kListPer;
+    uint8_t m[kListPer];
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < kListPer; ++e) {
+      m[e] = j0 + e < N ? mod[j0 + e] : 1;
+      cnt += m[e] == 0;
     }
-    int tile = 0;
-    for (int w = 0; w < nwaves; ++w) tile += wave_tot[w];
-    base += tile;
+    int incl = cnt;  // inclusive scan over the wave
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    __syncthreads();
+    if (lane == 63) wave_tot[wave] = incl;
+    __syncthreads();
+    int rv = carry + incl - cnt, span = 0;
+    for (int w = 0; w < nwaves; ++w) {
+      rv += w < wave ? wave_tot[w] : 0;
+      span += wave_tot[w];
+    }
+#pragma unroll
+    for (int e = 0; e < kListPer; ++e) {
+      const int j = j0 + e;
+      if (j >= N) break;
+      if (m[e] == 0) { Pv[rv] = j; R[j] = rv; ++rv; }
+      else { const int ra = j - rv; Pa[ra] = j; R[j] = ra; }
+    }
+    carry += span;
   }
+  const int kv = carry;
   if (threadIdx.x == 0) { counts[2 * l] = kv; counts[2 * l + 1] = N - kv; }
+  if (!make_plan) return;
+
+  // Gram work plan of this layer, in its own slot range [l * per_layer, ...):
+  // segment (g, mu) with T = ceil(K / 128) row blocks owns, for row block
+  // I, ceil((T - I) / S) items of up to S column blocks.
+  __syncthreads();
+  int4* it = items + (int64_t)l * items_per_layer;
+  int64_t ibase = 0;
+  for (int g = 0; g < dm.Hkv; ++g)
+    for (int smu = 0; smu < 2; ++smu) {
+      const int K = smu ? N - kv : kv;
+      const int T = (K + kGramTile - 1) / kGramTile;
+      const int64_t FT = plan_F(T);
+      const int seg = (l * dm.Hkv + g) * 2 + smu;
+      for (int I = threadIdx.x; I < T; I += blockDim.x) {
+        int64_t o = ibase + FT - plan_F(T - I);
+        for (int J0 = I; J0 < T; J0 += kGramStrip, ++o)
+          if (o < items_per_layer) it[o] = make_int4(seg, I, J0, min(T, J0 + kGramStrip));
+      }
+      ibase += FT;
+    }
+  if (threadIdx.x == 0) n_items[l] = (int)min<int64_t>(ibase, items_per_layer);
 }
 
 // --- Gram work plan ----------------------------------------------------------
@@ -78,36 +106,11 @@ __device__ inline int64_t plan_F(int64_t n) {
   return kGramStrip * q * (q + 1) / 2 + r * (q + 1);
 }
 
-__global__ __launch_bounds__(256) void gram_plan(Dims dm, const int* __restrict__ counts,
-                                                 int4* __restrict__ items, int* __restrict__ n_items,
-                                                 int64_t cap) {
-  const int nseg = dm.L * dm.Hkv * 2;
-  __shared__ int64_t s_base;
-  if (threadIdx.x == 0) s_base = 0;
-  __syncthreads();
-  for (int seg = 0; seg < nseg; ++seg) {
-    const int l = seg / (dm.Hkv * 2), mu = seg & 1;
-    const int K = counts[2 * l + mu];
-    const int T = (K + kGramTile - 1) / kGramTile;
-    const int64_t base = s_base;
-    const int64_t FT = plan_F(T);
-    for (int I = threadIdx.x; I < T; I += blockDim.x) {
-      int64_t off = base + FT - plan_F(T - I);
-      for (int J0 = I; J0 < T; J0 += kGramStrip, ++off)
-        if (off < cap) items[off] = make_int4(seg, I, J0, min(T, J0 + kGramStrip));
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) s_base = base + FT;
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) *n_items = (int)min(s_base, cap);
-}
-
 // --- inverse norms -----------------------------------------------------------
 // inv_norm[l][g][j] = 1 / ||u_j|| (0 for a zero row), accumulated in fp64.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void inv_norms(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
-                                                 float* __restrict__ inv) {
+                                                 float* __restrict__ inv, int* __restrict__ best) {
   const int l = blockIdx.z, g = blockIdx.y;
   const LayerDesc Ld = layers[l];
   const int N = Ld.n;
@@ -129,154 +132,194 @@ __global__ __launch_bounds__(256) void inv_norms(const LayerDesc* __restrict__ l
   }
 #pragma unroll
   for (int o = LPR / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
-  if (row < N && sub == 0) inv[((int64_t)l * dm.Hkv + g) * dm.max_tokens + row] = acc > 0.0 ? (float)(1.0 / sqrt(acc)) : 0.0f;
+  if (row < N && sub == 0) {
+    const int64_t o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + row;
+    inv[o] = acc > 0.0 ? (float)(1.0 / sqrt(acc)) : 0.0f;
+    best[o] = kNoPartner;  // the Gram pass merges maxima into this
+  }
 }
 
-__global__ void fill_int(int* __restrict__ p, int64_t n, int v) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
-}
 
 // --- Gram max -------------------------------------------------------------
-// One work item = row block I of a segment against column blocks [J0, J1).
-// Wave w computes the 64 x 64 quadrant (w >> 1, w & 1) of each 128 x 128
-// tile as 2 x 2 MFMA tiles.  Column maxima are reduced per tile and merged
-// at once; row maxima are carried across the strip and merged at the end.
+// One work item = row block I (128 rows) of a segment against column blocks
+// [J0, J1).  Wave w keeps rows w*32 .. w*32+31 of block I as MFMA A operands
+// in registers for the whole item and streams each 128-row column block
+// through double-buffered LDS (B operands, 4 column tiles of 32).  Per
+// element: cos = dot * inv_i * inv_j.  Column maxima are reduced in
+// registers per tile and merged with atomicMax at once; row maxima are
+// carried across the strip and reduced across lanes at the end.  Rows and
+// columns past the segment get a NaN inverse norm, which fmaxf ignores.
 template <typename T, int D>
-__global__ __launch_bounds__(256) void gram_max(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
-                                                const int* __restrict__ pos, const int* __restrict__ counts,
-                                                const float* __restrict__ inv, const int4* __restrict__ items,
-                                                const int* __restrict__ n_items, int* __restrict__ best) {
+struct GramStage {
+  static constexpr int CPR = D * (int)sizeof(T) / 16;
+  static constexpr int PER_THREAD = kGramTile * CPR / 256;
+  static constexpr int LD = D + lds_pad<T>();
+  uint4 r[PER_THREAD];
+  // rows `rows_idx[0 .. valid)` of u; the rest repeat row rows_idx[valid - 1]
+  __device__ inline void load(const T* u, int64_t row_stride, const int* rows_idx, int valid) {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int c = threadIdx.x + i * 256;
+      const int row = c / CPR, x = c % CPR;
+      const int src = rows_idx[min(row, valid - 1)];
+      r[i] = gload16(u + (int64_t)src * row_stride + x * (16 / sizeof(T)));
+    }
+  }
+  __device__ inline void store(T* lds) const {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      const int c = threadIdx.x + i * 256;
+      const int row = c / CPR, x = c % CPR;
+      *reinterpret_cast<uint4*>(lds + row * LD + x * (16 / sizeof(T))) = r[i];
+    }
+  }
+};
+
+// Accumulator register r holds tile row (r >> 2) * 8 + half * 4 + (r & 3):
+// it is the lane's own column when (r >> 2) * 8 + (r & 3) == d.
+__device__ inline void drop_diagonal(floatx16& a, int d) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) a[r] = ((r >> 2) * 8 + (r & 3)) == d ? __builtin_nanf("") : a[r];
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(256, 2) void gram_max(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
+                                                   const int* __restrict__ pos, const int* __restrict__ counts,
+                                                   const float* __restrict__ inv, const int4* __restrict__ items,
+                                                   const int* __restrict__ n_items, int64_t items_per_layer,
+                                                   int* __restrict__ best) {
   using M = Mfma<T>;
+  using S = GramStage<T, D>;
   constexpr int NKS = D / M::KSTEP;
-  constexpr int LD = D + lds_pad<T>();
+  constexpr int LD = S::LD;
   constexpr int TB = kGramTile;
-  __shared__ __attribute__((aligned(16))) T tI[TB * LD];
-  __shared__ __attribute__((aligned(16))) T tJ[TB * LD];
-  __shared__ float invI[TB], invJ[TB];
-  __shared__ int rowsI[TB], rowsJ[TB];
+  __shared__ __attribute__((aligned(16))) T tJ[2][TB * LD];
+  __shared__ float invJ[2][TB];
+  __shared__ int rowsJ[2][TB];
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5;
-  const int wr = wave >> 1, wc = wave & 1;
-  const int total = *n_items;
+  const int wave = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
+  const int64_t total = (int64_t)dm.L * items_per_layer;
 
-  for (int it = blockIdx.x; it < total; it += gridDim.x) {
+  for (int64_t it = blockIdx.x; it < total; it += gridDim.x) {
+    if (it % items_per_layer >= n_items[it / items_per_layer]) continue;  // unused slot
     const int4 item = items[it];
     const int seg = item.x, I = item.y, J0 = item.z, J1 = item.w;
     const int l = seg / (dm.Hkv * 2), g = (seg >> 1) % dm.Hkv, mu = seg & 1;
-    const LayerDesc Ld = layers[l];
     const int K = counts[2 * l + mu];
-    const int* P = pos + (int64_t)l * dm.max_tokens + (mu ? counts[2 * l] : 0);
-    const T* u = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
+    const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
+    const int64_t kv_rs = layers[l].kv_rs;
+    const T* u = reinterpret_cast<const T*>(on_keys ? layers[l].k : layers[l].v) + (int64_t)g * layers[l].kv_hs;
     const float* inv_g = inv + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
     int* best_g = best + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
 
-    __syncthreads();  // previous item done with the LDS tiles
+    // this wave's 32 rows of block I: A fragments and inverse norms
     const int validI = min(TB, K - I * TB);
-    if (threadIdx.x < TB) {
-      const int r = threadIdx.x;
-      const int row = r < validI ? P[I * TB + r] : 0;
-      rowsI[r] = row;
-      invI[r] = r < validI ? inv_g[row] : 0.0f;
+    const int r0 = wave * 32;
+    const bool wave_rows = r0 < validI;
+    const int my_row = r0 + (lane & 31);
+    const int my_pos = P[I * TB + min(my_row, validI - 1)];
+    typename M::frag af[NKS];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+      af[ks] = M::gload(u + (int64_t)my_pos * kv_rs + ks * M::KSTEP + half * M::PER_LANE);
+    float ri[16];  // inverse norms of the 16 rows this lane's accumulators hold
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = r0 + acc_row(r, lane);
+      ri[r] = row < validI ? inv_g[P[I * TB + row]] : __builtin_nanf("");
     }
-    __syncthreads();
-    stage_rows_gather<T, D>(tI, u, Ld.kv_rs, rowsI, TB, validI);
-
-    float rmax[2][16];
+    float rmax[16];
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) rmax[rt][r] = -INFINITY;
+    for (int r = 0; r < 16; ++r) rmax[r] = -INFINITY;
 
-    for (int J = J0; J < J1; ++J) {
-      const int validJ = min(TB, K - J * TB);
-      __syncthreads();
+    S pre;
+    __syncthreads();  // the previous item is done with the LDS buffers
+    {
+      const int validJ = min(TB, K - J0 * TB);
       if (threadIdx.x < TB) {
-        const int r = threadIdx.x;
-        const int row = r < validJ ? P[J * TB + r] : 0;
-        rowsJ[r] = row;
-        invJ[r] = r < validJ ? inv_g[row] : 0.0f;
+        const int c = threadIdx.x;
+        const int p = P[J0 * TB + min(c, validJ - 1)];
+        rowsJ[0][c] = p;
+        invJ[0][c] = c < validJ ? inv_g[p] : __builtin_nanf("");
       }
       __syncthreads();
-      stage_rows_gather<T, D>(tJ, u, Ld.kv_rs, rowsJ, TB, validJ);
-      __syncthreads();
-
-      floatx16 acc[2][2];
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int ct = 0; ct < 2; ++ct) acc[rt][ct] = floatx16{};
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        typename M::frag af[2], bf[2];
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-          af[rt] = M::load(tI + (wr * 64 + rt * 32 + (lane & 31)) * LD + ks * M::KSTEP + half * M::PER_LANE);
-#pragma unroll
-        for (int ct = 0; ct < 2; ++ct)
-          bf[ct] = M::load(tJ + (wc * 64 + ct * 32 + (lane & 31)) * LD + ks * M::KSTEP + half * M::PER_LANE);
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-          for (int ct = 0; ct < 2; ++ct) acc[rt][ct] = M::mma(af[rt], bf[ct], acc[rt][ct]);
+      pre.load(u, kv_rs, rowsJ[0], validJ);
+      pre.store(tJ[0]);
+    }
+    int buf = 0;
+    for (int J = J0; J < J1; ++J, buf ^= 1) {
+      const bool has_next = J + 1 < J1;
+      int validJn = 0;
+      if (has_next) {
+        validJn = min(TB, K - (J + 1) * TB);
+        if (threadIdx.x < TB) {
+          const int c = threadIdx.x;
+          const int p = P[(J + 1) * TB + min(c, validJn - 1)];
+          rowsJ[buf ^ 1][c] = p;
+          invJ[buf ^ 1][c] = c < validJn ? inv_g[p] : __builtin_nanf("");
+        }
       }
-
-      // Exclude the diagonal and the padding rows/columns of ragged blocks.
-      const bool masked = (I == J) || validI < TB || validJ < TB;
-      float ri[2][16];
+      __syncthreads();  // tJ[buf] staged; rowsJ[buf ^ 1] written
+      if (has_next) pre.load(u, kv_rs, rowsJ[buf ^ 1], validJn);
+      const int validJ = min(TB, K - J * TB);
+      if (wave_rows) {
+        floatx16 acc[4];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+        for (int ct = 0; ct < 4; ++ct) acc[ct] = floatx16{};
+        const T* b0 = tJ[buf] + (lane & 31) * LD + half * M::PER_LANE;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ri[rt][r] = invI[wr * 64 + rt * 32 + acc_row(r, lane)];
-      float cmax[2];
+        for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
-        const int cj = wc * 64 + ct * 32 + (lane & 31);
-        const float ij = invJ[cj];
-        float cm = -INFINITY;
+          for (int ct = 0; ct < 4; ++ct)
+            acc[ct] = M::mma(af[ks], M::load(b0 + ct * 32 * LD + ks * M::KSTEP), acc[ct]);
+        if (I == J) {
+          // the pair (row, row) lies in column tile `wave`: drop it
+          const int d = (lane & 31) - half * 4;
+          switch (wave) {
+            case 0: drop_diagonal(acc[0], d); break;
+            case 1: drop_diagonal(acc[1], d); break;
+            case 2: drop_diagonal(acc[2], d); break;
+            default: drop_diagonal(acc[3], d); break;
+          }
+        }
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
+        for (int ct = 0; ct < 4; ++ct) {
+          const int cj = ct * 32 + (lane & 31);
+          const float ij = invJ[buf][cj];
+          float cm = -INFINITY;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int ri_ = wr * 64 + rt * 32 + acc_row(r, lane);
-            float dot = acc[rt][ct][r];
-            if (masked && (ri_ >= validI || cj >= validJ || (I == J && ri_ == cj))) dot = -INFINITY;
-            cm = fmaxf(cm, dot * ri[rt][r]);
-            rmax[rt][r] = fmaxf(rmax[rt][r], dot * ij);
+            cm = fmaxf(cm, acc[ct][r] * ri[r]);
+            rmax[r] = fmaxf(rmax[r], acc[ct][r] * ij);
           }
-        cmax[ct] = cm;
+          // both row halves of column cj, scaled by its inverse norm
+          cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
+          if (half == 0 && cj < validJ && cm > -INFINITY) {
+            const float c = fminf(1.0f, fmaxf(-1.0f, cm * ij));
+            atomicMax(best_g + rowsJ[buf][cj], ord_f32(c));
+          }
+        }
       }
-      // Column maxima: combine the two row halves, scale, merge globally.
+      if (has_next) pre.store(tJ[buf ^ 1]);
+    }
+    // Row maxima: reduce over the 32 lanes of each half, then merge.
+    if (wave_rows) {
 #pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
-        float cm = fmaxf(cmax[ct], __shfl_xor(cmax[ct], 32, 64));
-        const int cj = wc * 64 + ct * 32 + (lane & 31);
-        if (half == ct && cj < validJ && cm != -INFINITY) {
-          const float c = fminf(1.0f, fmaxf(-1.0f, cm * invJ[cj]));
-          atomicMax(best_g + rowsJ[cj], ord_f32(c));
+      for (int r = 0; r < 16; ++r) {
+        float v = rmax[r];
+#pragma unroll
+        for (int o = 16; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+        rmax[r] = v;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = r0 + acc_row(r, lane);
+        if ((lane & 31) == r && row < validI && rmax[r] > -INFINITY) {
+          const float c = fminf(1.0f, fmaxf(-1.0f, rmax[r] * ri[r]));
+          atomicMax(best_g + P[I * TB + row], ord_f32(c));
         }
       }
     }
-    // Row maxima: reduce across the 32 lanes that share each row.
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = rmax[rt][r];
-#pragma unroll
-        for (int o = 16; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-        rmax[rt][r] = v;
-      }
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ri_ = wr * 64 + rt * 32 + acc_row(r, lane);
-        // lane (lane & 31) == r writes row r of its half
-        if ((lane & 31) == r && ri_ < validI && rmax[rt][r] != -INFINITY) {
-          const float c = fminf(1.0f, fmaxf(-1.0f, rmax[rt][r] * invI[ri_]));
-          atomicMax(best_g + rowsI[ri_], ord_f32(c));
-        }
-      }
   }
 }
 
@@ -317,7 +360,7 @@ __global__ void adjacent_cos(const LayerDesc* __restrict__ layers, Dims dm, int 
   if (j >= N) return;
   const int mu = Ld.mod[j] ? 1 : 0;
   const int K = counts[2 * l + mu];
-  const int* P = pos + (int64_t)l * dm.max_tokens + (mu ? counts[2 * l] : 0);
+  const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
   const int t = rank[(int64_t)l * dm.max_tokens + j];
   const T* u = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
   const T* x = u + (int64_t)j * Ld.kv_rs;
@@ -336,27 +379,26 @@ void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, c
     OMNIMEM_LAUNCH(ws, K_ADJ, st, adjacent_cos<T, D><<<gtok, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts, s));
     return;
   }
-  OMNIMEM_LAUNCH(ws, K_PLAN, st, gram_plan<<<1, 256, 0, st>>>(dm, ws.counts, ws.items, ws.n_items, ws.items_cap));
   const dim3 gnorm((unsigned)((dm.max_tokens + 15) / 16), dm.Hkv, dm.L);
-  OMNIMEM_LAUNCH(ws, K_NORMS, st, inv_norms<T, D><<<gnorm, 256, 0, st>>>(desc, dm, on_keys, ws.inv_norm));
-  const int64_t nbest = (int64_t)dm.L * dm.Hkv * dm.max_tokens;
-  OMNIMEM_LAUNCH(ws, K_FILL, st, fill_int<<<(unsigned)std::min<int64_t>((nbest + 255) / 256, 4096), 256, 0, st>>>(ws.best, nbest, kNoPartner));
-  const unsigned grid = (unsigned)std::min<int64_t>(ws.items_cap, 2048);
+  OMNIMEM_LAUNCH(ws, K_NORMS, st, inv_norms<T, D><<<gnorm, 256, 0, st>>>(desc, dm, on_keys, ws.inv_norm, ws.best));
+  const unsigned grid = (unsigned)std::min<int64_t>((int64_t)dm.L * ws.items_per_layer, 2048);
   OMNIMEM_LAUNCH(ws, K_GRAM, st, gram_max<T, D><<<grid, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.counts,
-                                       ws.inv_norm, ws.items, ws.n_items, ws.best));
+                                       ws.inv_norm, ws.items, ws.n_items, ws.items_per_layer, ws.best));
   OMNIMEM_LAUNCH(ws, K_GRAM_FINISH, st, gram_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.best, s));
 }
 
 }  // namespace
 
-hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, hipStream_t st) {
-  OMNIMEM_LAUNCH(ws, K_LISTS, st, modality_lists<<<dm.L, 1024, 0, st>>>(desc, dm, ws.pos, ws.rank, ws.counts));
+hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, int make_plan, hipStream_t st) {
+  OMNIMEM_LAUNCH(ws, K_LISTS, st,
+                 modality_lists<<<dm.L, 1024, 0, st>>>(desc, dm, ws.pos, ws.rank, ws.counts, ws.items, ws.n_items,
+                                                       ws.items_per_layer, make_plan));
   return hipGetLastError();
 }
 
 hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
                              const Workspace& ws, float* s, hipStream_t st) {
-  hipError_t e = launch_lists(dm, desc, ws, st);
+  hipError_t e = launch_lists(dm, desc, ws, sim == 0, st);
   if (e != hipSuccess) return e;
   if (dtype == 0) {
     if (dm.d == 128) launch_typed<uint16_t, 128>(dm, sim, on_keys, desc, ws, s, st);

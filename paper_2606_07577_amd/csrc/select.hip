@@ -15,7 +15,10 @@ namespace omnimem {
 
 namespace {
 
-constexpr int kSelThreads = 512;
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kLdsKeys = 32768;   // member keys of a segment held in LDS (128 KB)
+constexpr int kBins = 2048;       // radix digit of up to 11 bits
 
 __device__ inline uint32_t psi_key(float a, float s, float lambda) {
   s = fminf(1.0f, fmaxf(-1.0f, s));
@@ -25,21 +28,35 @@ __device__ inline uint32_t psi_key(float a, float s, float lambda) {
   return __float_as_uint(psi + 0.0f);  // +0 for -0: nonnegative floats order as uints
 }
 
-// Exclusive prefix of `flag` over the block in thread order, and the total.
+// Exclusive prefix of `flag` over the block in thread order; *total gets the
+// block's count.  Uses wave_tot[kSelWaves] and two barriers.
 __device__ inline int block_prefix(bool flag, int* wave_tot, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const unsigned long long bal = __ballot(flag);
   const int before = __popcll(bal & ((1ull << lane) - 1ull));
   __syncthreads();
   if (lane == 0) wave_tot[wave] = __popcll(bal);
   __syncthreads();
   int base = 0, tot = 0;
-  for (int w = 0; w < nw; ++w) {
-    if (w < wave) base += wave_tot[w];
-    tot += wave_tot[w];
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    const int c = wave_tot[w];
+    base += w < wave ? c : 0;
+    tot += c;
   }
   *total = tot;
   return base + before;
+}
+
+// Inclusive prefix sum of v over the 64 lanes.
+__device__ inline int wave_inclusive(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  return v;
 }
 
 __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restrict__ layers, Dims dm, float lambda,
@@ -47,68 +64,82 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
                                                         const int32_t* __restrict__ budgets,
                                                         uint32_t* __restrict__ keys, int32_t* __restrict__ idx,
                                                         int* __restrict__ eff) {
+  __shared__ uint32_t skey[kLdsKeys];
+  __shared__ int hist[kBins];
+  __shared__ int wave_tot[kSelWaves];
+  __shared__ int s_bin, s_need;
+
   const int mu = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
-  const LayerDesc Ld = layers[l];
-  const int N = Ld.n;
-  const uint8_t* mod = Ld.mod;
+  const int N = layers[l].n;
+  const uint8_t* mod = layers[l].mod;
   const int64_t off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
   const float* ag = a + off;
   const float* sg = s + off;
-  uint32_t* kg = keys + off;
+  uint32_t* kg = keys + off;   // keys by working-set row
   int32_t* ig = idx + off;
-  __shared__ int hist[256];
-  __shared__ int wave_tot[16];
-  __shared__ int s_k, s_bin, s_need;
 
-  // keys of this modality's rows, and their count
-  int cnt = 0;
-  for (int j = threadIdx.x; j < N; j += blockDim.x) {
-    if ((mod[j] ? 1 : 0) != mu) continue;
-    kg[j] = psi_key(ag[j], sg[j], lambda);
-    ++cnt;
+  // Pass 0: keys of this modality's rows, by row in global memory and by
+  // member rank in LDS.
+  int K = 0;
+  for (int t0 = 0; t0 < N; t0 += kSelThreads) {
+    const int j = t0 + threadIdx.x;
+    const bool member = j < N && (mod[j] ? 1 : 0) == mu;
+    int cnt;
+    const int rank = K + block_prefix(member, wave_tot, &cnt);
+    if (member) {
+      const uint32_t key = psi_key(ag[j], sg[j], lambda);
+      kg[j] = key;
+      if (rank < kLdsKeys) skey[rank] = key;
+    }
+    K += cnt;
   }
-  for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
-  if (threadIdx.x == 0) s_k = 0;
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) atomicAdd(&s_k, cnt);
-  __syncthreads();
-  const int K = s_k;
-  const int K_other = N - K;
-  const int Kv = mu ? K_other : K;
-  const int m_req = budgets[2 * l + mu];
-  const int M = min(max(m_req, 0), K);
+  const int M = min(max(budgets[2 * l + mu], 0), K);
+  const int Kv = mu ? N - K : K;
   const int Mv = mu ? min(max(budgets[2 * l], 0), Kv) : M;
   if (g == 0 && threadIdx.x == 0) eff[2 * l + mu] = M;
   const int out0 = mu ? Mv : 0;
+  const bool in_lds = K <= kLdsKeys;
+  __syncthreads();
 
-  // threshold key and how many rows equal to it are kept
+  // Radix select of the M-th largest key, digits of 11, 11 and 10 bits.
   uint32_t thr = 0;
   int take_eq = 0;
   const bool all = M >= K;
   if (!all && M > 0) {
     uint32_t prefix = 0, mask = 0;
     int need = M;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int b = threadIdx.x; b < 256; b += blockDim.x) hist[b] = 0;
+    for (int pass = 0; pass < 3; ++pass) {
+      const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+      const uint32_t dmask = pass == 2 ? 1023u : 2047u;
+      for (int b = threadIdx.x; b < kBins; b += kSelThreads) hist[b] = 0;
       __syncthreads();
-      for (int j = threadIdx.x; j < N; j += blockDim.x) {
-        if ((mod[j] ? 1 : 0) != mu) continue;
-        const uint32_t key = kg[j];
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1);
-      }
-      __syncthreads();
-      if (threadIdx.x == 0) {
-        int cum = 0, b = 255;
-        for (; b > 0; --b) {
-          if (cum + hist[b] >= need) break;
-          cum += hist[b];
+      if (in_lds) {
+        for (int r = threadIdx.x; r < K; r += kSelThreads) {
+          const uint32_t key = skey[r];
+          if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1);
         }
-        s_bin = b;
-        s_need = need - cum;
+      } else {
+        for (int j = threadIdx.x; j < N; j += kSelThreads) {
+          if ((mod[j] ? 1 : 0) != mu) continue;
+          const uint32_t key = kg[j];
+          if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1);
+        }
       }
+      __syncthreads();
+      // Counts above each bin, from the top: thread t owns bins 2047-2t, 2046-2t.
+      const int b1 = kBins - 1 - 2 * (int)threadIdx.x, b2 = b1 - 1;
+      const int h1 = hist[b1], h2 = hist[b2];
+      const int incl = wave_inclusive(h1 + h2);
+      const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+      if (lane == 63) wave_tot[wave] = incl;
+      __syncthreads();
+      int above = incl - (h1 + h2);
+      for (int w = 0; w < wave; ++w) above += wave_tot[w];
+      if (above < need && need <= above + h1) { s_bin = b1; s_need = need - above; }
+      else if (above + h1 < need && need <= above + h1 + h2) { s_bin = b2; s_need = need - above - h1; }
       __syncthreads();
       prefix |= (uint32_t)s_bin << shift;
-      mask |= 255u << shift;
+      mask |= dmask << shift;
       need = s_need;
       __syncthreads();
     }
@@ -116,14 +147,13 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     take_eq = need;
   }
 
-  // ordered emission: rows above the threshold, then the first `take_eq`
-  // rows equal to it, all in ascending row order
+  // Ordered emission: rows above the threshold and the first `take_eq` rows
+  // equal to it, in ascending row order.
   int eq_seen = 0, emitted = 0;
-  for (int t0 = 0; t0 < N; t0 += blockDim.x) {
+  for (int t0 = 0; t0 < N; t0 += kSelThreads) {
     const int j = t0 + threadIdx.x;
     const bool member = j < N && (mod[j] ? 1 : 0) == mu;
-    uint32_t key = 0;
-    if (member) key = kg[j];
+    const uint32_t key = member ? kg[j] : 0u;
     const bool eq = member && !all && key == thr;
     int eq_tot;
     const int eq_rank = eq_seen + block_prefix(eq, wave_tot, &eq_tot);

@@ -217,8 +217,9 @@ def test_caller_supplied_lse_matches_computed():
     step.set_lse_inputs(lse)
     step.score(lse_out=True)
     _sync()
-    np.testing.assert_array_equal(step.host("lse", 0), c.lse[0])
-    np.testing.assert_array_equal(step.host("a", 0), c.a[0])
+    np.testing.assert_array_equal(step.host("lse", 0), c.lse[0])  # passed through unchanged
+    # the given lse is the computed one rounded to natural log: a agrees to a few ulp
+    np.testing.assert_allclose(step.host("a", 0), c.a[0], rtol=2e-6, atol=0)
     step.close()
 
 
