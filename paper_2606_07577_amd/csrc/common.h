@@ -95,6 +95,18 @@ template <> struct Mfma<float> {  // fp32, v_mfma_f32_32x32x2_f32
   __device__ static inline frag zero() { return 0.0f; }
 };
 
+// Workgroups are dispatched to the 8 XCDs round robin (block b on XCD
+// b % 8).  With the grid padded to a multiple of 8, this bijection maps
+// consecutive logical ids onto the same XCD, so workgroups that share data
+// share one L2.
+constexpr int kXcds = 8;
+__host__ __device__ inline unsigned xcd_grid(int64_t logical_blocks) {
+  return (unsigned)((logical_blocks + kXcds - 1) / kXcds * kXcds);
+}
+__device__ inline int xcd_swizzle(unsigned b, unsigned grid) {
+  return (int)((b % kXcds) * (grid / kXcds) + b / kXcds);
+}
+
 // Row of the 32x32 output tile held by accumulator register r of lane l.
 __device__ inline int acc_row(int r, int lane) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }
 

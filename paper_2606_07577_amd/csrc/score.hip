@@ -37,56 +37,133 @@ __device__ inline float max16(const floatx16& v) {
   return fmaxf(fmaxf(fmaxf(a, b), fmaxf(c, d)), fmaxf(e, v[15]));
 }
 
-// Register prefetch of one LDS stage: kTile rows of D elements.
+// One LDS stage of kTile rows of D elements, unpadded.  The 16-byte chunk c
+// of row r is stored at chunk position c ^ (r & XM): the 16 rows that a
+// quarter-wave reads at the same chunk land on 16 different bank groups.
+// Rows are copied by the global-to-LDS DMA path (global_load_lds_dwordx4),
+// which writes 16 bytes per lane at consecutive LDS slots: no registers and
+// no LDS store instructions.
 template <typename T, int D>
-struct Stage {
-  static constexpr int CPR = D * (int)sizeof(T) / 16;           // 16-byte chunks per row
-  static constexpr int PER_THREAD = kTile * CPR / kThreads;     // chunks per thread
-  static constexpr int LD = D + lds_pad<T>();
-  uint4 r[PER_THREAD];
+struct SwzTile {
+  static constexpr int ROWB = D * (int)sizeof(T);   // bytes per row
+  static constexpr int CPR = ROWB / 16;             // chunks per row
+  static constexpr int XM = (CPR < 16 ? CPR : 16) - 1;
+  static constexpr int EPC = 16 / (int)sizeof(T);   // elements per chunk
+  static constexpr int ELEMS = kTile * D;
+  static constexpr int INSTR_PER_WAVE = kTile * CPR / 64 / 4;  // 1 KB copies per wave
 
-  // Rows at or past `valid` (>= 1) repeat the last valid row: the loads
-  // need no branch and no wait, and consumers mask those rows out.
-  __device__ inline void load(const T* src, int64_t row_stride, int valid) {
+  // Byte offset of element e of row r.
+  __device__ static inline int off(int r, int e) {
+    return r * ROWB + (((e / EPC) ^ (r & XM)) << 4) + (e % EPC) * (int)sizeof(T);
+  }
+  // Copy rows src[0 .. kTile) (rows at or past `valid` >= 1 repeat row
+  // valid - 1) into `lds`.  Every thread of the block takes part.
+  __device__ static inline void dma(T* lds, const T* src, int64_t row_stride, int valid) {
+    const int w = wave_id(), ln = threadIdx.x & 63;
 #pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = threadIdx.x + i * kThreads;
-      const int row = c / CPR, x = c % CPR;
-      r[i] = gload16(src + (int64_t)min(row, valid - 1) * row_stride + x * (16 / sizeof(T)));
+    for (int j = 0; j < INSTR_PER_WAVE; ++j) {
+      const int J = w * INSTR_PER_WAVE + j;
+      const int slot = J * 64 + ln;
+      const int row = slot / CPR, pos = slot % CPR;
+      const int c = pos ^ (row & XM);
+      const T* g = src + (int64_t)min(row, valid - 1) * row_stride + c * EPC;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                       (__attribute__((address_space(3))) void*)(lds + J * 64 * EPC), 16, 0, 0);
     }
   }
-  __device__ inline void store(T* lds) const {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = threadIdx.x + i * kThreads;
-      const int row = c / CPR, x = c % CPR;
-      *reinterpret_cast<uint4*>(lds + row * LD + x * (16 / sizeof(T))) = r[i];
-    }
+  // MFMA fragment of row r for k-step ks, lane half `half`.
+  template <typename M>
+  __device__ static inline typename M::frag frag(const T* lds, int r, int ks, int half) {
+    const char* base = reinterpret_cast<const char*>(lds);
+    return M::load(reinterpret_cast<const T*>(base + off(r, ks * M::KSTEP + half * M::PER_LANE)));
   }
 };
+
+// A wave's DMA copies count as vector-memory loads; s_barrier does not wait
+// for them on gfx950, so each wave drains its own copies before the barrier
+// that hands the tile to the other waves.
+__device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Interleave `nm` MFMAs with the VALU work of the same basic block:
+// groups of one MFMA followed by `nv` VALU instructions.
+#define OMNIMEM_INTERLEAVE(nm, nv)                          \
+  do {                                                      \
+    _Pragma("unroll") for (int _i = 0; _i < (nm); ++_i) {   \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    \
+      __builtin_amdgcn_sched_group_barrier(0x002, (nv), 0); \
+    }                                                       \
+  } while (0)
+
+__device__ inline float max3f(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
+
+// 16 MFMAs: one 32-row block of an LDS stage against two 32-column blocks
+// of register operands; each LDS fragment feeds two MFMAs.
+template <typename M, typename Tile, int NKS, typename T>
+__device__ inline void mma_rows(floatx16 (&acc)[2], const T* lds, int row, int half,
+                                const typename M::frag (&b)[2][NKS]) {
+  acc[0] = floatx16{};
+  acc[1] = floatx16{};
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const typename M::frag f = Tile::template frag<M>(lds, row, ks, half);
+    acc[0] = M::mma(f, b[0][ks], acc[0]);
+    acc[1] = M::mma(f, b[1][ks], acc[1]);
+  }
+}
+
+// Running (max, sum) of exp2(sl2 * score) over the 16 scores of one query
+// that a lane holds in an accumulator.
+__device__ inline void online_update(const floatx16& acc, float sl2, float& m, float& lsum) {
+  float mx = acc[0];
+#pragma unroll
+  for (int r = 1; r < 15; r += 2) mx = max3f(mx, acc[r], acc[r + 1]);
+  mx = fmaxf(mx, acc[15]);
+  const float mnew = fmaxf(m, mx * sl2);
+  const float neg = -mnew;
+  float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; r += 2) {
+    s0 += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r], sl2, neg));
+    s1 += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[r + 1], sl2, neg));
+  }
+  lsum = lsum * __builtin_amdgcn_exp2f(m - mnew) + (s0 + s1);
+  m = mnew;
+}
 
 // Pass 1: for the 256 queries [q0, q0+256) of head h and the keys
 // [kr0, kr1) of one range, the per-query running max m and sum l of
 // exp2(scale_log2 * q.k), merged over both lanes that share a query.
 // MFMA tile: rows = 32 keys (A from LDS), columns = 32 queries (B in
 // registers); each lane owns one query and 16 of its keys per tile.
+// Software pipeline inside each wave: the MFMAs of one 32-key row block
+// run while the exp/sum work of the previous row block executes; key tiles
+// arrive by DMA one tile ahead into the LDS stage just consumed.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restrict__ layers, Dims dm,
                                                         float2* __restrict__ part) {
   using M = Mfma<T>;
-  using S = Stage<T, D>;
+  using Tl = SwzTile<T, D>;
   constexpr int NKS = D / M::KSTEP;
-  constexpr int LD = S::LD;
-  __shared__ __attribute__((aligned(16))) T ktile[2][kTile * LD];
+  constexpr int NV = (D == 128 && sizeof(T) == 2) ? 7 : 2;  // VALU per MFMA in the interleave
+  __shared__ __attribute__((aligned(16))) T kt0[Tl::ELEMS];
+  __shared__ __attribute__((aligned(16))) T kt1[Tl::ELEMS];
 
-  const int l = blockIdx.z / dm.Hq, h = blockIdx.z % dm.Hq;
+  // Workgroups sharing a query head (hence its KV head's keys) run on the
+  // same XCD: consecutive logical ids go to one XCD's L2.
+  const int qblocks = (int)((dm.max_chunk + kBlockRows - 1) / kBlockRows);
+  const int logical = xcd_swizzle(blockIdx.x, gridDim.x);
+  if (logical >= dm.n_kr * qblocks * dm.L * dm.Hq) return;
+  const int range = logical % dm.n_kr;
+  const int qblk = (logical / dm.n_kr) % qblocks;
+  const int lh = logical / (dm.n_kr * qblocks);
+  const int l = lh / dm.Hq, h = lh % dm.Hq;
   const LayerDesc Ld = layers[l];
   if (Ld.lse_in) return;
   const int C = Ld.n_chunk, N = Ld.n, nc = Ld.n_cache;
-  const int q0 = blockIdx.y * kBlockRows;
+  const int q0 = qblk * kBlockRows;
   if (q0 >= C) return;
   const int kend_blk = dm.causal ? min(N, nc + min(q0 + kBlockRows, C)) : N;
-  const int kr0 = blockIdx.x * dm.krange;
+  const int kr0 = range * dm.krange;
   if (kr0 >= kend_blk) return;
   const int kr1 = min(kr0 + dm.krange, kend_blk);
 
@@ -94,80 +171,83 @@ __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restr
   const int g = h / dm.G;
   const T* q = reinterpret_cast<const T*>(Ld.q) + (int64_t)h * Ld.q_hs;
   const T* k = reinterpret_cast<const T*>(Ld.k) + (int64_t)g * Ld.kv_hs;
+  const int64_t kv_rs = Ld.kv_rs;
   const int qw = q0 + wave * kRowsPerWave;
   const bool active = qw < C;
   const int kend_wave = min(kr1, dm.causal ? min(N, nc + min(qw + kRowsPerWave, C)) : N);
 
+  // first tiles on their way before the query fragments are loaded
+  Tl::dma(kt0, k + (int64_t)kr0 * kv_rs, kv_rs, min(kTile, N - kr0));
+  if (kr0 + kTile < kr1) Tl::dma(kt1, k + (int64_t)(kr0 + kTile) * kv_rs, kv_rs, min(kTile, N - kr0 - kTile));
+
   typename M::frag qf[2][NKS];
 #pragma unroll
   for (int cb = 0; cb < 2; ++cb) {
-    const int my_q = qw + cb * 32 + (lane & 31);
+    const int my_q = min(qw + cb * 32 + (lane & 31), C - 1);
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
-      qf[cb][ks] = my_q < C ? M::gload(q + (int64_t)my_q * Ld.q_rs + ks * M::KSTEP + half * M::PER_LANE)
-                            : M::zero();
+      qf[cb][ks] = M::gload(q + (int64_t)my_q * Ld.q_rs + ks * M::KSTEP + half * M::PER_LANE);
   }
   const float sl2 = Ld.scale_log2;
   float m[2] = {-1e30f, -1e30f}, lsum[2] = {0.0f, 0.0f};
 
-  S pre;
-  pre.load(k + (int64_t)kr0 * Ld.kv_rs, Ld.kv_rs, min(kTile, N - kr0));
-  pre.store(ktile[0]);
-  __syncthreads();
-  int buf = 0;
-  for (int t = kr0; t < kr1; t += kTile, buf ^= 1) {
-    const bool has_next = t + kTile < kr1;
-    if (has_next) pre.load(k + (int64_t)(t + kTile) * Ld.kv_rs, Ld.kv_rs, min(kTile, N - t - kTile));
-    if (active && t < kend_wave) {
-      floatx16 acc[2][2];
+  // Scores of key row kb + off, off = acc_row(r) - half*4 (a constant), are
+  // kept iff off <= lim; a 32-key row block needs masking only where it
+  // passes the wave's key end or its first query's causal horizon.
+  auto need_mask = [&](int kb) {
+    return kb + 32 > kend_wave || (dm.causal && kb + 31 - nc > qw);
+  };
+  auto apply_mask = [&](floatx16 (&acc)[2], int kb) {
+    const int base = kb + half * 4;
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
+    for (int cb = 0; cb < 2; ++cb) {
+      int lim = kend_wave - 1 - base;
+      if (dm.causal) lim = min(lim, qw + cb * 32 + (lane & 31) + nc - base);
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = floatx16{};
-      const T* a0 = ktile[buf] + (lane & 31) * LD + half * M::PER_LANE;
-      const T* a1 = a0 + 32 * LD;
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const typename M::frag f0 = M::load(a0 + ks * M::KSTEP);
-        const typename M::frag f1 = M::load(a1 + ks * M::KSTEP);
-        acc[0][0] = M::mma(f0, qf[0][ks], acc[0][0]);
-        acc[0][1] = M::mma(f0, qf[1][ks], acc[0][1]);
-        acc[1][0] = M::mma(f1, qf[0][ks], acc[1][0]);
-        acc[1][1] = M::mma(f1, qf[1][ks], acc[1][1]);
-      }
-#pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
-        const int qcb = qw + cb * 32;
-        // masking only where the tile passes the range or some query's horizon;
-        // key t + off (off = rb*32 + acc_row(r, lane) - half*4, a constant) is
-        // visible iff off <= lim
-        if (t + kTile > kend_wave || (dm.causal && t + kTile - 1 - nc > qcb)) {
-          const int base = t + half * 4;
-          int lim = kend_wave - 1 - base;
-          if (dm.causal) lim = min(lim, qcb + (lane & 31) + nc - base);
-#pragma unroll
-          for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int off = rb * 32 + (r >> 2) * 8 + (r & 3);
-              acc[rb][cb][r] = off <= lim ? acc[rb][cb][r] : -INFINITY;
-            }
-        }
-        const float mx = fmaxf(max16(acc[0][cb]), max16(acc[1][cb])) * sl2;
-        const float mnew = fmaxf(m[cb], mx);
-        const float neg = -mnew;
-        float s0 = 0.0f, s1 = 0.0f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          s0 += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[0][cb][r], sl2, neg));
-          s1 += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[1][cb][r], sl2, neg));
-        }
-        lsum[cb] = lsum[cb] * __builtin_amdgcn_exp2f(m[cb] - mnew) + (s0 + s1);
-        m[cb] = mnew;
+      for (int r = 0; r < 16; ++r) {
+        const int off = (r >> 2) * 8 + (r & 3);
+        acc[cb][r] = off <= lim ? acc[cb][r] : -INFINITY;
       }
     }
-    if (has_next) pre.store(ktile[buf ^ 1]);
-    __syncthreads();
+  };
+
+  const int arow = lane & 31;
+  floatx16 acc0[2], acc1[2];  // [query column block] of key row block 0 / 1 of a tile
+  dma_wait();
+  __syncthreads();            // both first tiles landed in LDS for every wave
+  if (active && kr0 < kend_wave) mma_rows<M, Tl>(acc0, kt0, arow, half, qf);
+  // One tile t in `cur`; tile t+1 is in (or on its way to) `nxt`.
+  auto step = [&](int t, T* cur, const T* nxt) {
+    const bool has_next = t + kTile < kr1;
+    const bool busy = active && t < kend_wave;
+    // phase A: MFMAs of key rows 32..63 of tile t || exp/sum of rows 0..31
+    if (busy) {
+      if (need_mask(t)) apply_mask(acc0, t);
+      mma_rows<M, Tl>(acc1, cur, 32 + arow, half, qf);
+      online_update(acc0[0], sl2, m[0], lsum[0]);
+      online_update(acc0[1], sl2, m[1], lsum[1]);
+      OMNIMEM_INTERLEAVE(16, NV);
+    }
+    dma_wait();
+    __syncthreads();  // tile t+1 landed; every wave is done with `cur`
+    if (t + 2 * kTile < kr1) Tl::dma(cur, k + (int64_t)(t + 2 * kTile) * kv_rs, kv_rs, min(kTile, N - t - 2 * kTile));
+    // phase B: MFMAs of key rows 0..31 of tile t+1 || exp/sum of rows 32..63 of tile t
+    if (busy) {
+      if (need_mask(t + 32)) apply_mask(acc1, t + 32);
+      if (has_next && t + kTile < kend_wave) {
+        mma_rows<M, Tl>(acc0, nxt, arow, half, qf);
+        online_update(acc1[0], sl2, m[0], lsum[0]);
+        online_update(acc1[1], sl2, m[1], lsum[1]);
+        OMNIMEM_INTERLEAVE(16, NV);
+      } else {
+        online_update(acc1[0], sl2, m[0], lsum[0]);
+        online_update(acc1[1], sl2, m[1], lsum[1]);
+      }
+    }
+  };
+  for (int t = kr0; t < kr1; t += 2 * kTile) {
+    step(t, kt0, kt1);
+    if (t + kTile < kr1) step(t + kTile, kt1, kt0);
   }
   if (!active) return;
 #pragma unroll
@@ -177,7 +257,7 @@ __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restr
     const float lt = lsum[cb] * __builtin_amdgcn_exp2f(m[cb] - mt) + l2 * __builtin_amdgcn_exp2f(m2 - mt);
     const int my_q = qw + cb * 32 + (lane & 31);
     if (half == 0 && my_q < C)
-      part[(((int64_t)l * dm.Hq + h) * dm.n_kr + blockIdx.x) * dm.max_chunk + my_q] = make_float2(mt, lt);
+      part[(((int64_t)l * dm.Hq + h) * dm.n_kr + range) * dm.max_chunk + my_q] = make_float2(mt, lt);
   }
 }
 
@@ -215,25 +295,59 @@ __global__ __launch_bounds__(256) void lse_merge(const LayerDesc* __restrict__ l
   if (lse_out) lse_out[o] = v2 * kLn2;
 }
 
+// cs[cb] += sum over the lane's 16 query rows of exp2(sl2 * score - lse2).
+__device__ inline void colsum_update(const floatx16 (&acc)[2], const float* lse2_rows, int half, float sl2,
+                                     float (&cs)[2]) {
+  float nl[16];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const floatx4 v = *reinterpret_cast<const floatx4*>(lse2_rows + j * 8 + half * 4);
+    nl[j * 4 + 0] = -v[0]; nl[j * 4 + 1] = -v[1]; nl[j * 4 + 2] = -v[2]; nl[j * 4 + 3] = -v[3];
+  }
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) {
+      s0 += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[cb][r], sl2, nl[r]));
+      s1 += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[cb][r + 1], sl2, nl[r + 1]));
+    }
+    cs[cb] += s0 + s1;
+  }
+}
+
 // Pass 2: per-query-head column sums colsum[h][j] = sum_i exp(S[i][j] -
-// lse[i]) for the 256 keys [k0, k0+256).  MFMA tile: rows = 32 queries (A
-// from LDS), columns = 32 keys (B in registers, two blocks per wave); each
-// lane accumulates one key's sum over 16 query rows per tile. 
+// lse[i]) for the 256 keys [k0, k0+256) over one slice of the queries.
+// MFMA tile: rows = 32 queries (A from LDS), columns = 32 keys (B in
+// registers, two blocks per wave); each lane accumulates one key's sum
+// over 16 query rows per tile.  Software pipeline inside each wave: the
+// MFMAs of one 32-query half run while the exp/sum work of the previous
+// half executes; query tiles arrive by DMA one tile ahead.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __restrict__ layers, Dims dm,
                                                            const float* __restrict__ lse2_all,
                                                            float* __restrict__ colsum) {
   using M = Mfma<T>;
-  using S = Stage<T, D>;
+  using Tl = SwzTile<T, D>;
   constexpr int NKS = D / M::KSTEP;
-  constexpr int LD = S::LD;
-  __shared__ __attribute__((aligned(16))) T qtile[2][kTile * LD];
-  __shared__ __attribute__((aligned(16))) float lse2[2][kTile];
+  constexpr int NV = (D == 128 && sizeof(T) == 2) ? 6 : 2;
+  __shared__ __attribute__((aligned(16))) T qt0[Tl::ELEMS];
+  __shared__ __attribute__((aligned(16))) T qt1[Tl::ELEMS];
+  // normalisers: three slots, because phase B of tile i still reads slot i
+  // while a faster wave already stores tile i + 2's values
+  __shared__ __attribute__((aligned(16))) float lse2[3][kTile];
 
-  const int l = blockIdx.z, h = blockIdx.y / dm.n_qc, qc = blockIdx.y % dm.n_qc;
+  // Workgroups streaming the same query rows run on the same XCD.
+  const int kblocks = (int)((dm.max_tokens + kBlockRows - 1) / kBlockRows);
+  const int logical = xcd_swizzle(blockIdx.x, gridDim.x);
+  if (logical >= kblocks * dm.Hq * dm.n_qc * dm.L) return;
+  const int kblk = logical % kblocks;
+  const int hq = (logical / kblocks) % (dm.Hq * dm.n_qc);
+  const int l = logical / (kblocks * dm.Hq * dm.n_qc);
+  const int h = hq / dm.n_qc, qc = hq % dm.n_qc;
   const LayerDesc Ld = layers[l];
   const int N = Ld.n, nc = Ld.n_cache;
-  const int k0 = blockIdx.x * kBlockRows;
+  const int k0 = kblk * kBlockRows;
   if (k0 >= N) return;
   // this workgroup's slice of the chunk queries
   const int C = min(Ld.n_chunk, (qc + 1) * dm.qchunk);
@@ -242,98 +356,98 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __re
   const int g = h / dm.G;
   const T* q = reinterpret_cast<const T*>(Ld.q) + (int64_t)h * Ld.q_hs;
   const T* k = reinterpret_cast<const T*>(Ld.k) + (int64_t)g * Ld.kv_hs;
+  const int64_t q_rs = Ld.q_rs;
   const float* lse2_lh = lse2_all + ((int64_t)l * dm.Hq + h) * dm.max_chunk;
   const int kw = k0 + wave * kRowsPerWave;
   const bool active = kw < N;
-
-  typename M::frag kf[2][NKS];
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    const int key = kw + cb * 32 + (lane & 31);
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-      kf[cb][ks] = key < N ? M::gload(k + (int64_t)key * Ld.kv_rs + ks * M::KSTEP + half * M::PER_LANE)
-                           : M::zero();
-  }
   // First query seeing any key of the block (chunk row nc + t is seen by i >= t).
   const int qstart = max(qlo, dm.causal ? (max(0, k0 - nc) / kTile) * kTile : 0);
   const int qfirst_wave = dm.causal ? max(0, kw - nc) : 0;
-  const float sl2 = Ld.scale_log2;
-  float cs[2] = {0.0f, 0.0f};
-
-  // normaliser of tile row threadIdx.x (+inf past the chunk: probability 0)
+  // normaliser of tile row threadIdx.x (+inf past the slice: probability 0)
   auto load_lse = [&](int qt) {
     const int i = qt + (int)threadIdx.x;
     return (threadIdx.x < kTile && i < C) ? gload<float>(lse2_lh + i) : INFINITY;
   };
-
-  S pre;
-  float pre_lse = INFINITY;
+  float lse_next = INFINITY;
   if (qstart < C) {
-    pre.load(q + (int64_t)qstart * Ld.q_rs, Ld.q_rs, min(kTile, C - qstart));
-    pre.store(qtile[0]);
+    Tl::dma(qt0, q + (int64_t)qstart * q_rs, q_rs, min(kTile, C - qstart));
     if (threadIdx.x < kTile) lse2[0][threadIdx.x] = load_lse(qstart);
+    if (qstart + kTile < C) {
+      Tl::dma(qt1, q + (int64_t)(qstart + kTile) * q_rs, q_rs, min(kTile, C - qstart - kTile));
+      lse_next = load_lse(qstart + kTile);
+    }
   }
-  __syncthreads();
-  int buf = 0;
-  for (int qt = qstart; qt < C; qt += kTile, buf ^= 1) {
-    const bool has_next = qt + kTile < C;
-    if (has_next) {
-      pre.load(q + (int64_t)(qt + kTile) * Ld.q_rs, Ld.q_rs, min(kTile, C - qt - kTile));
-      pre_lse = load_lse(qt + kTile);
+
+  typename M::frag kf[2][NKS];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    const int key = min(kw + cb * 32 + (lane & 31), N - 1);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+      kf[cb][ks] = M::gload(k + (int64_t)key * Ld.kv_rs + ks * M::KSTEP + half * M::PER_LANE);
+  }
+  const float sl2 = Ld.scale_log2;
+  float cs[2] = {0.0f, 0.0f};
+
+  // Row block qb needs masking when a key of the wave lies past the causal
+  // horizon of its first query; the score of (query qb + acc_row(r), key
+  // kw + cb*32 + (lane & 31)) is kept iff (r >> 2) * 8 + (r & 3) >= dlim.
+  auto need_mask = [&](int qb) { return dm.causal && kw + kRowsPerWave - 1 - nc > qb; };
+  auto apply_mask = [&](floatx16 (&acc)[2], int qb) {
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      const int dlim = kw + cb * 32 + (lane & 31) - nc - qb - half * 4;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[cb][r] = ((r >> 2) * 8 + (r & 3)) >= dlim ? acc[cb][r] : -INFINITY;
     }
-    if (active && qt + kTile > qfirst_wave) {
-      floatx16 acc[2][2];
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = floatx16{};
-      const T* a0 = qtile[buf] + (lane & 31) * LD + half * M::PER_LANE;
-      const T* a1 = a0 + 32 * LD;
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const typename M::frag f0 = M::load(a0 + ks * M::KSTEP);
-        const typename M::frag f1 = M::load(a1 + ks * M::KSTEP);
-        acc[0][0] = M::mma(f0, kf[0][ks], acc[0][0]);
-        acc[0][1] = M::mma(f0, kf[1][ks], acc[0][1]);
-        acc[1][0] = M::mma(f1, kf[0][ks], acc[1][0]);
-        acc[1][1] = M::mma(f1, kf[1][ks], acc[1][1]);
+  };
+
+  if (qstart < C) {
+    const int arow = lane & 31;
+    floatx16 acc0[2], acc1[2];
+    auto busy_at = [&](int qt) { return active && qt + kTile > qfirst_wave; };
+    dma_wait();
+    __syncthreads();  // first tiles landed in LDS for every wave
+    if (busy_at(qstart)) mma_rows<M, Tl>(acc0, qt0, arow, half, kf);
+    int slot = 0;
+    auto step = [&](int qt, T* cur, const T* nxt) {
+      const int next_slot = slot == 2 ? 0 : slot + 1;
+      const bool has_next = qt + kTile < C;
+      const bool busy = busy_at(qt);
+      // phase A: MFMAs of row block 1 of tile qt || exp/sum of row block 0
+      if (busy) {
+        if (need_mask(qt)) apply_mask(acc0, qt);
+        mma_rows<M, Tl>(acc1, cur, 32 + arow, half, kf);
+        colsum_update(acc0, &lse2[slot][0], half, sl2, cs);
+        OMNIMEM_INTERLEAVE(16, NV);
       }
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        // lse2 of the 16 query rows this lane holds: 4 runs of 4 rows
-        float nl[16];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const floatx4 v = *reinterpret_cast<const floatx4*>(&lse2[buf][rb * 32 + j * 8 + half * 4]);
-          nl[j * 4 + 0] = -v[0]; nl[j * 4 + 1] = -v[1]; nl[j * 4 + 2] = -v[2]; nl[j * 4 + 3] = -v[3];
-        }
-        const int qb = qt + rb * 32;
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-          float sum = 0.0f;
-          if (dm.causal && kw + cb * 32 + 31 - nc > qb) {
-            // chunk key t = key - nc is seen by query qb + acc_row(r) iff
-            // (r >> 2) * 8 + (r & 3) >= t - qb - half * 4
-            const int dlim = kw + cb * 32 + (lane & 31) - nc - qb - half * 4;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][cb][r], sl2, nl[r]));
-              sum += ((r >> 2) * 8 + (r & 3)) >= dlim ? p : 0.0f;
-            }
-          } else {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][cb][r], sl2, nl[r]));
-          }
-          cs[cb] += sum;
-        }
+      if (has_next && threadIdx.x < kTile) lse2[next_slot][threadIdx.x] = lse_next;
+      dma_wait();
+      __syncthreads();  // tile qt+1 landed; every wave is done with `cur`
+      if (qt + 2 * kTile < C) {
+        Tl::dma(cur, q + (int64_t)(qt + 2 * kTile) * q_rs, q_rs, min(kTile, C - qt - 2 * kTile));
+        lse_next = load_lse(qt + 2 * kTile);
       }
+      // phase B: MFMAs of row block 0 of tile qt+1 || exp/sum of row block 1.
+      // A wave's tiles go from idle to busy (causal), so the next tile's
+      // first MFMAs are issued whether or not this tile was busy.
+      const bool busy_next = has_next && busy_at(qt + kTile);
+      if (busy && need_mask(qt + 32)) apply_mask(acc1, qt + 32);
+      if (busy && busy_next) {
+        mma_rows<M, Tl>(acc0, nxt, arow, half, kf);
+        colsum_update(acc1, &lse2[slot][32], half, sl2, cs);
+        OMNIMEM_INTERLEAVE(16, NV);
+      } else if (busy) {
+        colsum_update(acc1, &lse2[slot][32], half, sl2, cs);
+      } else if (busy_next) {
+        mma_rows<M, Tl>(acc0, nxt, arow, half, kf);
+      }
+      slot = next_slot;
+    };
+    for (int qt = qstart; qt < C; qt += 2 * kTile) {
+      step(qt, qt0, qt1);
+      if (qt + kTile < C) step(qt + kTile, qt1, qt0);
     }
-    if (has_next) {
-      pre.store(qtile[buf ^ 1]);
-      if (threadIdx.x < kTile) lse2[buf ^ 1][threadIdx.x] = pre_lse;
-    }
-    __syncthreads();
   }
   if (!active) return;
   cs[0] += wave_xor32(cs[0]);
@@ -369,10 +483,11 @@ __global__ void head_sum(const LayerDesc* __restrict__ layers, Dims dm, const fl
 template <typename T, int D>
 void launch_typed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, float* lse_out, float* a,
                   hipStream_t st) {
-  const unsigned qblocks = (unsigned)((dm.max_chunk + kBlockRows - 1) / kBlockRows);
-  dim3 g1((unsigned)dm.n_kr, qblocks, (unsigned)(dm.L * dm.Hq));
+  const int64_t qblocks = (dm.max_chunk + kBlockRows - 1) / kBlockRows;
+  const dim3 g1(xcd_grid((int64_t)dm.n_kr * qblocks * dm.L * dm.Hq));
   OMNIMEM_LAUNCH(ws, K_LSE, st, lse_pass<T, D><<<g1, kThreads, 0, st>>>(desc, dm, ws.lse_part));
-  dim3 g2((unsigned)((dm.max_tokens + kBlockRows - 1) / kBlockRows), (unsigned)(dm.Hq * dm.n_qc), dm.L);
+  const int64_t kblocks = (dm.max_tokens + kBlockRows - 1) / kBlockRows;
+  const dim3 g2(xcd_grid(kblocks * dm.Hq * dm.n_qc * dm.L));
   dim3 gm((unsigned)((dm.max_chunk + 255) / 256), dm.Hq, dm.L);
   OMNIMEM_LAUNCH(ws, K_LSE_MERGE, st, lse_merge<<<gm, 256, 0, st>>>(desc, dm, ws.lse_part, ws.lse2, lse_out));
   OMNIMEM_LAUNCH(ws, K_COLSUM, st, colsum_pass<T, D><<<g2, kThreads, 0, st>>>(desc, dm, ws.lse2, ws.part));
