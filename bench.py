@@ -21,6 +21,42 @@ METRIC = "KV tokens compressed/sec per layer-step; % MFMA peak (score+Gram), % H
 PEAK_HBM_GBS = 8000.0                                   # MI355X HBM3E
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}       # dense MFMA
 
+# HBM bytes per launch from two rocprofv3 counter passes (FETCH_SIZE, then
+# WRITE_SIZE, KiB per dispatch), each divided by what that counter reads for a
+# plain 1 GiB device-to-device copy (FETCH_SIZE 0.5x, WRITE_SIZE 1.0x), with
+# the SHA-256 of the library sources the counters were taken on.  A source
+# change makes the figures stale: the roofline then reports traffic null.
+KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f in (
+    "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
+MEASURED_TRAFFIC = {
+    "qwen7b-layer-6144": {
+        "sources_sha256": "15fd90247c902a44ab2b23f884723a0f41d628b4c0980ab8c7a138638a289774",
+        "lse_pass": 32300440, "colsum_pass": 31617259, "gram_max": 67980326,
+        "psi_topk": 616781, "gather_compact": 16875282,
+    },
+    "qwen7b-28layer-6144": {
+        "sources_sha256": "15fd90247c902a44ab2b23f884723a0f41d628b4c0980ab8c7a138638a289774",
+        "lse_pass": 617838124, "colsum_pass": 613104613, "gram_max": 2270518743,
+        "psi_topk": 13714521, "gather_compact": 472077352,
+    },
+}
+
+
+def sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, kernel):
+    rec = MEASURED_TRAFFIC.get(workload)
+    if rec is None or kernel not in rec or rec["sources_sha256"] != sources_sha256():
+        return None
+    return rec[kernel]
+
 
 def parse_args():
     p = argparse.ArgumentParser(description=__doc__)
@@ -29,7 +65,22 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="qwen7b-layer-6144")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run 5 device-to-device copies of MIB MiB each (reference kernel for "
+                        "scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return p.parse_args()
+
+
+def copy_calibration(mib):
+    """Plain copies of known size: each reads and writes exactly `mib` MiB."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
 
 
 def algorithmic_work(layers, budgets, causal=True):
@@ -81,6 +132,9 @@ def main():
               "(the step is per layer and KV head; sharding is described in the design notes)",
               file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     import numpy as np
     import torch
 
@@ -137,7 +191,8 @@ def main():
     dk = per_kernel[dominant]
     peak = PEAK_MFMA_TFLOPS[dtype] if dk["bound"] == "mfma" else PEAK_HBM_GBS
     roofline = {"bound": dk["bound"], "achieved": round(dk["achieved"], 3), "peak": peak, "unit": dk["unit"],
-                "frac": round(dk["frac"], 4), "traffic": None, "kernel": dominant,
+                "frac": round(dk["frac"], 4), "traffic": measured_traffic(args.workload, dominant),
+                "traffic_unit": "bytes", "kernel": dominant,
                 "units_per_launch": work[dominant][1], "avg_launch_us": dk["avg_us"]}
 
     def stage_frac(names, peak_units, scale):
