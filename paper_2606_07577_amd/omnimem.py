@@ -157,6 +157,13 @@ class Context:
             raise OmnimemError(st, lib.omnimem_last_error(None).decode())
         self.handle = handle
 
+    @staticmethod
+    def default_config():
+        """The library's default omnimem_config (sizes 0)."""
+        cfg = Config()
+        load_library().omnimem_config_default(ctypes.byref(cfg))
+        return cfg
+
     def _check(self, st):
         if st != OK:
             raise OmnimemError(st, self._lib.omnimem_last_error(self.handle).decode())

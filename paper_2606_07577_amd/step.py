@@ -96,3 +96,103 @@ class DeviceStep:
 
     def close(self):
         self.ctx.close()
+
+
+class StreamRunner:
+    """The compression step after every chunk of a stream, on the GPU.
+
+    Each layer's cache lives in two ping-pong buffers [H_kv, cap, d]: the
+    working set of a step is the current buffer's first N = n_cache + C rows
+    (retained visual, retained audio, then the new chunk, Eq. 3), and
+    omnimem_select_compact writes the kept rows to the front of the other
+    buffer, which then receives the next chunk behind them.  Appending the
+    chunk stands in for the model's prefill writing its K/V; it is a device
+    copy outside the library.  After each step the budgets are read back (a
+    stream synchronisation): the host needs them to describe the next
+    working set.
+    """
+
+    def __init__(self, n_layers, h_q, h_kv, d, chunk_len, total_budget, dtype="bf16", device="cuda",
+                 **options):
+        self.device = torch.device(device)
+        self.L, self.h_q, self.h_kv, self.d, self.C = n_layers, h_q, h_kv, d, chunk_len
+        self.total_budget = int(total_budget)
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        cfg_probe = om.Context.default_config()
+        bmax = options.get("b_max_frac", cfg_probe.b_max_frac)
+        self.cache_cap = int(bmax * total_budget / n_layers)   # no layer keeps more
+        self.cap = self.cache_cap + chunk_len
+        self.ctx = om.Context(n_layers, h_q, h_kv, d, self.cap, chunk_len,
+                              dtype=om.BF16 if dtype == "bf16" else om.F32, **options)
+        dev, td = self.device, self.tdtype
+        self.kbuf = [[torch.zeros((h_kv, self.cap, d), device=dev, dtype=td) for _ in range(n_layers)]
+                     for _ in range(2)]
+        self.vbuf = [[torch.zeros((h_kv, self.cap, d), device=dev, dtype=td) for _ in range(n_layers)]
+                     for _ in range(2)]
+        self.mbuf = [[torch.zeros(self.cap, device=dev, dtype=torch.uint8) for _ in range(n_layers)]
+                     for _ in range(2)]
+        shape = (n_layers, h_kv, self.cap)
+        self.a = torch.zeros(shape, device=dev, dtype=torch.float32)
+        self.s = torch.zeros(shape, device=dev, dtype=torch.float32)
+        self.idx = torch.full(shape, -1, device=dev, dtype=torch.int32)
+        self.budgets = torch.zeros((n_layers, 2), device=dev, dtype=torch.int32)
+        self.stats = torch.zeros((n_layers, 10), device=dev, dtype=torch.float32)
+        self.cur = 0
+        self.n_cache = [0] * n_layers
+        self.steps = 0
+        self.tokens = 0          # sum over steps and layers of the working-set size
+
+    def set_cache(self, l, k, v, m_v, m_a):
+        """Replace layer l's retained cache: k, v [H_kv, m_v + m_a, d] (host or
+        device), visual rows first."""
+        m = int(m_v) + int(m_a)
+        if m > self.cache_cap:
+            raise ValueError(f"cache of {m} rows exceeds the capacity {self.cache_cap}")
+        kb, vb, mb = self.kbuf[self.cur][l], self.vbuf[self.cur][l], self.mbuf[self.cur][l]
+        kb[:, :m] = torch.as_tensor(k).to(self.device, self.tdtype)
+        vb[:, :m] = torch.as_tensor(v).to(self.device, self.tdtype)
+        mb[:m_v] = 0
+        mb[m_v:m] = 1
+        self.n_cache[l] = m
+
+    def working_set(self, l):
+        """Device views of layer l's current working set (k, v, modality)."""
+        n = self.n_cache[l] + self.C
+        return (self.kbuf[self.cur][l][:, :n], self.vbuf[self.cur][l][:, :n], self.mbuf[self.cur][l][:n])
+
+    def push(self, chunk, stream=None):
+        """Append one chunk (list of per-layer dicts from synth.StreamSource)
+        and run the step.  Returns the budgets [L, 2] as a host array."""
+        dev, td = self.device, self.tdtype
+        descs, qs = [], []
+        other = 1 - self.cur
+        for l, ch in enumerate(chunk):
+            n0 = self.n_cache[l]
+            n = n0 + self.C
+            kb, vb, mb = self.kbuf[self.cur][l], self.vbuf[self.cur][l], self.mbuf[self.cur][l]
+            kb[:, n0:n] = torch.as_tensor(ch["k"]).to(dev, td)
+            vb[:, n0:n] = torch.as_tensor(ch["v"]).to(dev, td)
+            mb[n0:n] = torch.as_tensor(ch["modality"]).to(dev)
+            q = torch.as_tensor(ch["q"]).to(dev, td).contiguous()
+            qs.append(q)
+            descs.append(om.make_layer(q, kb[:, :n], vb[:, :n], mb[:n], n0, ch["sm_scale"], None,
+                                       self.kbuf[other][l], self.vbuf[other][l]))
+            self.tokens += n
+        self._descs, self._qs = descs, qs
+        self.ctx.omnimem_score(descs, self.a, None, stream)
+        self.ctx.omnimem_redundancy(descs, self.s, stream)
+        self.ctx.omnimem_allocate(descs, self.a, self.s, self.total_budget, self.budgets, self.stats, stream)
+        self.ctx.omnimem_select_compact(descs, self.a, self.s, self.budgets, self.idx, stream)
+        budgets = self.budgets.cpu().numpy()
+        for l in range(self.L):
+            m_v, m_a = int(budgets[l, 0]), int(budgets[l, 1])
+            mb = self.mbuf[other][l]
+            mb[:m_v] = 0
+            mb[m_v:m_v + m_a] = 1
+            self.n_cache[l] = m_v + m_a
+        self.cur = other
+        self.steps += 1
+        return budgets
+
+    def close(self):
+        self.ctx.close()

@@ -148,3 +148,136 @@ def tokens_per_step(name):
     spec = WORKLOADS[name]
     n = spec["n_cache_v"] + spec["n_cache_a"] + spec["n_frames"] * (spec["frame_v"] + spec["frame_a"])
     return spec["n_layers"] * n
+
+
+# ---------------------------------------------------------------------------
+# Streams: the step after every chunk, caches carried from step to step
+# ---------------------------------------------------------------------------
+
+# Each chunk is `n_frames` frames of [frame_v visual | frame_a audio] rows.
+# Visual K and V follow an AR(1) process over the global frame index, per
+# (layer, KV head, spatial slot p in 0..frame_v-1):
+#     x_f = rho x_{f-1} + sqrt(1 - rho^2) eps_f,   x_0 ~ N(0, 1),
+# so every frame is N(0, 1) and neighbouring frames are correlated by rho.
+# Audio K, V and the chunk queries are i.i.d. N(0, 1).  The stream starts
+# from empty caches.
+STREAMS = {
+    "qwen7b-stream-64x28": dict(
+        desc="64 chunks through 28 layers, 28 query / 4 KV heads, head_dim 128, bf16; each chunk "
+             "4 frames of 384 visual + 128 audio tokens; visual K/V AR(1) over frames (rho 0.9); "
+             "softmax temperature U(0.3,3) per layer; total budget 28x4096",
+        n_layers=28, h_q=28, h_kv=4, d=128, n_chunks=64, n_frames=4, frame_v=384, frame_a=128,
+        rho=0.9, temperature=(0.3, 3.0), dtype="bf16", total_budget=28 * 4096, seed=4),
+    "small-stream": dict(
+        desc="10 chunks through 3 layers, 8 query / 2 KV heads, head_dim 128, bf16; each chunk "
+             "2 frames of 96 visual + 32 audio tokens; AR(1) rho 0.9; total budget 3x256",
+        n_layers=3, h_q=8, h_kv=2, d=128, n_chunks=10, n_frames=2, frame_v=96, frame_a=32,
+        rho=0.9, temperature=(0.3, 3.0), dtype="bf16", total_budget=3 * 256, seed=5),
+}
+
+
+class StreamSource:
+    """The chunks of a named stream, generated in order.
+
+    backend "numpy": host float32 arrays (bf16-rounded for bf16 streams).
+    backend "torch": tensors on `device` in the stream's dtype, drawn with
+    torch's generator (other values than the numpy backend, same recipe).
+    chunk(t) must be called for t = 0, 1, 2, ... in order; it returns one
+    dict per layer with q [H_q, C, d], k and v [H_kv, C, d], modality [C]
+    and sm_scale.
+    """
+
+    def __init__(self, name, backend="numpy", device="cuda", **overrides):
+        spec = dict(STREAMS[name])
+        spec.update(overrides)
+        self.spec = spec
+        self.backend = backend
+        self.device = device
+        self.taus = layer_temperatures(spec)
+        self.modality = modality_mask(0, 0, spec["n_frames"], spec["frame_v"], spec["frame_a"])
+        self.chunk_len = len(self.modality)
+        self._state = [None] * spec["n_layers"]   # last visual frame (k, v) per layer
+        self._next = 0
+
+    def sm_scale(self, l):
+        return 1.0 / (self.taus[l] * math.sqrt(self.spec["d"]))
+
+    def chunk(self, t):
+        if t != self._next:
+            raise ValueError(f"chunks are generated in order: expected {self._next}, got {t}")
+        self._next += 1
+        return [self._layer_chunk(t, l) for l in range(self.spec["n_layers"])]
+
+    def _layer_chunk(self, t, l):
+        sp = self.spec
+        h_q, h_kv, d = sp["h_q"], sp["h_kv"], sp["d"]
+        nf, fv, fa = sp["n_frames"], sp["frame_v"], sp["frame_a"]
+        rho = sp["rho"]
+        c = self.chunk_len
+        if self.backend == "numpy":
+            rng = np.random.default_rng([sp["seed"], t, l])
+            normal = lambda *shape: rng.standard_normal(shape, dtype=np.float32)
+            empty = lambda *shape: np.empty(shape, dtype=np.float32)
+        else:
+            import torch
+            g = torch.Generator(device=self.device)
+            g.manual_seed((sp["seed"] * 1_000_003 + t) * 1009 + l)
+            normal = lambda *shape: torch.randn(shape, generator=g, device=self.device, dtype=torch.float32)
+            empty = lambda *shape: torch.empty(shape, device=self.device, dtype=torch.float32)
+        q = normal(h_q, c, d)
+        k, v = empty(h_kv, c, d), empty(h_kv, c, d)
+        innov = math.sqrt(1.0 - rho * rho)
+        state = self._state[l]
+        for f in range(nf):
+            base = f * (fv + fa)
+            if state is None:
+                kf, vf = normal(h_kv, fv, d), normal(h_kv, fv, d)
+            else:
+                kf = rho * state[0] + innov * normal(h_kv, fv, d)
+                vf = rho * state[1] + innov * normal(h_kv, fv, d)
+            state = (kf, vf)
+            k[:, base:base + fv], v[:, base:base + fv] = kf, vf
+            k[:, base + fv:base + fv + fa] = normal(h_kv, fa, d)
+            v[:, base + fv:base + fv + fa] = normal(h_kv, fa, d)
+        self._state[l] = state
+        if self.backend == "numpy":
+            if sp["dtype"] == "bf16":
+                q, k, v = round_to_bf16(q), round_to_bf16(k), round_to_bf16(v)
+            modality = self.modality.copy()
+        else:
+            import torch
+            td = torch.bfloat16 if sp["dtype"] == "bf16" else torch.float32
+            q, k, v = q.to(td), k.to(td), v.to(td)
+            modality = torch.from_numpy(self.modality).to(self.device)
+        return {"q": q, "k": k, "v": v, "modality": modality, "sm_scale": self.sm_scale(l),
+                "dtype": sp["dtype"]}
+
+
+def make_scores(modalities, h_kv, seed, group_queries=2048 * 7):
+    """Synthetic per-layer importance a [H_kv, N] and redundancy s [H_kv, N]
+    (float32) for driving the allocation and selection stages on their own.
+
+    a: log-normal with a per-layer spread U(0.3, 3) (so the normalised
+    entropies differ between layers), scaled to sum to `group_queries` per
+    head like a real column sum; a few exact zeros.  s: 70% of rows
+    N(0.1, 0.15), 30% near-duplicates 1 - LogUniform(1e-3, 1e-1), clipped to
+    [-1, 1]; a few exact ties of a and s between rows.
+    """
+    rng = np.random.default_rng([seed, 31337])
+    a_out, s_out = [], []
+    for mod in modalities:
+        n = len(mod)
+        spread = rng.uniform(0.3, 3.0)
+        a = np.exp(spread * rng.standard_normal((h_kv, n)))
+        a *= group_queries / a.sum(axis=1, keepdims=True)
+        a[:, rng.choice(n, size=max(1, n // 500), replace=False)] = 0.0
+        s = 0.1 + 0.15 * rng.standard_normal((h_kv, n))
+        dup = rng.random((h_kv, n)) < 0.3
+        s[dup] = 1.0 - np.exp(rng.uniform(np.log(1e-3), np.log(1e-1), size=dup.sum()))
+        s = np.clip(s, -1.0, 1.0)
+        twins = rng.choice(n, size=(max(1, n // 200), 2), replace=True)
+        a[:, twins[:, 1]] = a[:, twins[:, 0]]
+        s[:, twins[:, 1]] = s[:, twins[:, 0]]
+        a_out.append(a.astype(np.float32))
+        s_out.append(s.astype(np.float32))
+    return a_out, s_out

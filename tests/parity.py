@@ -73,6 +73,27 @@ def check_selection(idx_row, psi_row, modality, m_v, m_a, rel=REL):
     return exact
 
 
+def check_topk_property(idx_row, a_row, s_row, modality, m_v, m_a, lam=LAMBDA, rel=1e-5):
+    """One KV head of the GPU's own chain: the kept rows of each modality
+    are ascending, of that modality, M of them, and no dropped row has a
+    larger psi = a^lam (1 - s) than a kept one.  psi is recomputed here in
+    float64 from the GPU's fp32 a and s; the GPU orders by its fp32 psi, so
+    a relative slack of `rel` is allowed."""
+    modality = np.asarray(modality)
+    psi = np.power(np.asarray(a_row, dtype=np.float64), lam) * (1.0 - np.asarray(s_row, dtype=np.float64))
+    for mu, lo, hi in ((0, 0, m_v), (1, m_v, m_v + m_a)):
+        got = np.asarray(idx_row[lo:hi], dtype=np.int64)
+        pos = np.flatnonzero(modality == mu)
+        assert len(got) == hi - lo
+        if len(got) == 0:
+            continue
+        assert (np.diff(got) > 0).all(), "kept rows not ascending"
+        assert (modality[got] == mu).all(), "kept row of the wrong modality"
+        dropped = np.setdiff1d(pos, got)
+        if len(dropped):
+            assert psi[dropped].max() <= psi[got].min() * (1 + rel), "a dropped row outranks a kept one"
+
+
 def oracle_allocation(a_list, s_list, layers, total_budget, bmin=om.DEFAULT_BMIN_FRAC,
                       bmax=om.DEFAULT_BMAX_FRAC, temperature=TEMPERATURE, r=RATIO):
     """Oracle stats, shares and (M_v, M_a) per layer from given a, s."""

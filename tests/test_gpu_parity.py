@@ -227,58 +227,100 @@ def test_caller_supplied_lse_matches_computed():
 # Large workloads: sampled outputs and properties
 # ---------------------------------------------------------------------------
 
-def _sampled_checks(c, l, rng, n_q=48, n_k=96, n_s=96):
+def _sampled_checks(c, l, rng, kv_groups=None, n_q=48, n_k=96, n_s=96):
+    """lse at sampled queries, a at sampled keys and s at sampled rows of
+    layer l, each from the oracle on the generator's inputs.  a needs the
+    oracle's lse of every chunk query of the KV group's heads, so only the
+    groups in `kv_groups` (default all) are checked."""
     lay = c.layers64[l]
-    C = lay["q"].shape[1]
-    N = lay["k"].shape[1]
+    h_q, C, _ = lay["q"].shape
+    h_kv, N, _ = lay["k"].shape
+    group = h_q // h_kv
     qs = np.sort(rng.choice(C, size=min(n_q, C), replace=False))
     qs[0], qs[-1] = 0, C - 1
     lse_ref = om.attention_lse(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True, queries=qs)
     P.assert_close_a(c.lse[l][:, qs], lse_ref, f"lse layer {l} (sampled)")
     ks = np.sort(rng.choice(N, size=min(n_k, N), replace=False))
     ks[0], ks[-1] = 0, N - 1
-    a_ref = om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True,
-                                    lse=c.lse[l].astype(np.float64), keys=ks)
-    P.assert_close_a(c.a[l][:, ks], a_ref, f"a layer {l} (sampled keys, GPU lse)")
-    group = lay["q"].shape[0] // lay["k"].shape[0]
+    for g in (range(h_kv) if kv_groups is None else kv_groups):
+        q_g, k_g = lay["q"][g * group:(g + 1) * group], lay["k"][g:g + 1]
+        lse_g = om.attention_lse(q_g, k_g, lay["n_cache"], lay["sm_scale"], True)
+        a_ref = om.attention_importance(q_g, k_g, lay["n_cache"], lay["sm_scale"], True, lse=lse_g, keys=ks)
+        P.assert_close_a(c.a[l][g, ks], a_ref[0], f"a layer {l} KV head {g} (sampled keys)")
     np.testing.assert_allclose(c.a[l].sum(axis=1, dtype=np.float64), group * C, rtol=1e-4)
     rows = np.sort(rng.choice(N, size=min(n_s, N), replace=False))
     s_ref = om.redundancy(lay["v"], lay["modality"], "max", rows=rows)
     P.assert_close_s(c.s[l][:, rows], s_ref, f"s layer {l} (sampled rows)")
 
 
-def _allocation_and_selection_from_gpu_scores(c):
-    a64 = [x.astype(np.float64) for x in c.a]
-    s64 = [x.astype(np.float64) for x in c.s]
-    _, _, ref_budgets = P.oracle_allocation(a64, s64, c.layers, c.budget)
-    np.testing.assert_array_equal(c.budgets, ref_budgets)
+def _chain_properties(c):
+    """What the GPU's own chain must satisfy at any size: budgets that sum
+    to the total and fit each modality, a kept set that is a top-M of the
+    GPU's own psi per (layer, head, modality), and compacted rows equal to
+    the kept input rows."""
+    total = sum(len(lay["modality"]) for lay in c.layers)
+    assert c.budgets.sum() == min(c.budget, total)
     for l, lay in enumerate(c.layers):
+        mod = np.asarray(lay["modality"])
         mv, ma = c.budgets[l]
-        psi = om.retention_score(a64[l], s64[l], P.LAMBDA)
+        assert 0 <= mv <= (mod == 0).sum() and 0 <= ma <= (mod == 1).sum()
         for g in range(c.step.h_kv):
             row = c.idx[l][g, : mv + ma]
-            P.check_selection(row, psi[g], lay["modality"], mv, ma)
+            P.check_topk_property(row, c.a[l][g], c.s[l][g], mod, mv, ma)
             np.testing.assert_array_equal(c.k_out[l][g, : mv + ma], lay["k"][g, row])
             np.testing.assert_array_equal(c.v_out[l][g, : mv + ma], lay["v"][g, row])
+
+
+def _teacher_forced_full_size(c, seed):
+    """Allocation and selection at full size from generator-drawn a and s
+    (the ABI lets a caller supply them): budgets exactly the oracle's,
+    statistics within tolerance, kept rows the oracle's top-M."""
+    st = c.step
+    a_syn, s_syn = synth.make_scores([lay["modality"] for lay in c.layers], st.h_kv, seed)
+    a_dev, s_dev = st.to_device_f32(a_syn), st.to_device_f32(s_syn)
+    budgets = torch.zeros_like(st.budgets)
+    stats = torch.zeros_like(st.stats)
+    st.ctx.omnimem_allocate(st.descs, a_dev, s_dev, c.budget, budgets, stats)
+    _sync()
+    a64 = [x.astype(np.float64) for x in a_syn]
+    s64 = [x.astype(np.float64) for x in s_syn]
+    ref_stats, _, ref_budgets = P.oracle_allocation(a64, s64, c.layers, c.budget)
+    np.testing.assert_array_equal(budgets.cpu().numpy(), ref_budgets)
+    got = stats.cpu().numpy()
+    for l, rs in enumerate(ref_stats):
+        P.assert_close_a(got[l], [rs[k] for k in P.STAT_KEYS], f"stats layer {l}")
+    st.ctx.omnimem_select_compact(st.descs, a_dev, s_dev, budgets, st.idx)
+    _sync()
+    for l, lay in enumerate(c.layers):
+        mv, ma = ref_budgets[l]
+        psi = om.retention_score(a64[l], s64[l], P.LAMBDA)
+        idx = st.host("idx", l)[:, : mv + ma]
+        k_out = st.k_out[l].float().cpu().numpy()
+        for g in range(st.h_kv):
+            P.check_selection(idx[g], psi[g], lay["modality"], mv, ma)
+            np.testing.assert_array_equal(k_out[g, : mv + ma], lay["k"][g, idx[g]])
 
 
 def test_28_layer_workload_sampled():
     layers = synth.make_workload("qwen7b-28layer-6144")
     c = Case(layers, 28 * 4096)
     rng = np.random.default_rng(7)
-    for l in (0, 13, 27):
+    for l in (0, 27):
         _sampled_checks(c, l, rng)
+    _sampled_checks(c, 13, rng, kv_groups=[2])
     assert c.budgets.sum() == 28 * 4096
-    _allocation_and_selection_from_gpu_scores(c)
+    _chain_properties(c)
+    _teacher_forced_full_size(c, 11)
     c.step.close()
 
 
 def test_long_cache_workload_sampled():
     layers = synth.make_workload("qwen7b-longcache-40960")
     c = Case(layers, 32768)
-    _sampled_checks(c, 0, np.random.default_rng(8))
+    _sampled_checks(c, 0, np.random.default_rng(8), kv_groups=[3])
     assert c.budgets.sum() == 32768
-    _allocation_and_selection_from_gpu_scores(c)
+    _chain_properties(c)
+    _teacher_forced_full_size(c, 12)
     c.step.close()
 
 

@@ -1,5 +1,6 @@
 """The seeded input generator: shapes, determinism, bf16 rounding, structure."""
 import numpy as np
+import pytest
 import torch
 
 from paper_2606_07577_amd import synth
@@ -58,3 +59,42 @@ def test_long_cache_audio_keys_are_smaller():
     ratio = np.linalg.norm(layer["k"][0, ~aud], axis=1).mean() / \
         np.linalg.norm(layer["k"][0, aud], axis=1).mean()
     assert 2.7 < ratio < 3.3
+
+
+def test_stream_chunks_ar1_and_layout():
+    src = synth.StreamSource("small-stream")
+    sp = src.spec
+    fv, fa = sp["frame_v"], sp["frame_a"]
+    c0, c1 = src.chunk(0), src.chunk(1)
+    assert len(c0) == sp["n_layers"]
+    lay0, lay1 = c0[0], c1[0]
+    assert lay0["q"].shape == (sp["h_q"], src.chunk_len, sp["d"])
+    assert lay0["k"].shape == (sp["h_kv"], src.chunk_len, sp["d"])
+    np.testing.assert_array_equal(lay0["modality"][:fv], 0)
+    np.testing.assert_array_equal(lay0["modality"][fv:fv + fa], 1)
+    # bf16-representable values
+    np.testing.assert_array_equal(synth.round_to_bf16(lay0["k"]), lay0["k"])
+    # neighbouring frames at the same spatial slot are correlated by rho,
+    # across the chunk boundary too; audio rows are not
+    first = lay0["k"][:, :fv].ravel()
+    second = lay0["k"][:, fv + fa:2 * fv + fa].ravel()
+    assert abs(np.corrcoef(first, second)[0, 1] - sp["rho"]) < 0.02
+    last = lay0["k"][:, (sp["n_frames"] - 1) * (fv + fa):(sp["n_frames"] - 1) * (fv + fa) + fv].ravel()
+    assert abs(np.corrcoef(last, lay1["k"][:, :fv].ravel())[0, 1] - sp["rho"]) < 0.02
+    assert abs(np.corrcoef(lay0["k"][:, fv:fv + fa].ravel(), lay0["k"][:, 2 * fv + fa:2 * fv + 2 * fa].ravel())[0, 1]) < 0.05
+    assert abs(lay1["v"][:, :fv].std() - 1.0) < 0.05
+    # deterministic, generated in order only
+    again = synth.StreamSource("small-stream")
+    np.testing.assert_array_equal(again.chunk(0)[2]["v"], c0[2]["v"])
+    with pytest.raises(ValueError):
+        again.chunk(2)
+
+
+def test_synthetic_scores_ranges():
+    mods = [synth.modality_mask(30, 10, 2, 20, 5), synth.modality_mask(100, 20, 1, 8, 8)]
+    a, s = synth.make_scores(mods, 3, seed=1)
+    for ai, si, m in zip(a, s, mods):
+        assert ai.shape == si.shape == (3, len(m))
+        assert ai.dtype == si.dtype == np.float32
+        assert (ai >= 0).all() and (ai == 0).any()
+        assert (np.abs(si) <= 1).all() and (si > 0.99).any()
