@@ -83,26 +83,33 @@ def copy_calibration(mib):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
 
 
-def algorithmic_work(layers, budgets, causal=True):
-    """Per-launch algorithmic units of each kernel (all layers in one launch)."""
-    score_flops = gram_flops = 0
-    compact_bytes = topk_bytes = 0
+def layer_work(h_q, c, n_cache, h_kv, n, d, elt, k_v, k_a, m, causal=True):
+    """Algorithmic units of one layer in one step: score flops (per pass),
+    Gram flops, top-k bytes, compaction bytes."""
+    pairs = c * n_cache + c * (c + 1) // 2 if causal else c * n
+    score = 2 * d * h_q * pairs
+    gram = h_kv * (k_v * (k_v - 1) + k_a * (k_a - 1)) * d   # K(K-1)/2 pairs x 2d per segment
+    topk = h_kv * n * (4 + 4) + n + 4 * h_kv * m             # a, s, modality in; idx out
+    compact = 2 * 2 * h_kv * m * d * elt                      # K and V rows, read + write
+    return score, gram, topk, compact
+
+
+def work_table(score, gram, topk, compact):
+    """Per-launch algorithmic units of each counted kernel."""
+    return {"lse_pass": ("mfma", score), "colsum_pass": ("mfma", score), "gram_max": ("mfma", gram),
+            "gather_compact": ("hbm", compact), "psi_topk": ("hbm", topk)}
+
+
+def static_work(layers, budgets):
+    tot = [0, 0, 0, 0]
     for lay, (mv, ma) in zip(layers, budgets):
         h_q, c, d = lay["q"].shape
         h_kv, n, _ = lay["k"].shape
-        nc = lay["n_cache"]
-        elt = 2 if lay["dtype"] == "bf16" else 4
-        pairs = c * nc + c * (c + 1) // 2 if causal else c * n
-        score_flops += 2 * d * h_q * pairs
-        for mu in (0, 1):
-            k = int((lay["modality"] == mu).sum())
-            gram_flops += h_kv * k * (k - 1) * d          # k(k-1)/2 pairs x 2d
-        m = int(mv) + int(ma)
-        compact_bytes += 2 * 2 * h_kv * m * d * elt          # K and V rows, read + write
-        topk_bytes += h_kv * n * (4 + 4) + n + 4 * h_kv * m  # a, s, modality in; idx out
-    return {"lse_pass": ("mfma", score_flops), "colsum_pass": ("mfma", score_flops),
-            "gram_max": ("mfma", gram_flops), "gather_compact": ("hbm", compact_bytes),
-            "psi_topk": ("hbm", topk_bytes)}
+        mod = lay["modality"]
+        w = layer_work(h_q, c, lay["n_cache"], h_kv, n, d, 2 if lay["dtype"] == "bf16" else 4,
+                       int((mod == 0).sum()), int((mod == 1).sum()), int(mv) + int(ma))
+        tot = [x + y for x, y in zip(tot, w)]
+    return work_table(*tot)
 
 
 def cpu_baseline(layers, spec):
@@ -125,19 +132,8 @@ def cpu_baseline(layers, spec):
                       f"{dt:.1f} s wall; BLAS threads as cores (exp/sort single-threaded)"}
 
 
-def main():
-    args = parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the step is per layer and KV head; sharding is described in the design notes)",
-              file=sys.stderr)
-        sys.exit(1)
-    if args.copy_calibration:
-        copy_calibration(args.copy_calibration)
-        return
-    import numpy as np
-    import torch
-
+def run_static(args, torch):
+    """K steps of one fixed working set (every step sees the same inputs)."""
     from paper_2606_07577_amd import synth
     from paper_2606_07577_amd.step import DeviceStep
 
@@ -160,8 +156,6 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
     tokens = sum(int(l["k"].shape[1]) for l in layers)
-    value = tokens / (ms / 1e3)
-    print(f"[bench] {ms:.4f} ms/step, {value:.4g} tokens/s", file=sys.stderr, flush=True)
 
     # Same K steps again with per-kernel HIP events on the launch stream.
     step.ctx.omnimem_profile(True)
@@ -171,9 +165,101 @@ def main():
     torch.cuda.synchronize()
     kernels = step.ctx.omnimem_profile_report()
     step.ctx.omnimem_profile(False)
-    budgets = step.budgets.cpu().numpy()
-    work = algorithmic_work(layers, budgets)
-    dtype = layers[0]["dtype"]
+    work = static_work(layers, step.budgets.cpu().numpy())
+    config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
+              "kv_heads": spec["h_kv"], "head_dim": spec["d"], "cache": spec["n_cache_v"] + spec["n_cache_a"],
+              "chunk": spec["n_frames"] * (spec["frame_v"] + spec["frame_a"]), "budget": spec["total_budget"]}
+    baseline = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        baseline = cpu_baseline(layers, spec)
+    step.close()
+    return ms, tokens / (ms / 1e3), kernels, work, layers[0]["dtype"], config, baseline
+
+
+def run_stream(args, torch):
+    """The step after each of K consecutive chunks of a stream, from empty
+    caches.  All chunks are generated on the device before timing; the timed
+    region holds, per chunk, the append of its K/V behind the kept rows, the
+    four library calls and the read-back of the budgets."""
+    from paper_2606_07577_amd import synth
+    from paper_2606_07577_amd.step import StreamRunner
+
+    spec = synth.STREAMS[args.workload]
+    steps = args.steps = min(args.steps, spec["n_chunks"])
+    src = synth.StreamSource(args.workload, backend="torch")
+    chunks = [src.chunk(t) for t in range(steps)]
+    torch.cuda.synchronize()
+
+    def runner():
+        return StreamRunner(spec["n_layers"], spec["h_q"], spec["h_kv"], spec["d"], src.chunk_len,
+                            spec["total_budget"], dtype=spec["dtype"])
+
+    print(f"[bench] stream {args.workload}: {steps} chunks resident, warmup {args.warmup} chunks",
+          file=sys.stderr, flush=True)
+    warm = runner()
+    for t in range(min(args.warmup, steps)):
+        warm.push(chunks[t])
+    warm.close()
+    torch.cuda.synchronize()
+
+    run = runner()
+    stream = torch.cuda.current_stream()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for t in range(steps):
+        run.push(chunks[t], stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    tokens = run.tokens / steps            # working-set rows per step, summed over layers
+    run.close()
+
+    # The same stream again with per-kernel HIP events; per-step work from
+    # the shapes each step saw.
+    run = runner()
+    run.ctx.omnimem_profile(True)
+    tot = [0, 0, 0, 0]
+    elt = 2 if spec["dtype"] == "bf16" else 4
+    for t in range(steps):
+        n_cache = list(run.n_cache)
+        mods = [run.mbuf[run.cur][l][:n_cache[l]].cpu().numpy() for l in range(spec["n_layers"])]
+        budgets = run.push(chunks[t], stream)
+        for l in range(spec["n_layers"]):
+            k_a = int(mods[l].sum()) + spec["n_frames"] * spec["frame_a"]
+            n = n_cache[l] + src.chunk_len
+            w = layer_work(spec["h_q"], src.chunk_len, n_cache[l], spec["h_kv"], n, spec["d"], elt,
+                           n - k_a, k_a, int(budgets[l].sum()))
+            tot = [x + y for x, y in zip(tot, w)]
+    torch.cuda.synchronize()
+    kernels = run.ctx.omnimem_profile_report()
+    run.close()
+    work = work_table(*[x / steps for x in tot])
+    config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
+              "kv_heads": spec["h_kv"], "head_dim": spec["d"], "chunks": steps,
+              "chunk": src.chunk_len, "budget": spec["total_budget"]}
+    return ms, tokens / (ms / 1e3), kernels, work, spec["dtype"], config, None
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the step is per layer and KV head; sharding is described in the design notes)",
+              file=sys.stderr)
+        sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+    import torch
+
+    from paper_2606_07577_amd import synth
+    if args.workload in synth.STREAMS:
+        ms, value, kernels, work, dtype, config, base = run_stream(args, torch)
+    else:
+        ms, value, kernels, work, dtype, config, base = run_static(args, torch)
+    print(f"[bench] {ms:.4f} ms/step, {value:.4g} tokens/s", file=sys.stderr, flush=True)
     per_kernel = {}
     for name, (launches, total_ms) in kernels.items():
         avg_ms = total_ms / max(launches, 1)
@@ -204,23 +290,13 @@ def main():
         "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_max"], PEAK_MFMA_TFLOPS[dtype], 1e12),
         "hbm_frac_topk_compact": stage_frac(["psi_topk", "gather_compact"], PEAK_HBM_GBS, 1e9),
     }
-    base = None
-    if not args.no_cpu_baseline:
-        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
-        base = cpu_baseline(layers, spec)
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": dtype, "data": "synthetic",
-        "config": {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
-                   "kv_heads": spec["h_kv"], "head_dim": spec["d"],
-                   "cache": spec["n_cache_v"] + spec["n_cache_a"],
-                   "chunk": spec["n_frames"] * (spec["frame_v"] + spec["frame_a"]),
-                   "budget": spec["total_budget"]},
+        "vs_baseline": None, "dtype": dtype, "data": "synthetic", "config": config,
         "roofline": roofline, "fractions": fractions, "kernels": per_kernel, "cpu_baseline": base,
     }
     print(json.dumps(out))
-    step.close()
 
 
 if __name__ == "__main__":
