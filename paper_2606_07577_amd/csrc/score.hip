@@ -71,6 +71,39 @@ struct SwzTile {
                                        (__attribute__((address_space(3))) void*)(lds + J * 64 * EPC), 16, 0, 0);
     }
   }
+  // Per-lane byte offsets of the copies of a full tile, computed once: a
+  // full tile's copies then cost no address arithmetic beyond a scalar base.
+  struct Plan {
+    uint32_t off[INSTR_PER_WAVE];
+    bool ok;  // offsets fit in 31 bits
+  };
+  __device__ static inline Plan plan(int64_t row_stride) {
+    Plan p;
+    p.ok = (int64_t)kTile * row_stride * (int64_t)sizeof(T) < (int64_t{1} << 31);
+    const int w = wave_id(), ln = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < INSTR_PER_WAVE; ++j) {
+      const int slot = (w * INSTR_PER_WAVE + j) * 64 + ln;
+      const int row = slot / CPR, c = (slot % CPR) ^ (row & XM);
+      p.off[j] = (uint32_t)(((int64_t)row * row_stride + c * EPC) * (int64_t)sizeof(T));
+    }
+    return p;
+  }
+  // dma() for a tile of `valid` rows, through the plan when the tile is full.
+  __device__ static inline void copy(T* lds, const T* src, int64_t row_stride, int valid, const Plan& p) {
+    if (valid >= kTile && p.ok) {
+      const int w = wave_id();
+#pragma unroll
+      for (int j = 0; j < INSTR_PER_WAVE; ++j) {
+        const int J = w * INSTR_PER_WAVE + j;
+        const char* g = reinterpret_cast<const char*>(src) + p.off[j];
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                         (__attribute__((address_space(3))) void*)(lds + J * 64 * EPC), 16, 0, 0);
+      }
+    } else {
+      dma(lds, src, row_stride, valid);
+    }
+  }
   // MFMA fragment of row r for k-step ks, lane half `half`.
   template <typename M>
   __device__ static inline typename M::frag frag(const T* lds, int r, int ks, int half) {
@@ -95,6 +128,13 @@ __device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memor
   } while (0)
 
 __device__ inline float max3f(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
+
+// Request the LDS fragments of one 32-row block for all k-steps.
+template <typename M, typename Tl, int NKS, typename T>
+__device__ inline void load_frags(typename M::frag (&f)[NKS], const T* lds, int row, int half) {
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) f[ks] = Tl::template frag<M>(lds, row, ks, half);
+}
 
 // 16 MFMAs: one 32-row block of an LDS stage against two 32-column blocks
 // of register operands; each LDS fragment feeds two MFMAs.
@@ -130,6 +170,102 @@ __device__ inline void online_update(const floatx16& acc, float sl2, float& m, f
   m = mnew;
 }
 
+// An empty asm statement that claims to rewrite `v`: later uses of `v` are
+// ordered after it, and volatile statements keep their program order, so a
+// sequence of pins fixes the order in which independent MFMA and VALU work
+// is emitted.  It emits no instruction.
+template <typename V>
+__device__ inline void pin(V& v) { asm volatile("" : "+v"(v)); }
+
+// One pipeline phase of the LSE pass, scheduled by hand: the MFMAs of the
+// 32-key row block `row` of an LDS stage (into `out`) alternate with the
+// exp/sum work on the previous row block `in` (two query columns per lane,
+// 16 scores each).  The work is software-pipelined across groups of one
+// MFMA: a group issues its MFMA, the exps of scores whose exponents the
+// previous group formed, the sums of the previous group's exps and the
+// exponents of the next group, so no instruction waits on one issued just
+// before it.
+//
+// Exponents are taken against the running reference m of the lane's query
+// (not the block maximum): every exp2 stays finite while a score exceeds m
+// by less than 2^7 in log2 units, and sums up to ~2^100 lose nothing in fp32.
+// A block whose sum reaches 2^60 (or overflows; always true for the first
+// block, where m = -1e30) is redone against its true maximum, which becomes
+// the new reference.  So the common path needs no maximum at all.
+//
+// `f` holds the row block's LDS fragments, already requested.  With PF the
+// phase also requests, spread over its groups, the fragments of row block
+// `pf_row` of `pf_lds` into `pf` for the next phase.
+template <typename M, typename Tl, bool PF, int NKS, typename T>
+__device__ inline void lse_phase(floatx16 (&out)[2], typename M::frag (&f)[NKS], int half,
+                                 typename M::frag (&qf)[2][NKS], const floatx16 (&in)[2], float sl2,
+                                 float (&m)[2], float (&lsum)[2], const T* pf_lds, int pf_row,
+                                 typename M::frag (&pf)[NKS]) {
+  static_assert(16 % NKS == 0, "scores per k-step");
+  constexpr int PER = 16 / NKS;   // scores of one column per group
+  constexpr int NG = 2 * NKS;     // groups (one MFMA each)
+  const float neg[2] = {-m[0], -m[1]};
+  float y[2][PER], e[2][PER], s[2][2] = {{0.0f, 0.0f}, {0.0f, 0.0f}};
+  // group g covers column cb = g & 1, scores (g >> 1) * PER .. + PER
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    y[0][i] = __builtin_fmaf(in[0][i], sl2, neg[0]);
+    pin(y[0][i]);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int ks = g >> 1, cb = g & 1, b = g & 1;
+    if (cb == 0) pin(f[ks]);
+    pin(qf[cb][ks]);
+    out[cb] = M::mma(f[ks], qf[cb][ks], ks ? out[cb] : floatx16{});
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      e[b][i] = __builtin_amdgcn_exp2f(y[b][i]);
+      pin(e[b][i]);
+    }
+    if (g > 0) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) s[cb ^ 1][i & 1] += e[b ^ 1][i];
+      pin(s[cb ^ 1][0]);
+      pin(s[cb ^ 1][1]);
+    }
+    if (g + 1 < NG) {
+      const int ncb = (g + 1) & 1, nks = (g + 1) >> 1;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        y[b ^ 1][i] = __builtin_fmaf(in[ncb][nks * PER + i], sl2, neg[ncb]);
+        pin(y[b ^ 1][i]);
+      }
+    }
+    if (PF && cb == 1) pf[ks] = Tl::template frag<M>(pf_lds, pf_row, ks, half);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) s[1][i & 1] += e[(NG - 1) & 1][i];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    const float tot = s[cb][0] + s[cb][1];
+    if (tot < 0x1p60f) {
+      lsum[cb] += tot;
+    } else {
+      float mx = in[cb][0];
+#pragma unroll
+      for (int r = 1; r < 15; r += 2) mx = max3f(mx, in[cb][r], in[cb][r + 1]);
+      mx = fmaxf(mx, in[cb][15]);
+      const float mnew = fmaxf(m[cb], mx * sl2);
+      float t0 = 0.0f, t1 = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        t0 += __builtin_amdgcn_exp2f(__builtin_fmaf(in[cb][r], sl2, -mnew));
+        t1 += __builtin_amdgcn_exp2f(__builtin_fmaf(in[cb][r + 1], sl2, -mnew));
+      }
+      lsum[cb] = lsum[cb] * __builtin_amdgcn_exp2f(m[cb] - mnew) + (t0 + t1);
+      m[cb] = mnew;
+    }
+  }
+}
+
 // Pass 1: for the 256 queries [q0, q0+256) of head h and the keys
 // [kr0, kr1) of one range, the per-query running max m and sum l of
 // exp2(scale_log2 * q.k), merged over both lanes that share a query.
@@ -144,7 +280,8 @@ __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restr
   using M = Mfma<T>;
   using Tl = SwzTile<T, D>;
   constexpr int NKS = D / M::KSTEP;
-  constexpr int NV = (D == 128 && sizeof(T) == 2) ? 7 : 2;  // VALU per MFMA in the interleave
+  constexpr int NV = 2;                   // VALU per MFMA in the compiler-scheduled (fp32) path
+  constexpr bool kHandSched = NKS <= 16;  // bf16: hand-interleaved phases
   __shared__ __attribute__((aligned(16))) T kt0[Tl::ELEMS];
   __shared__ __attribute__((aligned(16))) T kt1[Tl::ELEMS];
 
@@ -177,8 +314,9 @@ __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restr
   const int kend_wave = min(kr1, dm.causal ? min(N, nc + min(qw + kRowsPerWave, C)) : N);
 
   // first tiles on their way before the query fragments are loaded
-  Tl::dma(kt0, k + (int64_t)kr0 * kv_rs, kv_rs, min(kTile, N - kr0));
-  if (kr0 + kTile < kr1) Tl::dma(kt1, k + (int64_t)(kr0 + kTile) * kv_rs, kv_rs, min(kTile, N - kr0 - kTile));
+  const typename Tl::Plan plan = Tl::plan(kv_rs);
+  Tl::copy(kt0, k + (int64_t)kr0 * kv_rs, kv_rs, min(kTile, N - kr0), plan);
+  if (kr0 + kTile < kr1) Tl::copy(kt1, k + (int64_t)(kr0 + kTile) * kv_rs, kv_rs, min(kTile, N - kr0 - kTile), plan);
 
   typename M::frag qf[2][NKS];
 #pragma unroll
@@ -213,9 +351,13 @@ __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restr
 
   const int arow = lane & 31;
   floatx16 acc0[2], acc1[2];  // [query column block] of key row block 0 / 1 of a tile
+  typename M::frag fA[NKS], fB[NKS];  // LDS fragments of row block 1 / 0 of a tile
   dma_wait();
   __syncthreads();            // both first tiles landed in LDS for every wave
-  if (active && kr0 < kend_wave) mma_rows<M, Tl>(acc0, kt0, arow, half, qf);
+  if (active && kr0 < kend_wave) {
+    mma_rows<M, Tl>(acc0, kt0, arow, half, qf);
+    if constexpr (kHandSched) load_frags<M, Tl>(fA, kt0, 32 + arow, half);
+  }
   // One tile t in `cur`; tile t+1 is in (or on its way to) `nxt`.
   auto step = [&](int t, T* cur, const T* nxt) {
     const bool has_next = t + kTile < kr1;
@@ -223,22 +365,32 @@ __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restr
     // phase A: MFMAs of key rows 32..63 of tile t || exp/sum of rows 0..31
     if (busy) {
       if (need_mask(t)) apply_mask(acc0, t);
-      mma_rows<M, Tl>(acc1, cur, 32 + arow, half, qf);
-      online_update(acc0[0], sl2, m[0], lsum[0]);
-      online_update(acc0[1], sl2, m[1], lsum[1]);
-      OMNIMEM_INTERLEAVE(16, NV);
+      if constexpr (kHandSched) {
+        lse_phase<M, Tl, false>(acc1, fA, half, qf, acc0, sl2, m, lsum, cur, 0, fB);
+      } else {
+        mma_rows<M, Tl>(acc1, cur, 32 + arow, half, qf);
+        online_update(acc0[0], sl2, m[0], lsum[0]);
+        online_update(acc0[1], sl2, m[1], lsum[1]);
+        OMNIMEM_INTERLEAVE(16, NV);
+      }
     }
     dma_wait();
     __syncthreads();  // tile t+1 landed; every wave is done with `cur`
-    if (t + 2 * kTile < kr1) Tl::dma(cur, k + (int64_t)(t + 2 * kTile) * kv_rs, kv_rs, min(kTile, N - t - 2 * kTile));
+    if (t + 2 * kTile < kr1)
+      Tl::copy(cur, k + (int64_t)(t + 2 * kTile) * kv_rs, kv_rs, min(kTile, N - t - 2 * kTile), plan);
     // phase B: MFMAs of key rows 0..31 of tile t+1 || exp/sum of rows 32..63 of tile t
     if (busy) {
       if (need_mask(t + 32)) apply_mask(acc1, t + 32);
       if (has_next && t + kTile < kend_wave) {
-        mma_rows<M, Tl>(acc0, nxt, arow, half, qf);
-        online_update(acc1[0], sl2, m[0], lsum[0]);
-        online_update(acc1[1], sl2, m[1], lsum[1]);
-        OMNIMEM_INTERLEAVE(16, NV);
+        if constexpr (kHandSched) {
+          load_frags<M, Tl>(fB, nxt, arow, half);
+          lse_phase<M, Tl, true>(acc0, fB, half, qf, acc1, sl2, m, lsum, nxt, 32 + arow, fA);
+        } else {
+          mma_rows<M, Tl>(acc0, nxt, arow, half, qf);
+          online_update(acc1[0], sl2, m[0], lsum[0]);
+          online_update(acc1[1], sl2, m[1], lsum[1]);
+          OMNIMEM_INTERLEAVE(16, NV);
+        }
       } else {
         online_update(acc1[0], sl2, m[0], lsum[0]);
         online_update(acc1[1], sl2, m[1], lsum[1]);
@@ -316,6 +468,68 @@ __device__ inline void colsum_update(const floatx16 (&acc)[2], const float* lse2
   }
 }
 
+// One pipeline phase of the column-sum pass, scheduled and software-
+// pipelined like lse_phase: the MFMAs of query row block `row` (into `out`)
+// alternate with exp2(score * sl2 - lse2) and its sum over the 16 query rows
+// per lane of the previous row block `in`; row r's normaliser is
+// lse2_rows[(r >> 2) * 8 + half * 4 + (r & 3)].
+template <typename M, typename Tl, int NKS, typename T>
+__device__ inline void colsum_phase(floatx16 (&out)[2], const T* lds, int row, int half,
+                                    typename M::frag (&kf)[2][NKS], const floatx16 (&in)[2],
+                                    const float* lse2_rows, float sl2, float (&cs)[2]) {
+  static_assert(16 % NKS == 0, "scores per k-step");
+  constexpr int PER = 16 / NKS;
+  constexpr int NG = 2 * NKS;
+  float nl[16];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const floatx4 v = *reinterpret_cast<const floatx4*>(lse2_rows + j * 8 + half * 4);
+    nl[j * 4 + 0] = v[0]; nl[j * 4 + 1] = v[1]; nl[j * 4 + 2] = v[2]; nl[j * 4 + 3] = v[3];
+  }
+  typename M::frag f[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) f[ks] = Tl::template frag<M>(lds, row, ks, half);
+  float y[2][PER], e[2][PER], s[2][2] = {{0.0f, 0.0f}, {0.0f, 0.0f}};
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    y[0][i] = __builtin_fmaf(in[0][i], sl2, -nl[i]);
+    pin(y[0][i]);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int ks = g >> 1, cb = g & 1, b = g & 1;
+    if (cb == 0) pin(f[ks]);
+    pin(kf[cb][ks]);
+    out[cb] = M::mma(f[ks], kf[cb][ks], ks ? out[cb] : floatx16{});
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      e[b][i] = __builtin_amdgcn_exp2f(y[b][i]);
+      pin(e[b][i]);
+    }
+    if (g > 0) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) s[cb ^ 1][i & 1] += e[b ^ 1][i];
+      pin(s[cb ^ 1][0]);
+      pin(s[cb ^ 1][1]);
+    }
+    if (g + 1 < NG) {
+      const int ncb = (g + 1) & 1, nks = (g + 1) >> 1;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int r = nks * PER + i;
+        y[b ^ 1][i] = __builtin_fmaf(in[ncb][r], sl2, -nl[r]);
+        pin(y[b ^ 1][i]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) s[1][i & 1] += e[(NG - 1) & 1][i];
+  cs[0] += s[0][0] + s[0][1];
+  cs[1] += s[1][0] + s[1][1];
+}
+
 // Pass 2: per-query-head column sums colsum[h][j] = sum_i exp(S[i][j] -
 // lse[i]) for the 256 keys [k0, k0+256) over one slice of the queries.
 // MFMA tile: rows = 32 queries (A from LDS), columns = 32 keys (B in
@@ -330,7 +544,8 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __re
   using M = Mfma<T>;
   using Tl = SwzTile<T, D>;
   constexpr int NKS = D / M::KSTEP;
-  constexpr int NV = (D == 128 && sizeof(T) == 2) ? 6 : 2;
+  constexpr int NV = 2;                   // VALU per MFMA in the compiler-scheduled (fp32) path
+  constexpr bool kHandSched = NKS <= 16;  // bf16: hand-interleaved phases
   __shared__ __attribute__((aligned(16))) T qt0[Tl::ELEMS];
   __shared__ __attribute__((aligned(16))) T qt1[Tl::ELEMS];
   // normalisers: three slots, because phase B of tile i still reads slot i
@@ -369,11 +584,12 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __re
     return (threadIdx.x < kTile && i < C) ? gload<float>(lse2_lh + i) : INFINITY;
   };
   float lse_next = INFINITY;
+  const typename Tl::Plan plan = Tl::plan(q_rs);
   if (qstart < C) {
-    Tl::dma(qt0, q + (int64_t)qstart * q_rs, q_rs, min(kTile, C - qstart));
+    Tl::copy(qt0, q + (int64_t)qstart * q_rs, q_rs, min(kTile, C - qstart), plan);
     if (threadIdx.x < kTile) lse2[0][threadIdx.x] = load_lse(qstart);
     if (qstart + kTile < C) {
-      Tl::dma(qt1, q + (int64_t)(qstart + kTile) * q_rs, q_rs, min(kTile, C - qstart - kTile));
+      Tl::copy(qt1, q + (int64_t)(qstart + kTile) * q_rs, q_rs, min(kTile, C - qstart - kTile), plan);
       lse_next = load_lse(qstart + kTile);
     }
   }
@@ -417,15 +633,19 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __re
       // phase A: MFMAs of row block 1 of tile qt || exp/sum of row block 0
       if (busy) {
         if (need_mask(qt)) apply_mask(acc0, qt);
-        mma_rows<M, Tl>(acc1, cur, 32 + arow, half, kf);
-        colsum_update(acc0, &lse2[slot][0], half, sl2, cs);
-        OMNIMEM_INTERLEAVE(16, NV);
+        if constexpr (kHandSched) {
+          colsum_phase<M, Tl>(acc1, cur, 32 + arow, half, kf, acc0, &lse2[slot][0], sl2, cs);
+        } else {
+          mma_rows<M, Tl>(acc1, cur, 32 + arow, half, kf);
+          colsum_update(acc0, &lse2[slot][0], half, sl2, cs);
+          OMNIMEM_INTERLEAVE(16, NV);
+        }
       }
       if (has_next && threadIdx.x < kTile) lse2[next_slot][threadIdx.x] = lse_next;
       dma_wait();
       __syncthreads();  // tile qt+1 landed; every wave is done with `cur`
       if (qt + 2 * kTile < C) {
-        Tl::dma(cur, q + (int64_t)(qt + 2 * kTile) * q_rs, q_rs, min(kTile, C - qt - 2 * kTile));
+        Tl::copy(cur, q + (int64_t)(qt + 2 * kTile) * q_rs, q_rs, min(kTile, C - qt - 2 * kTile), plan);
         lse_next = load_lse(qt + 2 * kTile);
       }
       // phase B: MFMAs of row block 0 of tile qt+1 || exp/sum of row block 1.
@@ -434,9 +654,13 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __re
       const bool busy_next = has_next && busy_at(qt + kTile);
       if (busy && need_mask(qt + 32)) apply_mask(acc1, qt + 32);
       if (busy && busy_next) {
-        mma_rows<M, Tl>(acc0, nxt, arow, half, kf);
-        colsum_update(acc1, &lse2[slot][32], half, sl2, cs);
-        OMNIMEM_INTERLEAVE(16, NV);
+        if constexpr (kHandSched) {
+          colsum_phase<M, Tl>(acc0, nxt, arow, half, kf, acc1, &lse2[slot][32], sl2, cs);
+        } else {
+          mma_rows<M, Tl>(acc0, nxt, arow, half, kf);
+          colsum_update(acc1, &lse2[slot][32], half, sl2, cs);
+          OMNIMEM_INTERLEAVE(16, NV);
+        }
       } else if (busy) {
         colsum_update(acc1, &lse2[slot][32], half, sl2, cs);
       } else if (busy_next) {
