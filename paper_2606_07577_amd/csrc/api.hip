@@ -63,6 +63,8 @@ struct omnimem_ctx {
   int next_slot = 0;
   int last_slot = -1;                   // slot holding the last uploaded table
   std::vector<LayerDesc> last_table;
+  PassPlan lse_plan{0, 0}, cs_plan{0, 0};  // score-pass plans of the last table
+  int max_workgroups = 512;               // persistent score-pass grid: 2 per compute unit
   std::string err;
   std::vector<void*> allocations;
   Profiler prof;
@@ -177,6 +179,7 @@ omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t
     const double scale = s.sm_scale != 0.0f ? (double)s.sm_scale : 1.0 / std::sqrt((double)ctx->cfg.head_dim);
     x.scale_log2 = (float)(scale * log2e);
   }
+  plan_score(ctx->dm, t.data(), ctx->max_workgroups, &ctx->lse_plan, &ctx->cs_plan);
   if (ctx->last_slot >= 0 && ctx->last_table.size() == t.size() &&
       std::memcmp(ctx->last_table.data(), t.data(), sizeof(LayerDesc) * L) == 0) {
     *dev = ctx->ws.desc + (size_t)ctx->last_slot * L;
@@ -280,15 +283,19 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
   dm.L = c.n_layers; dm.Hq = c.n_q_heads; dm.Hkv = c.n_kv_heads; dm.G = c.n_q_heads / c.n_kv_heads;
   dm.d = c.head_dim; dm.max_tokens = c.max_tokens; dm.max_chunk = std::max<int64_t>(c.max_chunk, 1);
   dm.causal = c.causal ? 1 : 0;
-  choose_key_ranges(&dm);
+  dm.qb = (int)((dm.max_chunk + kScoreBlock - 1) / kScoreBlock);
+  dm.kb = (int)((dm.max_tokens + kScoreBlock - 1) / kScoreBlock);
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ctx->device) == hipSuccess && cus > 0)
+    ctx->max_workgroups = 2 * cus;
   const size_t L = c.n_layers, Hq = c.n_q_heads, Hkv = c.n_kv_heads, T = c.max_tokens, Cm = dm.max_chunk;
   const int64_t tblocks = (c.max_tokens + kGramTile - 1) / kGramTile;
   Workspace& ws = ctx->ws;
   ws.items_per_layer = (int64_t)Hkv * plan_F(tblocks + 1);
   if ((e = dalloc(ctx, &ws.desc, (size_t)kSlots * L)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.lse_part, L * Hq * (size_t)dm.n_kr * Cm)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.lse_part, L * Hq * (size_t)dm.qb * kMaxSeg * kScoreBlock)) != hipSuccess ||
       (e = dalloc(ctx, &ws.lse2, L * Hq * Cm)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.part, L * Hq * (size_t)dm.n_qc * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.part, L * Hq * (size_t)dm.kb * kMaxSeg * kScoreBlock)) != hipSuccess ||
       (e = dalloc(ctx, &ws.pos, L * 2 * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.rank, L * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.counts, L * 2)) != hipSuccess ||
@@ -344,8 +351,9 @@ omnimem_status omnimem_score(omnimem_ctx* ctx, const omnimem_layer* layers, floa
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
-  return finish(ctx, launch_score(ctx->dm, ctx->cfg.dtype, dev, ctx->ws, lse_out, a, 0, stream), stream,
-                "omnimem_score launch");
+  return finish(ctx, launch_score(ctx->dm, ctx->cfg.dtype, dev, ctx->ws, ctx->lse_plan, ctx->cs_plan, lse_out, a,
+                                  stream),
+                stream, "omnimem_score launch");
 }
 
 omnimem_status omnimem_redundancy(omnimem_ctx* ctx, const omnimem_layer* layers, float* s, hipStream_t stream) {

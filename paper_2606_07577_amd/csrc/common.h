@@ -30,6 +30,11 @@ struct LayerDesc {
   int64_t out_hs, out_rs;
   int32_t n_cache, n_chunk, n;
   float scale_log2;      // softmax scale times log2(e)
+  // Work layout of the two score passes (see PassPlan): the layer's first
+  // tile in each pass's global tile sequence and its tiles per query head.
+  int64_t lse_base, cs_base;
+  int32_t lse_th, cs_th;
+  int64_t lse_rbase, cs_rbase;  // the layer's first row in each pass
 };
 
 // Sizes fixed for a context.
@@ -37,11 +42,53 @@ struct Dims {
   int L, Hq, Hkv, G, d;
   int64_t max_tokens, max_chunk;
   int causal;
-  int krange;   // keys per range of the LSE pass (multiple of 64)
-  int n_kr;     // ranges covering max_tokens
-  int qchunk;   // queries per slice of the column-sum pass (multiple of 64)
-  int n_qc;     // slices covering max_chunk
+  int qb;       // 256-query blocks covering max_chunk
+  int kb;       // 256-key blocks covering max_tokens
 };
+
+// Score-pass work decomposition.  A "row" is one 256-row block that a
+// workgroup keeps in registers (LSE pass: queries of one head; column-sum
+// pass: keys of one query head); its "tiles" are the 64-row tiles it streams
+// past them (LSE: visible key tiles; column sums: query tiles that see a
+// key of the block).  Rows are numbered layer-major, then head, then block,
+// and their tiles form one global sequence of W tiles, cut into chunks of c
+// tiles.  Workgroup i of P takes chunks i, i + P, i + 2P, ...: at any time
+// the P workgroups work on one stretch of the sequence (so the streamed
+// operands of the few heads in it stay in L2), and the work per workgroup
+// differs by at most one chunk.  A chunk may hold parts of several rows;
+// each part writes a partial result for (row, segment), the segment being
+// the chunk's index minus that of the row's first tile.  c is at least
+// (longest row) / (kMaxSeg - 1), so no row has more than kMaxSeg segments.
+// With many more rows than workgroup slots a plan has c = 0 ("row mode"):
+// one workgroup per row, W = the number of rows, and a single segment.
+constexpr int kScoreBlock = 256;  // rows a workgroup keeps in registers
+constexpr int kScoreTile = 64;    // rows per streamed tile
+constexpr int kMaxSeg = 4;
+struct PassPlan {
+  int64_t W;  // tiles
+  int P;      // workgroups
+  int c;      // tiles per chunk
+};
+// Segment of the row starting at tile `start` that holds tile g.
+__host__ __device__ inline int plan_seg(const PassPlan& p, int64_t start, int64_t g) {
+  return p.c == 0 ? 0 : (int)(g / p.c - start / p.c);
+}
+// LSE pass: key tiles seen by the queries [256 b, 256 b + 256).
+__host__ __device__ inline int lse_row_tiles(int N, int nc, int C, int b, int causal) {
+  const int q0 = b * kScoreBlock;
+  if (q0 >= C) return 0;
+  const int kend = causal ? std::min(N, nc + std::min(q0 + kScoreBlock, C)) : N;
+  return (kend + kScoreTile - 1) / kScoreTile;
+}
+// Column-sum pass: first query tile that sees a key of [256 b, 256 b + 256)
+// and the number of query tiles from there.
+__host__ __device__ inline int cs_first_tile(int nc, int b, int causal) {
+  return causal ? std::max(0, b * kScoreBlock - nc) / kScoreTile : 0;
+}
+__host__ __device__ inline int cs_row_tiles(int N, int nc, int C, int b, int causal) {
+  if (b * kScoreBlock >= N) return 0;
+  return std::max(0, (C + kScoreTile - 1) / kScoreTile - cs_first_tile(nc, b, causal));
+}
 
 // Loads through the global address space.  Pointers read from a
 // descriptor are generic; a generic (flat) load also counts against the LDS
@@ -175,9 +222,9 @@ void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
 // ---------------------------------------------------------------------------
 struct Workspace {
   LayerDesc* desc;        // [slots][L]
-  float2* lse_part;       // [L][Hq][n_kr][max_chunk] running (max, sum) in log2 units
+  float2* lse_part;       // [L][Hq][qb][kMaxSeg][256] partial (reference, sum) in log2 units
   float* lse2;            // [L][Hq][max_chunk] merged normaliser, log2 units
-  float* part;            // [L][Hq][n_qc][max_tokens] column sums per query head and slice
+  float* part;            // [L][Hq][kb][kMaxSeg][256] partial column sums per query head
   int* pos;               // [L][2][max_tokens] visual rows, audio rows (ascending)
   int* rank;              // [L][max_tokens]  rank of row j inside its modality
   int* counts;            // [L][2]           K_v, K_a
@@ -195,8 +242,9 @@ struct Workspace {
 
 // Launchers (each returns hipGetLastError() after its launches).
 hipError_t launch_score(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws,
-                        float* lse_out, float* a, int unused, hipStream_t st);
-void choose_key_ranges(Dims* dm);
+                        const PassPlan& lse_plan, const PassPlan& cs_plan, float* lse_out, float* a,
+                        hipStream_t st);
+void plan_score(const Dims& dm, LayerDesc* layers, int max_workgroups, PassPlan* lse_plan, PassPlan* cs_plan);
 int allocate_part_chunks(const Dims& dm);
 hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
                              const Workspace& ws, float* s, hipStream_t st);

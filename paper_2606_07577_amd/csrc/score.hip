@@ -23,8 +23,9 @@ namespace {
 
 constexpr int kThreads = 256;       // 4 wavefronts
 constexpr int kRowsPerWave = 64;    // register-resident rows per wave (two 32-wide MFMA blocks)
-constexpr int kBlockRows = 4 * kRowsPerWave;
-constexpr int kTile = 64;           // streamed rows per LDS stage
+constexpr int kBlockRows = kScoreBlock;  // = 4 * kRowsPerWave
+constexpr int kTile = kScoreTile;        // streamed rows per LDS stage
+static_assert(kBlockRows == 4 * kRowsPerWave, "four waves per block");
 
 __device__ inline float wave_xor32(float x) { return __shfl_xor(x, 32, 64); }
 
@@ -266,43 +267,24 @@ __device__ inline void lse_phase(floatx16 (&out)[2], typename M::frag (&f)[NKS],
   }
 }
 
-// Pass 1: for the 256 queries [q0, q0+256) of head h and the keys
-// [kr0, kr1) of one range, the per-query running max m and sum l of
-// exp2(scale_log2 * q.k), merged over both lanes that share a query.
+// Pass 1, one segment: for the 256 queries [q0, q0+256) of head h of layer
+// l and the keys [kr0, kr1), the per-query reference m and sum of
+// exp2(scale_log2 * q.k - m), merged over both lanes that share a query,
+// written as partial `seg` of row `row`.
 // MFMA tile: rows = 32 keys (A from LDS), columns = 32 queries (B in
 // registers); each lane owns one query and 16 of its keys per tile.
 // Software pipeline inside each wave: the MFMAs of one 32-key row block
 // run while the exp/sum work of the previous row block executes; key tiles
 // arrive by DMA one tile ahead into the LDS stage just consumed.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restrict__ layers, Dims dm,
-                                                        float2* __restrict__ part) {
+__device__ inline void lse_segment(const LayerDesc& Ld, const Dims& dm, int h, int q0, int kr0, int kr1,
+                                   int64_t row, int seg, T* kt0, T* kt1, float2* __restrict__ part) {
   using M = Mfma<T>;
   using Tl = SwzTile<T, D>;
   constexpr int NKS = D / M::KSTEP;
   constexpr int NV = 2;                   // VALU per MFMA in the compiler-scheduled (fp32) path
   constexpr bool kHandSched = NKS <= 16;  // bf16: hand-interleaved phases
-  __shared__ __attribute__((aligned(16))) T kt0[Tl::ELEMS];
-  __shared__ __attribute__((aligned(16))) T kt1[Tl::ELEMS];
-
-  // Workgroups sharing a query head (hence its KV head's keys) run on the
-  // same XCD: consecutive logical ids go to one XCD's L2.
-  const int qblocks = (int)((dm.max_chunk + kBlockRows - 1) / kBlockRows);
-  const int logical = xcd_swizzle(blockIdx.x, gridDim.x);
-  if (logical >= dm.n_kr * qblocks * dm.L * dm.Hq) return;
-  const int range = logical % dm.n_kr;
-  const int qblk = (logical / dm.n_kr) % qblocks;
-  const int lh = logical / (dm.n_kr * qblocks);
-  const int l = lh / dm.Hq, h = lh % dm.Hq;
-  const LayerDesc Ld = layers[l];
-  if (Ld.lse_in) return;
   const int C = Ld.n_chunk, N = Ld.n, nc = Ld.n_cache;
-  const int q0 = qblk * kBlockRows;
-  if (q0 >= C) return;
-  const int kend_blk = dm.causal ? min(N, nc + min(q0 + kBlockRows, C)) : N;
-  const int kr0 = range * dm.krange;
-  if (kr0 >= kend_blk) return;
-  const int kr1 = min(kr0 + dm.krange, kend_blk);
 
   const int wave = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
   const int g = h / dm.G;
@@ -409,14 +391,79 @@ __global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restr
     const float lt = lsum[cb] * __builtin_amdgcn_exp2f(m[cb] - mt) + l2 * __builtin_amdgcn_exp2f(m2 - mt);
     const int my_q = qw + cb * 32 + (lane & 31);
     if (half == 0 && my_q < C)
-      part[(((int64_t)l * dm.Hq + h) * dm.n_kr + range) * dm.max_chunk + my_q] = make_float2(mt, lt);
+      part[(row * kMaxSeg + seg) * kBlockRows + (my_q - q0)] = make_float2(mt, lt);
+  }
+}
+
+// Pass 1 over the plan's tiles (rows = (layer, head, 256-query block),
+// tiles = the block's visible 64-key tiles): each workgroup walks its tile
+// interval row by row.  Consecutive workgroups share rows and heads, so
+// their logical ids go to one XCD's L2.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads, 2) void lse_pass(const LayerDesc* __restrict__ layers, Dims dm, PassPlan pl,
+                                                        float2* __restrict__ part) {
+  using Tl = SwzTile<T, D>;
+  __shared__ __attribute__((aligned(16))) T kt0[Tl::ELEMS];
+  __shared__ __attribute__((aligned(16))) T kt1[Tl::ELEMS];
+  const int i = gridDim.x % kXcds == 0 ? xcd_swizzle(blockIdx.x, gridDim.x) : (int)blockIdx.x;
+  if (pl.c == 0) {  // row mode: row i, whole
+    if (i >= pl.W) return;
+    int l = 0;
+    for (int lo = 0, hi = dm.L - 1; lo < hi;) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (layers[mid].lse_rbase <= i) lo = mid; else hi = mid - 1;
+      l = lo;
+    }
+    const LayerDesc Ld = layers[l];
+    const int nb = (Ld.n_chunk + kBlockRows - 1) / kBlockRows;
+    const int h = (int)((i - Ld.lse_rbase) / nb), b = (int)((i - Ld.lse_rbase) % nb);
+    const int q0 = b * kBlockRows;
+    const int kend_blk = dm.causal ? min(Ld.n, Ld.n_cache + min(q0 + kBlockRows, Ld.n_chunk)) : Ld.n;
+    lse_segment<T, D>(Ld, dm, h, q0, 0, kend_blk, ((int64_t)l * dm.Hq + h) * dm.qb + b, 0, kt0, kt1, part);
+    return;
+  }
+  bool first = true;
+  for (int64_t chunk = i; chunk * pl.c < pl.W; chunk += pl.P) {
+    int64_t g = chunk * pl.c;
+    const int64_t gend = min(pl.W, g + pl.c);
+    // the layer holding tile g: the last layer whose first tile is <= g
+    int l = 0;
+    for (int lo = 0, hi = dm.L - 1; lo < hi;) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (layers[mid].lse_base <= g) lo = mid; else hi = mid - 1;
+      l = lo;
+    }
+    LayerDesc Ld = layers[l];
+    int h = (int)((g - Ld.lse_base) / Ld.lse_th);
+    int ta = (int)((g - Ld.lse_base) % Ld.lse_th), b = 0;
+    for (int t; ta >= (t = lse_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, b, dm.causal)); ta -= t) ++b;
+    for (; g < gend; first = false) {
+      const int tiles = lse_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, b, dm.causal);
+      const int tb = (int)min((int64_t)tiles, ta + (gend - g));
+      const int q0 = b * kBlockRows;
+      const int kend_blk = dm.causal ? min(Ld.n, Ld.n_cache + min(q0 + kBlockRows, Ld.n_chunk)) : Ld.n;
+      if (!first) __syncthreads();  // every wave is done with the stages of the previous segment
+      lse_segment<T, D>(Ld, dm, h, q0, ta * kTile, min(tb * kTile, kend_blk),
+                        ((int64_t)l * dm.Hq + h) * dm.qb + b, plan_seg(pl, g - ta, g), kt0, kt1, part);
+      g += tb - ta;
+      ta = 0;
+      if (++b * kBlockRows >= Ld.n_chunk) {
+        b = 0;
+        if (++h == dm.Hq) {
+          h = 0;
+          do { ++l; } while (g < gend && l < dm.L && layers[l].lse_th == 0);
+          if (g >= gend || l >= dm.L) break;
+          Ld = layers[l];
+        }
+      }
+    }
   }
 }
 
 // Normaliser of every chunk query in log2 units: the caller's lse, or the
-// merge of the key-range partials covering the query's visible keys.
+// merge of the segment partials of the query's row (in segment order).
 // Also writes the natural-log value to lse_out when requested.
-__global__ __launch_bounds__(256) void lse_merge(const LayerDesc* __restrict__ layers, Dims dm,
+__global__ __launch_bounds__(256) void lse_merge(const LayerDesc* __restrict__ layers, Dims dm, PassPlan pl,
                                                  const float2* __restrict__ part, float* __restrict__ lse2,
                                                  float* __restrict__ lse_out) {
   const int l = blockIdx.z, h = blockIdx.y;
@@ -430,14 +477,15 @@ __global__ __launch_bounds__(256) void lse_merge(const LayerDesc* __restrict__ l
     if (lse_out) lse_out[o] = v;
     return;
   }
-  const float2* p = part + ((int64_t)l * dm.Hq + h) * dm.n_kr * dm.max_chunk + i;
-  const int vis = dm.causal ? min(Ld.n, Ld.n_cache + i + 1) : Ld.n;
-  const int nr = (vis + dm.krange - 1) / dm.krange;
-  // one pass, online: (mx, sum) of the ranges seen so far
+  const int b = i / kBlockRows;
+  int64_t start = Ld.lse_base + (int64_t)h * Ld.lse_th;
+  for (int bb = 0; bb < b; ++bb) start += lse_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, bb, dm.causal);
+  const int tiles = lse_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, b, dm.causal);
+  const int nseg = plan_seg(pl, start, start + tiles - 1) + 1;
+  const float2* p = part + ((((int64_t)l * dm.Hq + h) * dm.qb + b) * kMaxSeg) * kBlockRows + (i - b * kBlockRows);
   float mx = -1e30f, sum = 0.0f;
-#pragma unroll 4
-  for (int r = 0; r < nr; ++r) {
-    const float2 v = p[(int64_t)r * dm.max_chunk];
+  for (int sg = 0; sg < nseg; ++sg) {
+    const float2 v = p[sg * kBlockRows];
     const float m2 = fmaxf(mx, v.x);
     sum = sum * __builtin_amdgcn_exp2f(mx - m2) + v.y * __builtin_amdgcn_exp2f(v.x - m2);
     mx = m2;
@@ -530,43 +578,24 @@ __device__ inline void colsum_phase(floatx16 (&out)[2], const T* lds, int row, i
   cs[1] += s[1][0] + s[1][1];
 }
 
-// Pass 2: per-query-head column sums colsum[h][j] = sum_i exp(S[i][j] -
-// lse[i]) for the 256 keys [k0, k0+256) over one slice of the queries.
+// Pass 2, one segment: per-query-head column sums sum_i exp(S[i][j] -
+// lse[i]) for the 256 keys [k0, k0+256) of head h over the chunk queries
+// [qstart, C), written as partial `seg` of row `row`.
 // MFMA tile: rows = 32 queries (A from LDS), columns = 32 keys (B in
 // registers, two blocks per wave); each lane accumulates one key's sum
 // over 16 query rows per tile.  Software pipeline inside each wave: the
 // MFMAs of one 32-query half run while the exp/sum work of the previous
 // half executes; query tiles arrive by DMA one tile ahead.
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __restrict__ layers, Dims dm,
-                                                           const float* __restrict__ lse2_all,
-                                                           float* __restrict__ colsum) {
+__device__ inline void colsum_segment(const LayerDesc& Ld, const Dims& dm, int l, int h, int k0, int qstart,
+                                      int C, int64_t row, int seg, T* qt0, T* qt1, float (&lse2)[3][kTile],
+                                      const float* __restrict__ lse2_all, float* __restrict__ part) {
   using M = Mfma<T>;
   using Tl = SwzTile<T, D>;
   constexpr int NKS = D / M::KSTEP;
   constexpr int NV = 2;                   // VALU per MFMA in the compiler-scheduled (fp32) path
   constexpr bool kHandSched = NKS <= 16;  // bf16: hand-interleaved phases
-  __shared__ __attribute__((aligned(16))) T qt0[Tl::ELEMS];
-  __shared__ __attribute__((aligned(16))) T qt1[Tl::ELEMS];
-  // normalisers: three slots, because phase B of tile i still reads slot i
-  // while a faster wave already stores tile i + 2's values
-  __shared__ __attribute__((aligned(16))) float lse2[3][kTile];
-
-  // Workgroups streaming the same query rows run on the same XCD.
-  const int kblocks = (int)((dm.max_tokens + kBlockRows - 1) / kBlockRows);
-  const int logical = xcd_swizzle(blockIdx.x, gridDim.x);
-  if (logical >= kblocks * dm.Hq * dm.n_qc * dm.L) return;
-  const int kblk = logical % kblocks;
-  const int hq = (logical / kblocks) % (dm.Hq * dm.n_qc);
-  const int l = logical / (kblocks * dm.Hq * dm.n_qc);
-  const int h = hq / dm.n_qc, qc = hq % dm.n_qc;
-  const LayerDesc Ld = layers[l];
   const int N = Ld.n, nc = Ld.n_cache;
-  const int k0 = kblk * kBlockRows;
-  if (k0 >= N) return;
-  // this workgroup's slice of the chunk queries
-  const int C = min(Ld.n_chunk, (qc + 1) * dm.qchunk);
-  const int qlo = qc * dm.qchunk;
   const int wave = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
   const int g = h / dm.G;
   const T* q = reinterpret_cast<const T*>(Ld.q) + (int64_t)h * Ld.q_hs;
@@ -575,8 +604,6 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __re
   const float* lse2_lh = lse2_all + ((int64_t)l * dm.Hq + h) * dm.max_chunk;
   const int kw = k0 + wave * kRowsPerWave;
   const bool active = kw < N;
-  // First query seeing any key of the block (chunk row nc + t is seen by i >= t).
-  const int qstart = max(qlo, dm.causal ? (max(0, k0 - nc) / kTile) * kTile : 0);
   const int qfirst_wave = dm.causal ? max(0, kw - nc) : 0;
   // normaliser of tile row threadIdx.x (+inf past the slice: probability 0)
   auto load_lse = [&](int qt) {
@@ -676,79 +703,191 @@ __global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __re
   if (!active) return;
   cs[0] += wave_xor32(cs[0]);
   cs[1] += wave_xor32(cs[1]);
-  float* out = colsum + (((int64_t)l * dm.Hq + h) * dm.n_qc + qc) * dm.max_tokens;
   const int key = kw + half * 32 + (lane & 31);
-  if (key < N) out[key] = half ? cs[1] : cs[0];
+  if (key < N) part[(row * kMaxSeg + seg) * kBlockRows + (key - k0)] = half ? cs[1] : cs[0];
 }
 
-// a[l][g][j] = sum over the G query heads of KV head g and the query
-// slices, in a fixed order.
-__global__ void head_sum(const LayerDesc* __restrict__ layers, Dims dm, const float* __restrict__ colsum,
-                         float* __restrict__ a) {
-  const int l = blockIdx.z, g = blockIdx.y;
-  const int N = layers[l].n;
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= N) return;
-  const float* p = colsum + ((int64_t)l * dm.Hq + (int64_t)g * dm.G) * dm.n_qc * dm.max_tokens + j;
-  const int n = dm.G * dm.n_qc;
-  float sum = 0.0f;
-  int x = 0;
-  for (; x + 8 <= n; x += 8) {  // eight independent loads in flight
-    float v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = p[(int64_t)(x + u) * dm.max_tokens];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) sum += v[u];
+// Pass 2 over the plan's tiles (rows = (layer, head, 256-key block), tiles
+// = the 64-query tiles that see a key of the block), walked like lse_pass.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads, 2) void colsum_pass(const LayerDesc* __restrict__ layers, Dims dm,
+                                                           PassPlan pl, const float* __restrict__ lse2_all,
+                                                           float* __restrict__ part) {
+  using Tl = SwzTile<T, D>;
+  __shared__ __attribute__((aligned(16))) T qt0[Tl::ELEMS];
+  __shared__ __attribute__((aligned(16))) T qt1[Tl::ELEMS];
+  // normalisers: three slots, because phase B of tile i still reads slot i
+  // while a faster wave already stores tile i + 2's values
+  __shared__ __attribute__((aligned(16))) float lse2[3][kTile];
+  const int i = gridDim.x % kXcds == 0 ? xcd_swizzle(blockIdx.x, gridDim.x) : (int)blockIdx.x;
+  if (pl.c == 0) {  // row mode: row i, whole
+    if (i >= pl.W) return;
+    int l = 0;
+    for (int lo = 0, hi = dm.L - 1; lo < hi;) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (layers[mid].cs_rbase <= i) lo = mid; else hi = mid - 1;
+      l = lo;
+    }
+    const LayerDesc Ld = layers[l];
+    const int nb = (Ld.n + kBlockRows - 1) / kBlockRows;
+    const int h = (int)((i - Ld.cs_rbase) / nb), b = (int)((i - Ld.cs_rbase) % nb);
+    const int t0 = cs_first_tile(Ld.n_cache, b, dm.causal);
+    colsum_segment<T, D>(Ld, dm, l, h, b * kBlockRows, t0 * kTile, Ld.n_chunk, ((int64_t)l * dm.Hq + h) * dm.kb + b, 0,
+                         qt0, qt1, lse2, lse2_all, part);
+    return;
   }
-  for (; x < n; ++x) sum += p[(int64_t)x * dm.max_tokens];
+  bool first = true;
+  for (int64_t chunk = i; chunk * pl.c < pl.W; chunk += pl.P) {
+    int64_t g = chunk * pl.c;
+    const int64_t gend = min(pl.W, g + pl.c);
+    int l = 0;
+    for (int lo = 0, hi = dm.L - 1; lo < hi;) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (layers[mid].cs_base <= g) lo = mid; else hi = mid - 1;
+      l = lo;
+    }
+    LayerDesc Ld = layers[l];
+    int h = (int)((g - Ld.cs_base) / Ld.cs_th);
+    int ta = (int)((g - Ld.cs_base) % Ld.cs_th), b = 0;
+    for (int t; ta >= (t = cs_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, b, dm.causal)); ta -= t) ++b;
+    for (; g < gend; first = false) {
+      const int tiles = cs_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, b, dm.causal);
+      const int tb = (int)min((int64_t)tiles, ta + (gend - g));
+      const int t0 = cs_first_tile(Ld.n_cache, b, dm.causal);
+      if (!first) __syncthreads();  // every wave is done with the stages of the previous segment
+      colsum_segment<T, D>(Ld, dm, l, h, b * kBlockRows, (t0 + ta) * kTile, min(Ld.n_chunk, (t0 + tb) * kTile),
+                           ((int64_t)l * dm.Hq + h) * dm.kb + b, plan_seg(pl, g - ta, g), qt0, qt1, lse2,
+                           lse2_all, part);
+      g += tb - ta;
+      ta = 0;
+      if (++b * kBlockRows >= Ld.n) {
+        b = 0;
+        if (++h == dm.Hq) {
+          h = 0;
+          do { ++l; } while (g < gend && l < dm.L && layers[l].cs_th == 0);
+          if (g >= gend || l >= dm.L) break;
+          Ld = layers[l];
+        }
+      }
+    }
+  }
+}
+
+// a[l][g][j] = sum over the G query heads of KV head g and the segments of
+// their column-sum rows, in a fixed order.
+__global__ void head_sum(const LayerDesc* __restrict__ layers, Dims dm, PassPlan pl,
+                         const float* __restrict__ part, float* __restrict__ a) {
+  const int l = blockIdx.z, g = blockIdx.y;
+  const LayerDesc Ld = layers[l];
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= Ld.n) return;
+  const int b = j / kBlockRows;
+  float sum = 0.0f;
+  const int tiles = cs_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, b, dm.causal);
+  if (Ld.cs_th > 0 && tiles > 0) {
+    int64_t start = Ld.cs_base;
+    for (int bb = 0; bb < b; ++bb) start += cs_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, bb, dm.causal);
+    for (int hh = 0; hh < dm.G; ++hh) {
+      const int h = g * dm.G + hh;
+      const int64_t s0 = start + (int64_t)h * Ld.cs_th;
+      const int nseg = plan_seg(pl, s0, s0 + tiles - 1) + 1;
+      const float* p = part + ((((int64_t)l * dm.Hq + h) * dm.kb + b) * kMaxSeg) * kBlockRows + (j - b * kBlockRows);
+      for (int sg = 0; sg < nseg; ++sg) sum += p[sg * kBlockRows];
+    }
+  }
   a[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = sum;
 }
 
 template <typename T, int D>
-void launch_typed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, float* lse_out, float* a,
-                  hipStream_t st) {
-  const int64_t qblocks = (dm.max_chunk + kBlockRows - 1) / kBlockRows;
-  const dim3 g1(xcd_grid((int64_t)dm.n_kr * qblocks * dm.L * dm.Hq));
-  OMNIMEM_LAUNCH(ws, K_LSE, st, lse_pass<T, D><<<g1, kThreads, 0, st>>>(desc, dm, ws.lse_part));
-  const int64_t kblocks = (dm.max_tokens + kBlockRows - 1) / kBlockRows;
-  const dim3 g2(xcd_grid(kblocks * dm.Hq * dm.n_qc * dm.L));
+void launch_typed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const PassPlan& lp,
+                  const PassPlan& cp, float* lse_out, float* a, hipStream_t st) {
+  if (lp.W > 0)
+    OMNIMEM_LAUNCH(ws, K_LSE, st, lse_pass<T, D><<<lp.P, kThreads, 0, st>>>(desc, dm, lp, ws.lse_part));
   dim3 gm((unsigned)((dm.max_chunk + 255) / 256), dm.Hq, dm.L);
-  OMNIMEM_LAUNCH(ws, K_LSE_MERGE, st, lse_merge<<<gm, 256, 0, st>>>(desc, dm, ws.lse_part, ws.lse2, lse_out));
-  OMNIMEM_LAUNCH(ws, K_COLSUM, st, colsum_pass<T, D><<<g2, kThreads, 0, st>>>(desc, dm, ws.lse2, ws.part));
+  OMNIMEM_LAUNCH(ws, K_LSE_MERGE, st, lse_merge<<<gm, 256, 0, st>>>(desc, dm, lp, ws.lse_part, ws.lse2, lse_out));
+  if (cp.W > 0)
+    OMNIMEM_LAUNCH(ws, K_COLSUM, st, colsum_pass<T, D><<<cp.P, kThreads, 0, st>>>(desc, dm, cp, ws.lse2, ws.part));
   dim3 g3((unsigned)((dm.max_tokens + 255) / 256), dm.Hkv, dm.L);
-  OMNIMEM_LAUNCH(ws, K_HEADSUM, st, head_sum<<<g3, 256, 0, st>>>(desc, dm, ws.part, a));
+  OMNIMEM_LAUNCH(ws, K_HEADSUM, st, head_sum<<<g3, 256, 0, st>>>(desc, dm, cp, ws.part, a));
+}
+
+// Plan a pass of W tiles in `rows` rows, the longest of t_max tiles.  With
+// rows to spare (at least 8 per workgroup slot) the hardware dispatcher
+// balances one workgroup per row best.  Otherwise chunks hold at least
+// t_max / (kMaxSeg - 1) tiles (the bound on segments per row) and, if the
+// work allows, about two rows (a segment's start costs about as much as a
+// few tiles); then as many rounds of P chunks as fit, with the chunk size
+// that fills the rounds evenly.
+PassPlan choose_plan(int64_t W, int64_t rows, int t_max, int max_workgroups) {
+  PassPlan p{W, 0, 1};
+  if (W <= 0) return p;
+  if (rows >= 8 * (int64_t)max_workgroups && rows < (int64_t{1} << 31) / 2) {
+    p.W = rows;
+    p.P = (int)xcd_grid(rows);
+    p.c = 0;
+    return p;
+  }
+  const int64_t c_min = std::max<int64_t>((t_max + kMaxSeg - 2) / (kMaxSeg - 1), 1);
+  const int64_t c_pref = std::max<int64_t>(c_min, std::max(2 * t_max, 32));
+  if (W <= (int64_t)max_workgroups * c_pref) {
+    p.P = (int)std::max<int64_t>(1, std::min<int64_t>(max_workgroups, W / c_min));
+    if (p.P >= kXcds) p.P = p.P / kXcds * kXcds;
+    p.c = (int)((W + p.P - 1) / p.P);
+  } else {
+    const int64_t rounds = W / ((int64_t)max_workgroups * c_pref);
+    p.c = (int)((W + (int64_t)max_workgroups * rounds - 1) / ((int64_t)max_workgroups * rounds));
+    p.P = max_workgroups / kXcds * kXcds;
+  }
+  return p;
 }
 
 }  // namespace
 
-// Work split of both passes: key ranges of the LSE pass and query slices of
-// the column-sum pass, each only as fine as needed to give the chip about
-// 3072 workgroups (ranges never below 512 keys, slices never below 256
-// queries; both multiples of the 64-row stage).
-void choose_key_ranges(Dims* dm) {
-  const int64_t want = 3072;
-  auto split = [&](int64_t base, int64_t len, int64_t min_len, int* out_len, int* out_n) {
-    const int64_t most = std::max<int64_t>(1, len / min_len);
-    const int64_t n = std::min(std::max<int64_t>(1, (want + base - 1) / base), most);
-    int64_t piece = (len + n - 1) / n;
-    piece = (piece + kTile - 1) / kTile * kTile;
-    *out_len = (int)piece;
-    *out_n = (int)((len + piece - 1) / piece);
-  };
-  const int64_t qblocks = (dm->max_chunk + kBlockRows - 1) / kBlockRows;
-  split(qblocks * dm->Hq * dm->L, dm->max_tokens, 512, &dm->krange, &dm->n_kr);
-  const int64_t kblocks = (dm->max_tokens + kBlockRows - 1) / kBlockRows;
-  split(kblocks * dm->Hq * dm->L, dm->max_chunk, 256, &dm->qchunk, &dm->n_qc);
+// Fill each layer's tile bases of both score passes and the two plans.
+void plan_score(const Dims& dm, LayerDesc* layers, int max_workgroups, PassPlan* lse_plan, PassPlan* cs_plan) {
+  int64_t lse_w = 0, cs_w = 0, lse_rows = 0, cs_rows = 0;
+  int lse_tmax = 0, cs_tmax = 0;
+  for (int l = 0; l < dm.L; ++l) {
+    LayerDesc& x = layers[l];
+    int th = 0, nb = 0;
+    if (!x.lse_in) {
+      for (int b = 0; b * kBlockRows < x.n_chunk; ++b, ++nb) {
+        const int t = lse_row_tiles(x.n, x.n_cache, x.n_chunk, b, dm.causal);
+        th += t;
+        lse_tmax = std::max(lse_tmax, t);
+      }
+    }
+    x.lse_base = lse_w;
+    x.lse_th = th;
+    x.lse_rbase = lse_rows;
+    lse_w += (int64_t)dm.Hq * th;
+    lse_rows += th > 0 ? (int64_t)dm.Hq * nb : 0;
+    int ch = 0;
+    nb = 0;
+    for (int b = 0; b * kBlockRows < x.n; ++b, ++nb) {
+      const int t = cs_row_tiles(x.n, x.n_cache, x.n_chunk, b, dm.causal);
+      ch += t;
+      cs_tmax = std::max(cs_tmax, t);
+    }
+    x.cs_base = cs_w;
+    x.cs_th = ch;
+    x.cs_rbase = cs_rows;
+    cs_w += (int64_t)dm.Hq * ch;
+    cs_rows += ch > 0 ? (int64_t)dm.Hq * nb : 0;
+  }
+  *lse_plan = choose_plan(lse_w, lse_rows, lse_tmax, max_workgroups);
+  *cs_plan = choose_plan(cs_w, cs_rows, cs_tmax, max_workgroups);
 }
 
 hipError_t launch_score(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws,
-                        float* lse_out, float* a, int /*unused*/, hipStream_t st) {
+                        const PassPlan& lse_plan, const PassPlan& cs_plan, float* lse_out, float* a,
+                        hipStream_t st) {
   if (dtype == 0) {
-    if (dm.d == 128) launch_typed<uint16_t, 128>(dm, desc, ws, lse_out, a, st);
-    else launch_typed<uint16_t, 64>(dm, desc, ws, lse_out, a, st);
+    if (dm.d == 128) launch_typed<uint16_t, 128>(dm, desc, ws, lse_plan, cs_plan, lse_out, a, st);
+    else launch_typed<uint16_t, 64>(dm, desc, ws, lse_plan, cs_plan, lse_out, a, st);
   } else {
-    if (dm.d == 128) launch_typed<float, 128>(dm, desc, ws, lse_out, a, st);
-    else launch_typed<float, 64>(dm, desc, ws, lse_out, a, st);
+    if (dm.d == 128) launch_typed<float, 128>(dm, desc, ws, lse_plan, cs_plan, lse_out, a, st);
+    else launch_typed<float, 64>(dm, desc, ws, lse_plan, cs_plan, lse_out, a, st);
   }
   return hipGetLastError();
 }
