@@ -230,10 +230,6 @@ hipError_t dalloc(omnimem_ctx* ctx, T** p, size_t count) {
   return e;
 }
 
-int64_t plan_F(int64_t n) {
-  const int64_t q = n / kGramStrip, r = n % kGramStrip;
-  return kGramStrip * q * (q + 1) / 2 + r * (q + 1);
-}
 
 }  // namespace
 
@@ -289,9 +285,9 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ctx->device) == hipSuccess && cus > 0)
     ctx->max_workgroups = 2 * cus;
   const size_t L = c.n_layers, Hq = c.n_q_heads, Hkv = c.n_kv_heads, T = c.max_tokens, Cm = dm.max_chunk;
-  const int64_t tblocks = (c.max_tokens + kGramTile - 1) / kGramTile;
   Workspace& ws = ctx->ws;
-  ws.items_per_layer = (int64_t)Hkv * plan_F(tblocks + 1);
+  ws.gram_grid = ctx->max_workgroups;
+  const size_t elt = c.dtype == OMNIMEM_BF16 ? 2 : 4;
   if ((e = dalloc(ctx, &ws.desc, (size_t)kSlots * L)) != hipSuccess ||
       (e = dalloc(ctx, &ws.lse_part, L * Hq * (size_t)dm.qb * kMaxSeg * kScoreBlock)) != hipSuccess ||
       (e = dalloc(ctx, &ws.lse2, L * Hq * Cm)) != hipSuccess ||
@@ -301,8 +297,7 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       (e = dalloc(ctx, &ws.counts, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.inv_norm, L * Hkv * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.best, L * Hkv * T)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.items, L * (size_t)ws.items_per_layer)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.n_items, L)) != hipSuccess ||
+      (e = dalloc(ctx, reinterpret_cast<char**>(&ws.perm), L * Hkv * T * (size_t)c.head_dim * elt)) != hipSuccess ||
       (e = dalloc(ctx, &ws.stat_part, L * Hkv * (size_t)allocate_part_chunks(dm) * 2 * 4)) != hipSuccess ||
       (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.idx, L * Hkv * T)) != hipSuccess ||

@@ -228,11 +228,10 @@ struct Workspace {
   int* pos;               // [L][2][max_tokens] visual rows, audio rows (ascending)
   int* rank;              // [L][max_tokens]  rank of row j inside its modality
   int* counts;            // [L][2]           K_v, K_a
-  float* inv_norm;        // [L][Hkv][max_tokens]
-  int* best;              // [L][Hkv][max_tokens] ord_f32 of the best cosine
-  int4* items;            // [L][items_per_layer] Gram work items (seg, I, J0, J1)
-  int* n_items;           // [L] items used in each layer's slot range
-  int64_t items_per_layer;
+  float* inv_norm;        // [L][Hkv][max_tokens] inverse norms, segment order
+  int* best;              // [L][Hkv][max_tokens] ord_f32 of the best cosine, segment order
+  void* perm;             // [L][Hkv][max_tokens][d] rows in segment order (visual, then audio)
+  int gram_grid;          // persistent Gram workgroups
   double* stat_part;      // [L][Hkv][chunks][2][4]
   int* eff;               // [L][2] budgets as applied by select
   int* idx;               // [L][Hkv][max_tokens] fallback for the idx output
@@ -248,7 +247,7 @@ void plan_score(const Dims& dm, LayerDesc* layers, int max_workgroups, PassPlan*
 int allocate_part_chunks(const Dims& dm);
 hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
                              const Workspace& ws, float* s, hipStream_t st);
-hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, int make_plan, hipStream_t st);
+hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, hipStream_t st);
 hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspace& ws,
                            const float* a, const float* s, int64_t total, float ratio_r,
                            float temperature, float bmin_frac, float bmax_frac, int32_t* budgets,
@@ -257,8 +256,92 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, const 
                                  const Workspace& ws, const float* a, const float* s,
                                  const int32_t* budgets, int32_t* idx, hipStream_t st);
 
-constexpr int kGramTile = 128;   // rows per Gram block
+// One LDS stage of kScoreTile rows of D elements, unpadded.  The 16-byte chunk c
+// of row r is stored at chunk position c ^ (r & XM): the 16 rows that a
+// quarter-wave reads at the same chunk land on 16 different bank groups.
+// Rows are copied by the global-to-LDS DMA path (global_load_lds_dwordx4),
+// which writes 16 bytes per lane at consecutive LDS slots: no registers and
+// no LDS store instructions.
+template <typename T, int D>
+struct SwzTile {
+  static constexpr int ROWB = D * (int)sizeof(T);   // bytes per row
+  static constexpr int CPR = ROWB / 16;             // chunks per row
+  static constexpr int XM = (CPR < 16 ? CPR : 16) - 1;
+  static constexpr int EPC = 16 / (int)sizeof(T);   // elements per chunk
+  static constexpr int ELEMS = kScoreTile * D;
+  static constexpr int INSTR_PER_WAVE = kScoreTile * CPR / 64 / 4;  // 1 KB copies per wave
 
-constexpr int kGramStrip = 4;    // J blocks per work item
+  // Byte offset of element e of row r.
+  __device__ static inline int off(int r, int e) {
+    return r * ROWB + (((e / EPC) ^ (r & XM)) << 4) + (e % EPC) * (int)sizeof(T);
+  }
+  // Copy rows src[0 .. kScoreTile) (rows at or past `valid` >= 1 repeat row
+  // valid - 1) into `lds`.  Every thread of the block takes part.
+  __device__ static inline void dma(T* lds, const T* src, int64_t row_stride, int valid) {
+    const int w = wave_id(), ln = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < INSTR_PER_WAVE; ++j) {
+      const int J = w * INSTR_PER_WAVE + j;
+      const int slot = J * 64 + ln;
+      const int row = slot / CPR, pos = slot % CPR;
+      const int c = pos ^ (row & XM);
+      const T* g = src + (int64_t)min(row, valid - 1) * row_stride + c * EPC;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                       (__attribute__((address_space(3))) void*)(lds + J * 64 * EPC), 16, 0, 0);
+    }
+  }
+  // Per-lane byte offsets of the copies of a full tile, computed once: a
+  // full tile's copies then cost no address arithmetic beyond a scalar base.
+  struct Plan {
+    uint32_t off[INSTR_PER_WAVE];
+    bool ok;  // offsets fit in 31 bits
+  };
+  __device__ static inline Plan plan(int64_t row_stride) {
+    Plan p;
+    p.ok = (int64_t)kScoreTile * row_stride * (int64_t)sizeof(T) < (int64_t{1} << 31);
+    const int w = wave_id(), ln = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < INSTR_PER_WAVE; ++j) {
+      const int slot = (w * INSTR_PER_WAVE + j) * 64 + ln;
+      const int row = slot / CPR, c = (slot % CPR) ^ (row & XM);
+      p.off[j] = (uint32_t)(((int64_t)row * row_stride + c * EPC) * (int64_t)sizeof(T));
+    }
+    return p;
+  }
+  // dma() for a tile of `valid` rows, through the plan when the tile is full.
+  __device__ static inline void copy(T* lds, const T* src, int64_t row_stride, int valid, const Plan& p) {
+    if (valid >= kScoreTile && p.ok) {
+      const int w = wave_id();
+#pragma unroll
+      for (int j = 0; j < INSTR_PER_WAVE; ++j) {
+        const int J = w * INSTR_PER_WAVE + j;
+        const char* g = reinterpret_cast<const char*>(src) + p.off[j];
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                         (__attribute__((address_space(3))) void*)(lds + J * 64 * EPC), 16, 0, 0);
+      }
+    } else {
+      dma(lds, src, row_stride, valid);
+    }
+  }
+  // MFMA fragment of row r for k-step ks, lane half `half`.
+  template <typename M>
+  __device__ static inline typename M::frag frag(const T* lds, int r, int ks, int half) {
+    const char* base = reinterpret_cast<const char*>(lds);
+    return M::load(reinterpret_cast<const T*>(base + off(r, ks * M::KSTEP + half * M::PER_LANE)));
+  }
+};
+
+// A wave's DMA copies count as vector-memory loads; s_barrier does not wait
+// for them on gfx950, so each wave drains its own copies before the barrier
+// that hands the tile to the other waves.
+__device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// An empty asm statement that claims to rewrite `v`: later uses of `v` are
+// ordered after it, and volatile statements keep their program order, so a
+// sequence of pins fixes the order in which independent MFMA and VALU work
+// is emitted.  It emits no instruction.
+template <typename V>
+__device__ inline void pin(V& v) { asm volatile("" : "+v"(v)); }
+
 
 }  // namespace omnimem

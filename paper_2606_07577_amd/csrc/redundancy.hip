@@ -3,12 +3,15 @@
 //
 // Two modes:
 //  SIM_MAX  s_k = max over the other rows j of k's (KV head, modality)
-//           segment of cos(u_k, u_j).  The segment's Gram matrix U U^T is
-//           tiled 128 x 128 over its upper triangle on MFMA (raw bf16/fp32
-//           inputs, fp32 accumulation), scaled by fp32 inverse norms, and
-//           reduced to row and column maxima in registers; maxima merge with
-//           atomicMax on an order-preserving int encoding.  The N x N matrix
-//           never leaves the chip.
+//           segment of cos(u_k, u_j).  The segment's rows are first gathered
+//           into one contiguous block (visual rows, then audio rows, each in
+//           ascending order) with their fp32 inverse norms; the Gram matrix
+//           U U^T is then computed on MFMA over its upper triangle in
+//           256 x 64 tiles (raw bf16/fp32 inputs, fp32 accumulation),
+//           scaled by the inverse norms and reduced to row and column maxima
+//           in registers; maxima merge with atomicMax on an
+//           order-preserving int encoding.  The N x N matrix never leaves
+//           the chip.
 //  SIM_ADJ  Eq. (7) as printed: mean cosine with the previous and next row
 //           of the same modality, in fp64.
 #include "common.h"
@@ -23,13 +26,10 @@ namespace {
 // list.  One pass, 16 rows per thread.
 constexpr int kListPer = 16;
 
-__device__ inline int64_t plan_F(int64_t n);
 
 __global__ __launch_bounds__(1024) void modality_lists(const LayerDesc* __restrict__ layers, Dims dm,
                                                       int* __restrict__ pos, int* __restrict__ rank,
-                                                      int* __restrict__ counts, int4* __restrict__ items,
-                                                      int* __restrict__ n_items, int64_t items_per_layer,
-                                                      int make_plan) {
+                                                      int* __restrict__ counts) {
   const int l = blockIdx.x;
   const int N = layers[l].n;
   const uint8_t* mod = layers[l].mod;
@@ -73,266 +73,253 @@ __global__ __launch_bounds__(1024) void modality_lists(const LayerDesc* __restri
   }
   const int kv = carry;
   if (threadIdx.x == 0) { counts[2 * l] = kv; counts[2 * l + 1] = N - kv; }
-  if (!make_plan) return;
-
-  // Gram work plan of this layer, in its own slot range [l * per_layer, ...):
-  // segment (g, mu) with T = ceil(K / 128) row blocks owns, for row block
-  // I, ceil((T - I) / S) items of up to S column blocks.
-  __syncthreads();
-  int4* it = items + (int64_t)l * items_per_layer;
-  int64_t ibase = 0;
-  for (int g = 0; g < dm.Hkv; ++g)
-    for (int smu = 0; smu < 2; ++smu) {
-      const int K = smu ? N - kv : kv;
-      const int T = (K + kGramTile - 1) / kGramTile;
-      const int64_t FT = plan_F(T);
-      const int seg = (l * dm.Hkv + g) * 2 + smu;
-      for (int I = threadIdx.x; I < T; I += blockDim.x) {
-        int64_t o = ibase + FT - plan_F(T - I);
-        for (int J0 = I; J0 < T; J0 += kGramStrip, ++o)
-          if (o < items_per_layer) it[o] = make_int4(seg, I, J0, min(T, J0 + kGramStrip));
-      }
-      ibase += FT;
-    }
-  if (threadIdx.x == 0) n_items[l] = (int)min<int64_t>(ibase, items_per_layer);
 }
 
-// --- Gram work plan ----------------------------------------------------------
-// Segment (l, g, mu) with T = ceil(K / 128) row blocks owns, for each row
-// block I, ceil((T - I) / S) items covering column blocks [J0, J0 + S).
-// F(n) = sum_{m=1..n} ceil(m / S) counts the items of rows with n blocks.
-__device__ inline int64_t plan_F(int64_t n) {
-  const int64_t q = n / kGramStrip, r = n % kGramStrip;
-  return kGramStrip * q * (q + 1) / 2 + r * (q + 1);
+// --- gathered rows and inverse norms ------------------------------------------
+// For each (layer, KV head): perm[k] = u[row_k] with row_k the k-th row of
+// the segment order [visual rows ascending | audio rows ascending], its
+// inverse norm 1 / ||u|| in fp64 (0 for a zero row), and best[k] reset.
+// One 16-byte piece per lane.
+// 16 MFMAs: the 32-row block `row` of an LDS stage against two 32-column
+// blocks of register operands; each LDS fragment feeds two MFMAs.
+template <typename M, typename Tl, int NKS, typename T>
+__device__ inline void mma_block(floatx16 (&acc)[2], const T* lds, int row, int half,
+                                 const typename M::frag (&b)[2][NKS]) {
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const typename M::frag f = Tl::template frag<M>(lds, row, ks, half);
+    acc[0] = M::mma(f, b[0][ks], ks ? acc[0] : floatx16{});
+    acc[1] = M::mma(f, b[1][ks], ks ? acc[1] : floatx16{});
+  }
 }
 
-// --- inverse norms -----------------------------------------------------------
-// inv_norm[l][g][j] = 1 / ||u_j|| (0 for a zero row), accumulated in fp64.
 template <typename T, int D>
-__global__ __launch_bounds__(256) void inv_norms(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
-                                                 float* __restrict__ inv, int* __restrict__ best) {
+struct GatherShape {
+  static constexpr int LPR = D * (int)sizeof(T) / 16;  // lanes per row
+  static constexpr int RPB = 256 / LPR;                 // rows per workgroup
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void gather_norms(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
+                                                    const int* __restrict__ pos, const int* __restrict__ counts,
+                                                    T* __restrict__ perm, float* __restrict__ inv,
+                                                    int* __restrict__ best) {
   const int l = blockIdx.z, g = blockIdx.y;
   const LayerDesc Ld = layers[l];
   const int N = Ld.n;
-  constexpr int LPR = 16;                              // lanes per row
+  constexpr int LPR = GatherShape<T, D>::LPR;
   constexpr int EPL = D / LPR;                         // elements per lane
-  const int row = blockIdx.x * (256 / LPR) + threadIdx.x / LPR;
+  const int k = blockIdx.x * GatherShape<T, D>::RPB + threadIdx.x / LPR;
   const int sub = threadIdx.x % LPR;
+  if (k >= N) return;  // whole row groups leave together
+  const int kv = counts[2 * l];
+  const int row = k < kv ? pos[(int64_t)(2 * l) * dm.max_tokens + k] : pos[(int64_t)(2 * l + 1) * dm.max_tokens + k - kv];
   const T* u = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
+  const T* src = u + (int64_t)row * Ld.kv_rs + sub * EPL;
+  const int64_t o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + k;
+  T* dst = perm + o * D + sub * EPL;
   double acc = 0.0;
-  if (row < N) {
-    const T* p = u + (int64_t)row * Ld.kv_rs + sub * EPL;
+  static_assert(EPL * sizeof(T) == 16, "one 16-byte piece per lane");
+  {
+    const uint4 v = gload16(src);
+    *reinterpret_cast<uint4*>(dst) = v;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) {
-      float x;
-      if constexpr (sizeof(T) == 2) x = __uint_as_float(((uint32_t)p[e]) << 16);
-      else x = p[e];
-      acc += (double)x * (double)x;
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (sizeof(T) == 2) {
+        const double a = __uint_as_float(w[e] << 16), b = __uint_as_float(w[e] & 0xFFFF0000u);
+        acc += a * a + b * b;
+      } else {
+        const double a = __uint_as_float(w[e]);
+        acc += a * a;
+      }
     }
   }
 #pragma unroll
-  for (int o = LPR / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
-  if (row < N && sub == 0) {
-    const int64_t o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + row;
+  for (int x = LPR / 2; x > 0; x >>= 1) acc += __shfl_xor(acc, x, 64);
+  if (sub == 0) {
     inv[o] = acc > 0.0 ? (float)(1.0 / sqrt(acc)) : 0.0f;
     best[o] = kNoPartner;  // the Gram pass merges maxima into this
   }
 }
 
+// --- Gram max ------------------------------------------------------------------
+// Work layout: a "row" is one block of 256 segment rows (4 waves x 64) held
+// as MFMA B operands in registers; its "tiles" are all 64-row tiles of the
+// same segment, streamed through LDS by DMA as A operands.  Rows of all
+// segments (layer, KV head, modality) form one tile sequence, cut into
+// chunks that the persistent workgroups take round-robin (as the score
+// passes do).  The full matrix is computed, not its upper triangle: each
+// row's maximum is then complete within its own register block, per lane
+// (a lane holds one register row and 16 tile rows per 32-row block), with
+// no cross-lane reduction or atomics per tile, no per-row norms in
+// registers and one atomicMax per row per chunk.  Per element the work is
+// dot * inv_j and a running maximum; inv_i scales the row's maximum once.
+// Tile rows past the segment carry NaN inverse norms, which fmaxf ignores;
+// a row's pair with itself is masked the same way.
+constexpr int kGramBlock = 256;
 
-// --- Gram max -------------------------------------------------------------
-// One work item = row block I (128 rows) of a segment against column blocks
-// [J0, J1).  Wave w keeps rows w*32 .. w*32+31 of block I as MFMA A operands
-// in registers for the whole item and streams each 128-row column block
-// through double-buffered LDS (B operands, 4 column tiles of 32).  Per
-// element: cos = dot * inv_i * inv_j.  Column maxima are reduced in
-// registers per tile and merged with atomicMax at once; row maxima are
-// carried across the strip and reduced across lanes at the end.  Rows and
-// columns past the segment get a NaN inverse norm, which fmaxf ignores.
-template <typename T, int D>
-struct GramStage {
-  static constexpr int CPR = D * (int)sizeof(T) / 16;
-  static constexpr int PER_THREAD = kGramTile * CPR / 256;
-  static constexpr int LD = D + lds_pad<T>();
-  uint4 r[PER_THREAD];
-  // rows `rows_idx[0 .. valid)` of u; the rest repeat row rows_idx[valid - 1]
-  __device__ inline void load(const T* u, int64_t row_stride, const int* rows_idx, int valid) {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = threadIdx.x + i * 256;
-      const int row = c / CPR, x = c % CPR;
-      const int src = rows_idx[min(row, valid - 1)];
-      r[i] = gload16(u + (int64_t)src * row_stride + x * (16 / sizeof(T)));
-    }
-  }
-  __device__ inline void store(T* lds) const {
-#pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = threadIdx.x + i * 256;
-      const int row = c / CPR, x = c % CPR;
-      *reinterpret_cast<uint4*>(lds + row * LD + x * (16 / sizeof(T))) = r[i];
-    }
-  }
-};
-
-// Accumulator register r holds tile row (r >> 2) * 8 + half * 4 + (r & 3):
-// it is the lane's own column when (r >> 2) * 8 + (r & 3) == d.
-__device__ inline void drop_diagonal(floatx16& a, int d) {
-#pragma unroll
-  for (int r = 0; r < 16; ++r) a[r] = ((r >> 2) * 8 + (r & 3)) == d ? __builtin_nanf("") : a[r];
+// Tiles of a segment of K rows: every 256-row block sees all ceil(K/64).
+__device__ inline int64_t gram_seg_tiles(int K) {
+  const int64_t kt = (K + kScoreTile - 1) / kScoreTile, nb = (K + kGramBlock - 1) / kGramBlock;
+  return nb * kt;
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(256, 2) void gram_max(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
-                                                   const int* __restrict__ pos, const int* __restrict__ counts,
-                                                   const float* __restrict__ inv, const int4* __restrict__ items,
-                                                   const int* __restrict__ n_items, int64_t items_per_layer,
-                                                   int* __restrict__ best) {
+__global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict__ layers, Dims dm,
+                                                    const int* __restrict__ counts, const T* __restrict__ perm,
+                                                    const float* __restrict__ inv, int* __restrict__ best) {
   using M = Mfma<T>;
-  using S = GramStage<T, D>;
+  using Tl = SwzTile<T, D>;
   constexpr int NKS = D / M::KSTEP;
-  constexpr int LD = S::LD;
-  constexpr int TB = kGramTile;
-  __shared__ __attribute__((aligned(16))) T tJ[2][TB * LD];
-  __shared__ float invJ[2][TB];
-  __shared__ int rowsJ[2][TB];
+  constexpr int kMaxL = 1024;
+  __shared__ __attribute__((aligned(16))) T jt0[Tl::ELEMS];
+  __shared__ __attribute__((aligned(16))) T jt1[Tl::ELEMS];
+  __shared__ __attribute__((aligned(16))) float jinv[2][kScoreTile];
+  __shared__ int64_t lbase[kMaxL + 1];  // first tile of each layer
+  __shared__ int64_t sc[2];             // chunk size, total tiles
 
+  // Tile bases of the layers and the chunking (as the score passes choose it).
+  if (threadIdx.x == 0) {
+    int64_t w = 0;
+    int tmax = 0;
+    for (int l = 0; l < dm.L; ++l) {
+      lbase[l] = w;
+      const int kv = counts[2 * l], ka = counts[2 * l + 1];
+      w += (int64_t)dm.Hkv * (gram_seg_tiles(kv) + gram_seg_tiles(ka));
+      tmax = max(tmax, (max(kv, ka) + kScoreTile - 1) / kScoreTile);
+    }
+    lbase[dm.L] = w;
+    const int64_t P = gridDim.x, c_pref = max((int64_t)2 * tmax, (int64_t)32);
+    int64_t c = 1;
+    if (w > 0) {
+      if (w <= P * c_pref) c = (w + P - 1) / P;
+      else { const int64_t rounds = w / (P * c_pref); c = (w + P * rounds - 1) / (P * rounds); }
+    }
+    sc[0] = c;
+    sc[1] = w;
+  }
+  __syncthreads();
+  const int64_t c = sc[0], W = sc[1];
+  const int i = gridDim.x % kXcds == 0 ? xcd_swizzle(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const int wave = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
-  const int64_t total = (int64_t)dm.L * items_per_layer;
-
-  for (int64_t it = blockIdx.x; it < total; it += gridDim.x) {
-    if (it % items_per_layer >= n_items[it / items_per_layer]) continue;  // unused slot
-    const int4 item = items[it];
-    const int seg = item.x, I = item.y, J0 = item.z, J1 = item.w;
-    const int l = seg / (dm.Hkv * 2), g = (seg >> 1) % dm.Hkv, mu = seg & 1;
-    const int K = counts[2 * l + mu];
-    const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
-    const int64_t kv_rs = layers[l].kv_rs;
-    const T* u = reinterpret_cast<const T*>(on_keys ? layers[l].k : layers[l].v) + (int64_t)g * layers[l].kv_hs;
-    const float* inv_g = inv + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
-    int* best_g = best + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
-
-    // this wave's 32 rows of block I: A fragments and inverse norms
-    const int validI = min(TB, K - I * TB);
-    const int r0 = wave * 32;
-    const bool wave_rows = r0 < validI;
-    const int my_row = r0 + (lane & 31);
-    const int my_pos = P[I * TB + min(my_row, validI - 1)];
-    typename M::frag af[NKS];
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-      af[ks] = M::gload(u + (int64_t)my_pos * kv_rs + ks * M::KSTEP + half * M::PER_LANE);
-    float ri[16];  // inverse norms of the 16 rows this lane's accumulators hold
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = r0 + acc_row(r, lane);
-      ri[r] = row < validI ? inv_g[P[I * TB + row]] : __builtin_nanf("");
-    }
-    float rmax[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) rmax[r] = -INFINITY;
-
-    S pre;
-    __syncthreads();  // the previous item is done with the LDS buffers
-    {
-      const int validJ = min(TB, K - J0 * TB);
-      if (threadIdx.x < TB) {
-        const int c = threadIdx.x;
-        const int p = P[J0 * TB + min(c, validJ - 1)];
-        rowsJ[0][c] = p;
-        invJ[0][c] = c < validJ ? inv_g[p] : __builtin_nanf("");
+  const typename Tl::Plan plan = Tl::plan(D);
+  bool first = true;
+  for (int64_t chunk = i; chunk * c < W; chunk += gridDim.x) {
+    int64_t gt = chunk * c;
+    const int64_t gend = min(W, gt + c);
+    while (gt < gend) {
+      // the row holding tile gt: layer, KV head, modality, register block
+      int l = 0;
+      for (int lo = 0, hi = dm.L - 1; lo < hi;) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (lbase[mid] <= gt) lo = mid; else hi = mid - 1;
+        l = lo;
       }
-      __syncthreads();
-      pre.load(u, kv_rs, rowsJ[0], validJ);
-      pre.store(tJ[0]);
-    }
-    int buf = 0;
-    for (int J = J0; J < J1; ++J, buf ^= 1) {
-      const bool has_next = J + 1 < J1;
-      int validJn = 0;
-      if (has_next) {
-        validJn = min(TB, K - (J + 1) * TB);
-        if (threadIdx.x < TB) {
-          const int c = threadIdx.x;
-          const int p = P[(J + 1) * TB + min(c, validJn - 1)];
-          rowsJ[buf ^ 1][c] = p;
-          invJ[buf ^ 1][c] = c < validJn ? inv_g[p] : __builtin_nanf("");
-        }
+      const int kv = counts[2 * l], ka = counts[2 * l + 1];
+      const int64_t tv = gram_seg_tiles(kv), tav = gram_seg_tiles(ka);
+      int64_t rem = gt - lbase[l];
+      const int g = (int)(rem / (tv + tav));
+      rem -= g * (tv + tav);
+      const int mu = rem >= tv ? 1 : 0;
+      if (mu) rem -= tv;
+      const int K = mu ? ka : kv;
+      const int kt = (K + kScoreTile - 1) / kScoreTile;
+      const int I = (int)(rem / kt);
+      const int t0 = (int)(rem % kt);
+      const int t1 = (int)min((int64_t)kt, t0 + (gend - gt));
+      gt += t1 - t0;
+
+      const int64_t seg_off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + (mu ? kv : 0);
+      const T* U = perm + seg_off * D;
+      const float* invs = inv + seg_off;
+      if (!first) __syncthreads();  // every wave is done with the previous segment's stages
+      first = false;
+
+      auto tile_rows = [&](int t) { return min(kScoreTile, K - t * kScoreTile); };
+      auto jinv_of = [&](int t) {  // inverse norm of tile row threadIdx.x (NaN past K)
+        const int row = t * kScoreTile + (int)threadIdx.x;
+        return row < K ? gload<float>(invs + row) : __builtin_nanf("");
+      };
+      Tl::copy(jt0, U + (int64_t)t0 * kScoreTile * D, D, tile_rows(t0), plan);
+      if (threadIdx.x < kScoreTile) jinv[0][threadIdx.x] = jinv_of(t0);
+      float jinv_next = 0.0f;
+      if (t0 + 1 < t1) {
+        Tl::copy(jt1, U + (int64_t)(t0 + 1) * kScoreTile * D, D, tile_rows(t0 + 1), plan);
+        if (threadIdx.x < kScoreTile) jinv_next = jinv_of(t0 + 1);
       }
-      __syncthreads();  // tJ[buf] staged; rowsJ[buf ^ 1] written
-      if (has_next) pre.load(u, kv_rs, rowsJ[buf ^ 1], validJn);
-      const int validJ = min(TB, K - J * TB);
-      if (wave_rows) {
-        floatx16 acc[4];
+      // this wave's 64 register rows (two 32-column blocks of the output)
+      const int c0 = I * kGramBlock + wave * 64;
+      typename M::frag bf[2][NKS];
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) acc[ct] = floatx16{};
-        const T* b0 = tJ[buf] + (lane & 31) * LD + half * M::PER_LANE;
+      for (int cb = 0; cb < 2; ++cb) {
+        const int my = min(c0 + cb * 32 + (lane & 31), K - 1);
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-          for (int ct = 0; ct < 4; ++ct)
-            acc[ct] = M::mma(af[ks], M::load(b0 + ct * 32 * LD + ks * M::KSTEP), acc[ct]);
-        if (I == J) {
-          // the pair (row, row) lies in column tile `wave`: drop it
-          const int d = (lane & 31) - half * 4;
-          switch (wave) {
-            case 0: drop_diagonal(acc[0], d); break;
-            case 1: drop_diagonal(acc[1], d); break;
-            case 2: drop_diagonal(acc[2], d); break;
-            default: drop_diagonal(acc[3], d); break;
-          }
+        for (int ks = 0; ks < NKS; ++ks) bf[cb][ks] = M::gload(U + (int64_t)my * D + ks * M::KSTEP + half * M::PER_LANE);
+      }
+      float rmax[2] = {-INFINITY, -INFINITY};
+      for (int t = t0; t < t1; ++t) {
+        const int st = (t - t0) & 1;
+        const T* cur = st ? jt1 : jt0;
+        if (t > t0 && threadIdx.x < kScoreTile) jinv[st][threadIdx.x] = jinv_next;
+        dma_wait();
+        __syncthreads();  // tile t and its norms landed; tile t-1's stage is free
+        if (t > t0 && t + 1 < t1) {
+          Tl::copy(st ? jt0 : jt1, U + (int64_t)(t + 1) * kScoreTile * D, D, tile_rows(t + 1), plan);
+          if (threadIdx.x < kScoreTile) jinv_next = jinv_of(t + 1);
         }
+        const bool diag = t * kScoreTile < c0 + 64 && c0 < (t + 1) * kScoreTile;
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
-          const int cj = ct * 32 + (lane & 31);
-          const float ij = invJ[buf][cj];
-          float cm = -INFINITY;
+        for (int rb = 0; rb < 2; ++rb) {
+          floatx16 acc[2];
+          mma_block<M, Tl>(acc, cur, rb * 32 + (lane & 31), half, bf);
+          float ij[16];
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            cm = fmaxf(cm, acc[ct][r] * ri[r]);
-            rmax[r] = fmaxf(rmax[r], acc[ct][r] * ij);
+          for (int j = 0; j < 4; ++j) {
+            const floatx4 v = *reinterpret_cast<const floatx4*>(&jinv[st][rb * 32 + j * 8 + half * 4]);
+            ij[j * 4 + 0] = v[0]; ij[j * 4 + 1] = v[1]; ij[j * 4 + 2] = v[2]; ij[j * 4 + 3] = v[3];
           }
-          // both row halves of column cj, scaled by its inverse norm
-          cm = fmaxf(cm, __shfl_xor(cm, 32, 64));
-          if (half == 0 && cj < validJ && cm > -INFINITY) {
-            const float c = fminf(1.0f, fmaxf(-1.0f, cm * ij));
-            atomicMax(best_g + rowsJ[buf][cj], ord_f32(c));
+          if (diag) {
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+              const int d = c0 + cb * 32 + (lane & 31) - (t * kScoreTile + rb * 32);
+#pragma unroll
+              for (int r = 0; r < 16; ++r) acc[cb][r] = acc_row(r, lane) == d ? __builtin_nanf("") : acc[cb][r];
+            }
+          }
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb) {
+            float m = rmax[cb];
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) m = fmaxf(m, fmaxf(acc[cb][r] * ij[r], acc[cb][r + 1] * ij[r + 1]));
+            rmax[cb] = m;
           }
         }
       }
-      if (has_next) pre.store(tJ[buf ^ 1]);
-    }
-    // Row maxima: reduce over the 32 lanes of each half, then merge.
-    if (wave_rows) {
+      // both lane halves hold different tile rows of the same register row
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = rmax[r];
-#pragma unroll
-        for (int o = 16; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-        rmax[r] = v;
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = r0 + acc_row(r, lane);
-        if ((lane & 31) == r && row < validI && rmax[r] > -INFINITY) {
-          const float c = fminf(1.0f, fmaxf(-1.0f, rmax[r] * ri[r]));
-          atomicMax(best_g + P[I * TB + row], ord_f32(c));
-        }
+      for (int cb = 0; cb < 2; ++cb) {
+        const float m = fmaxf(rmax[cb], __shfl_xor(rmax[cb], 32, 64));
+        const int row = c0 + cb * 32 + (lane & 31);
+        if (half == cb && row < K && m > -INFINITY)
+          atomicMax(best + seg_off + row, ord_f32(fminf(1.0f, fmaxf(-1.0f, m * gload<float>(invs + row)))));
       }
     }
   }
 }
 
-// s[l][g][j] from the merged maxima; a row with no partner gets 0.
-__global__ void gram_finish(const LayerDesc* __restrict__ layers, Dims dm, const int* __restrict__ best,
-                            float* __restrict__ s) {
+// s in row order from the segment-order maxima.
+__global__ void gram_finish(const LayerDesc* __restrict__ layers, Dims dm, const int* __restrict__ pos,
+                            const int* __restrict__ counts, const int* __restrict__ best, float* __restrict__ s) {
   const int l = blockIdx.z, g = blockIdx.y;
   const int N = layers[l].n;
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= N) return;
-  const int64_t o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + j;
-  const int b = best[o];
-  s[o] = b == kNoPartner ? 0.0f : fminf(1.0f, fmaxf(-1.0f, unord_f32(b)));
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= N) return;
+  const int kv = counts[2 * l];
+  const int row = k < kv ? pos[(int64_t)(2 * l) * dm.max_tokens + k] : pos[(int64_t)(2 * l + 1) * dm.max_tokens + k - kv];
+  const int64_t o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
+  const int b = best[o + k];
+  s[o + row] = b == kNoPartner ? 0.0f : fminf(1.0f, fmaxf(-1.0f, unord_f32(b)));
 }
 
 // --- SIM_ADJ: Eq. (7) with the modality's own neighbours --------------------
@@ -379,26 +366,26 @@ void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, c
     OMNIMEM_LAUNCH(ws, K_ADJ, st, adjacent_cos<T, D><<<gtok, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts, s));
     return;
   }
-  const dim3 gnorm((unsigned)((dm.max_tokens + 15) / 16), dm.Hkv, dm.L);
-  OMNIMEM_LAUNCH(ws, K_NORMS, st, inv_norms<T, D><<<gnorm, 256, 0, st>>>(desc, dm, on_keys, ws.inv_norm, ws.best));
-  const unsigned grid = (unsigned)std::min<int64_t>((int64_t)dm.L * ws.items_per_layer, 2048);
-  OMNIMEM_LAUNCH(ws, K_GRAM, st, gram_max<T, D><<<grid, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.counts,
-                                       ws.inv_norm, ws.items, ws.n_items, ws.items_per_layer, ws.best));
-  OMNIMEM_LAUNCH(ws, K_GRAM_FINISH, st, gram_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.best, s));
+  constexpr int RPB = GatherShape<T, D>::RPB;
+  const dim3 gnorm((unsigned)((dm.max_tokens + RPB - 1) / RPB), dm.Hkv, dm.L);
+  T* perm = reinterpret_cast<T*>(ws.perm);
+  OMNIMEM_LAUNCH(ws, K_NORMS, st,
+                 gather_norms<T, D><<<gnorm, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.counts, perm, ws.inv_norm, ws.best));
+  OMNIMEM_LAUNCH(ws, K_GRAM, st,
+                 gram_pass<T, D><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.counts, perm, ws.inv_norm, ws.best));
+  OMNIMEM_LAUNCH(ws, K_GRAM_FINISH, st, gram_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.pos, ws.counts, ws.best, s));
 }
 
 }  // namespace
 
-hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, int make_plan, hipStream_t st) {
-  OMNIMEM_LAUNCH(ws, K_LISTS, st,
-                 modality_lists<<<dm.L, 1024, 0, st>>>(desc, dm, ws.pos, ws.rank, ws.counts, ws.items, ws.n_items,
-                                                       ws.items_per_layer, make_plan));
+hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& ws, hipStream_t st) {
+  OMNIMEM_LAUNCH(ws, K_LISTS, st, modality_lists<<<dm.L, 1024, 0, st>>>(desc, dm, ws.pos, ws.rank, ws.counts));
   return hipGetLastError();
 }
 
 hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
                              const Workspace& ws, float* s, hipStream_t st) {
-  hipError_t e = launch_lists(dm, desc, ws, sim == 0, st);
+  hipError_t e = launch_lists(dm, desc, ws, st);
   if (e != hipSuccess) return e;
   if (dtype == 0) {
     if (dm.d == 128) launch_typed<uint16_t, 128>(dm, sim, on_keys, desc, ws, s, st);

@@ -38,85 +38,6 @@ __device__ inline float max16(const floatx16& v) {
   return fmaxf(fmaxf(fmaxf(a, b), fmaxf(c, d)), fmaxf(e, v[15]));
 }
 
-// One LDS stage of kTile rows of D elements, unpadded.  The 16-byte chunk c
-// of row r is stored at chunk position c ^ (r & XM): the 16 rows that a
-// quarter-wave reads at the same chunk land on 16 different bank groups.
-// Rows are copied by the global-to-LDS DMA path (global_load_lds_dwordx4),
-// which writes 16 bytes per lane at consecutive LDS slots: no registers and
-// no LDS store instructions.
-template <typename T, int D>
-struct SwzTile {
-  static constexpr int ROWB = D * (int)sizeof(T);   // bytes per row
-  static constexpr int CPR = ROWB / 16;             // chunks per row
-  static constexpr int XM = (CPR < 16 ? CPR : 16) - 1;
-  static constexpr int EPC = 16 / (int)sizeof(T);   // elements per chunk
-  static constexpr int ELEMS = kTile * D;
-  static constexpr int INSTR_PER_WAVE = kTile * CPR / 64 / 4;  // 1 KB copies per wave
-
-  // Byte offset of element e of row r.
-  __device__ static inline int off(int r, int e) {
-    return r * ROWB + (((e / EPC) ^ (r & XM)) << 4) + (e % EPC) * (int)sizeof(T);
-  }
-  // Copy rows src[0 .. kTile) (rows at or past `valid` >= 1 repeat row
-  // valid - 1) into `lds`.  Every thread of the block takes part.
-  __device__ static inline void dma(T* lds, const T* src, int64_t row_stride, int valid) {
-    const int w = wave_id(), ln = threadIdx.x & 63;
-#pragma unroll
-    for (int j = 0; j < INSTR_PER_WAVE; ++j) {
-      const int J = w * INSTR_PER_WAVE + j;
-      const int slot = J * 64 + ln;
-      const int row = slot / CPR, pos = slot % CPR;
-      const int c = pos ^ (row & XM);
-      const T* g = src + (int64_t)min(row, valid - 1) * row_stride + c * EPC;
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
-                                       (__attribute__((address_space(3))) void*)(lds + J * 64 * EPC), 16, 0, 0);
-    }
-  }
-  // Per-lane byte offsets of the copies of a full tile, computed once: a
-  // full tile's copies then cost no address arithmetic beyond a scalar base.
-  struct Plan {
-    uint32_t off[INSTR_PER_WAVE];
-    bool ok;  // offsets fit in 31 bits
-  };
-  __device__ static inline Plan plan(int64_t row_stride) {
-    Plan p;
-    p.ok = (int64_t)kTile * row_stride * (int64_t)sizeof(T) < (int64_t{1} << 31);
-    const int w = wave_id(), ln = threadIdx.x & 63;
-#pragma unroll
-    for (int j = 0; j < INSTR_PER_WAVE; ++j) {
-      const int slot = (w * INSTR_PER_WAVE + j) * 64 + ln;
-      const int row = slot / CPR, c = (slot % CPR) ^ (row & XM);
-      p.off[j] = (uint32_t)(((int64_t)row * row_stride + c * EPC) * (int64_t)sizeof(T));
-    }
-    return p;
-  }
-  // dma() for a tile of `valid` rows, through the plan when the tile is full.
-  __device__ static inline void copy(T* lds, const T* src, int64_t row_stride, int valid, const Plan& p) {
-    if (valid >= kTile && p.ok) {
-      const int w = wave_id();
-#pragma unroll
-      for (int j = 0; j < INSTR_PER_WAVE; ++j) {
-        const int J = w * INSTR_PER_WAVE + j;
-        const char* g = reinterpret_cast<const char*>(src) + p.off[j];
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
-                                         (__attribute__((address_space(3))) void*)(lds + J * 64 * EPC), 16, 0, 0);
-      }
-    } else {
-      dma(lds, src, row_stride, valid);
-    }
-  }
-  // MFMA fragment of row r for k-step ks, lane half `half`.
-  template <typename M>
-  __device__ static inline typename M::frag frag(const T* lds, int r, int ks, int half) {
-    const char* base = reinterpret_cast<const char*>(lds);
-    return M::load(reinterpret_cast<const T*>(base + off(r, ks * M::KSTEP + half * M::PER_LANE)));
-  }
-};
-
-// A wave's DMA copies count as vector-memory loads; s_barrier does not wait
-// for them on gfx950, so each wave drains its own copies before the barrier
-// that hands the tile to the other waves.
-__device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Interleave `nm` MFMAs with the VALU work of the same basic block:
 // groups of one MFMA followed by `nv` VALU instructions.
@@ -171,12 +92,6 @@ __device__ inline void online_update(const floatx16& acc, float sl2, float& m, f
   m = mnew;
 }
 
-// An empty asm statement that claims to rewrite `v`: later uses of `v` are
-// ordered after it, and volatile statements keep their program order, so a
-// sequence of pins fixes the order in which independent MFMA and VALU work
-// is emitted.  It emits no instruction.
-template <typename V>
-__device__ inline void pin(V& v) { asm volatile("" : "+v"(v)); }
 
 // One pipeline phase of the LSE pass, scheduled by hand: the MFMAs of the
 // 32-key row block `row` of an LDS stage (into `out`) alternate with the
