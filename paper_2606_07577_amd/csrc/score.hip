@@ -398,11 +398,14 @@ __global__ __launch_bounds__(256) void lse_merge(const LayerDesc* __restrict__ l
   const int tiles = lse_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, b, dm.causal);
   const int nseg = plan_seg(pl, start, start + tiles - 1) + 1;
   const float2* p = part + ((((int64_t)l * dm.Hq + h) * dm.qb + b) * kMaxSeg) * kBlockRows + (i - b * kBlockRows);
+  float2 v[kMaxSeg];  // all partials requested before the first is used
+#pragma unroll
+  for (int sg = 0; sg < kMaxSeg; ++sg) v[sg] = sg < nseg ? p[sg * kBlockRows] : make_float2(-1e30f, 0.0f);
   float mx = -1e30f, sum = 0.0f;
-  for (int sg = 0; sg < nseg; ++sg) {
-    const float2 v = p[sg * kBlockRows];
-    const float m2 = fmaxf(mx, v.x);
-    sum = sum * __builtin_amdgcn_exp2f(mx - m2) + v.y * __builtin_amdgcn_exp2f(v.x - m2);
+#pragma unroll
+  for (int sg = 0; sg < kMaxSeg; ++sg) {
+    const float m2 = fmaxf(mx, v[sg].x);
+    sum = sum * __builtin_amdgcn_exp2f(mx - m2) + v[sg].y * __builtin_amdgcn_exp2f(v[sg].x - m2);
     mx = m2;
   }
   const float v2 = mx + __log2f(sum);
@@ -702,12 +705,17 @@ __global__ void head_sum(const LayerDesc* __restrict__ layers, Dims dm, PassPlan
   if (Ld.cs_th > 0 && tiles > 0) {
     int64_t start = Ld.cs_base;
     for (int bb = 0; bb < b; ++bb) start += cs_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, bb, dm.causal);
+    // per query head, all its segment partials requested at once
     for (int hh = 0; hh < dm.G; ++hh) {
       const int h = g * dm.G + hh;
       const int64_t s0 = start + (int64_t)h * Ld.cs_th;
       const int nseg = plan_seg(pl, s0, s0 + tiles - 1) + 1;
       const float* p = part + ((((int64_t)l * dm.Hq + h) * dm.kb + b) * kMaxSeg) * kBlockRows + (j - b * kBlockRows);
-      for (int sg = 0; sg < nseg; ++sg) sum += p[sg * kBlockRows];
+      float v[kMaxSeg];
+#pragma unroll
+      for (int sg = 0; sg < kMaxSeg; ++sg) v[sg] = sg < nseg ? p[sg * kBlockRows] : 0.0f;
+#pragma unroll
+      for (int sg = 0; sg < kMaxSeg; ++sg) sum += v[sg];
     }
   }
   a[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = sum;

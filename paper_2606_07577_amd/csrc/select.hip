@@ -1,14 +1,16 @@
 // Select and compact (Eqs. 4, 5 and 8 of the OmniMem paper).
 //
 //  psi_topk        one workgroup per (layer, KV head, modality): psi =
-//                  a^lambda (1 - s) as an order-preserving 32-bit key,
-//                  radix select of the M-th largest key (4 passes of 8 bits,
-//                  LDS histogram), then an ordered ballot/prefix-sum pass
-//                  that keeps every key above the threshold and the first
-//                  ones equal to it (ties to the lower row), emitting rows
-//                  in ascending order.
+//                  a^lambda (1 - s) as an order-preserving 32-bit key per
+//                  member row (rows dealt to waves in contiguous spans, read
+//                  coalesced), radix select of the M-th largest key (12-bit
+//                  digits below the bits all keys share, LDS histogram),
+//                  then an ordered emission that keeps every key above the
+//                  threshold and the first ones equal to it (ties to the
+//                  lower row), in ascending row order, placed by ballots and
+//                  block-wide scans.
 //  gather_compact  k_out[g][i] = k[g][idx[g][i]] and the same for v, 16 bytes
-//                  per lane, whole 256-byte rows per 16 lanes.
+//                  per lane, whole rows per lane group.
 #include "common.h"
 
 namespace omnimem {
@@ -18,34 +20,17 @@ namespace {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kLdsKeys = 32768;   // member keys of a segment held in LDS (128 KB)
-constexpr int kBins = 2048;       // radix digit of up to 11 bits
+constexpr int kDigit = 12;        // radix digit bits
+constexpr int kBins = 1 << kDigit;
 
+// a^lambda as exp2(lambda * log2 a) on the hardware transcendentals (about
+// 1e-7 relative error, far inside the ordering tolerance of the selection).
 __device__ inline uint32_t psi_key(float a, float s, float lambda) {
   s = fminf(1.0f, fmaxf(-1.0f, s));
-  const float w = lambda == 0.0f ? 1.0f : (a > 0.0f ? powf(a, lambda) : 0.0f);
+  const float w = lambda == 0.0f ? 1.0f : (a > 0.0f ? __builtin_amdgcn_exp2f(lambda * __builtin_amdgcn_logf(a)) : 0.0f);
   float psi = w * (1.0f - s);
   if (!(psi >= 0.0f)) psi = 0.0f;  // NaN or negative inputs rank last
   return __float_as_uint(psi + 0.0f);  // +0 for -0: nonnegative floats order as uints
-}
-
-// Exclusive prefix of `flag` over the block in thread order; *total gets the
-// block's count.  Uses wave_tot[kSelWaves] and two barriers.
-__device__ inline int block_prefix(bool flag, int* wave_tot, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const unsigned long long bal = __ballot(flag);
-  const int before = __popcll(bal & ((1ull << lane) - 1ull));
-  __syncthreads();
-  if (lane == 0) wave_tot[wave] = __popcll(bal);
-  __syncthreads();
-  int base = 0, tot = 0;
-#pragma unroll
-  for (int w = 0; w < kSelWaves; ++w) {
-    const int c = wave_tot[w];
-    base += w < wave ? c : 0;
-    tot += c;
-  }
-  *total = tot;
-  return base + before;
 }
 
 // Inclusive prefix sum of v over the 64 lanes.
@@ -59,6 +44,31 @@ __device__ inline int wave_inclusive(int v) {
   return v;
 }
 
+// Exclusive prefix of v over the block in thread order; *total gets the
+// sum.  Uses wave_tot[kSelWaves] and two barriers.
+__device__ inline int block_scan(int v, int* wave_tot, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int incl = wave_inclusive(v);
+  __syncthreads();
+  if (lane == 63) wave_tot[wave] = incl;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    const int c = wave_tot[w];
+    base += w < wave ? c : 0;
+    tot += c;
+  }
+  *total = tot;
+  return base + incl - v;
+}
+
+// Rows are dealt to waves in contiguous spans: wave w owns rows
+// [w * 64R, (w + 1) * 64R), and step i of the wave covers the 64 consecutive
+// rows w * 64R + 64 i + lane, so every load is coalesced.  Member ranks come
+// from ballots within the wave and one scan of the wave totals; the members'
+// keys sit at their ranks in LDS (or, for segments too large for LDS, by row
+// in global memory).
 __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restrict__ layers, Dims dm, float lambda,
                                                         const float* __restrict__ a, const float* __restrict__ s,
                                                         const int32_t* __restrict__ budgets,
@@ -67,7 +77,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   __shared__ uint32_t skey[kLdsKeys];
   __shared__ int hist[kBins];
   __shared__ int wave_tot[kSelWaves];
-  __shared__ int s_bin, s_need;
+  __shared__ uint32_t wmin[kSelWaves], wmax[kSelWaves];
+  __shared__ int s_bin, s_need, s_cnt;
 
   const int mu = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
   const int N = layers[l].n;
@@ -75,42 +86,102 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   const int64_t off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
   const float* ag = a + off;
   const float* sg = s + off;
-  uint32_t* kg = keys + off;   // keys by working-set row
+  uint32_t* kg = keys + off;   // keys by working-set row (segments past LDS)
   int32_t* ig = idx + off;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  const int R = (N + kSelThreads - 1) / kSelThreads;   // rows per lane
+  const int wrow0 = wave * 64 * R;
+  auto member = [&](int j) { return j < N && (mod[j] ? 1 : 0) == mu; };
 
-  // Pass 0: keys of this modality's rows, by row in global memory and by
-  // member rank in LDS.
-  int K = 0;
-  for (int t0 = 0; t0 < N; t0 += kSelThreads) {
-    const int j = t0 + threadIdx.x;
-    const bool member = j < N && (mod[j] ? 1 : 0) == mu;
-    int cnt;
-    const int rank = K + block_prefix(member, wave_tot, &cnt);
-    if (member) {
-      const uint32_t key = psi_key(ag[j], sg[j], lambda);
-      kg[j] = key;
-      if (rank < kLdsKeys) skey[rank] = key;
+  // Membership of this lane's rows (bit i: row wrow0 + 64 i + lane), read in
+  // groups of 8 steps so their loads are in flight together; with more than
+  // 64 rows per lane the flags are re-read where needed.
+  constexpr int kGrp = 8;
+  const bool bits_ok = R <= 64;
+  unsigned long long mbits = 0;
+  int wcount = 0;
+  for (int i0 = 0; i0 < R; i0 += kGrp) {
+    // branch-free reads (index clamped into the working set), all issued
+    // before the first use
+    int mv[kGrp];
+    bool mb[kGrp];
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) mv[u] = gload<uint8_t>(mod + min(wrow0 + (i0 + u) * 64 + lane, N - 1));
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      pin(mv[u]);
+      mb[u] = i0 + u < R && wrow0 + (i0 + u) * 64 + lane < N && (mv[u] ? 1 : 0) == mu;
     }
-    K += cnt;
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      wcount += __popcll(__ballot(mb[u]));
+      if (mb[u] && i0 + u < 64) mbits |= 1ull << (i0 + u);
+    }
+  }
+  auto member_at = [&](int i, int j) { return bits_ok ? ((mbits >> i) & 1ull) != 0 : member(j); };
+  int K;
+  const int wbase = block_scan(lane == 0 ? wcount : 0, wave_tot, &K);
+  const int rank_base = __shfl(wbase, 0, 64);
+  const bool in_lds = K <= kLdsKeys;
+  // keys at their ranks, and the range they span
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  for (int i0 = 0, run = rank_base; i0 < R; i0 += kGrp) {
+    bool mb[kGrp];
+    float av[kGrp], sv[kGrp];
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      const int j = wrow0 + (i0 + u) * 64 + lane;
+      mb[u] = i0 + u < R && member_at(i0 + u, j);
+      av[u] = gload<float>(ag + min(j, N - 1));
+      sv[u] = gload<float>(sg + min(j, N - 1));
+    }
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) { pin(av[u]); pin(sv[u]); }
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      const unsigned long long bal = __ballot(mb[u]);
+      if (mb[u]) {
+        const uint32_t key = psi_key(av[u], sv[u], lambda);
+        kmin = min(kmin, key);
+        kmax = max(kmax, key);
+        if (in_lds) skey[run + __popcll(bal & lt)] = key;
+        else kg[wrow0 + (i0 + u) * 64 + lane] = key;
+      }
+      run += __popcll(bal);
+    }
   }
   const int M = min(max(budgets[2 * l + mu], 0), K);
   const int Kv = mu ? N - K : K;
   const int Mv = mu ? min(max(budgets[2 * l], 0), Kv) : M;
   if (g == 0 && threadIdx.x == 0) eff[2 * l + mu] = M;
   const int out0 = mu ? Mv : 0;
-  const bool in_lds = K <= kLdsKeys;
-  __syncthreads();
 
-  // Radix select of the M-th largest key, digits of 11, 11 and 10 bits.
+  // Bits shared by every key (keys of psi in a narrow range share sign,
+  // exponent and leading mantissa bits): the radix digits start below them,
+  // which spreads the first histogram over its bins instead of piling its
+  // atomics onto a few.
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, 64));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
+  }
+  if (lane == 0) { wmin[wave] = kmin; wmax[wave] = kmax; }
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) { kmin = min(kmin, wmin[w]); kmax = max(kmax, wmax[w]); }
+  const int width = (kmin ^ kmax) ? 32 - __clz(kmin ^ kmax) : 0;  // low bits in which keys differ
+
+  // Radix select of the M-th largest key over those bits, kDigit at a time.
   uint32_t thr = 0;
-  int take_eq = 0;
+  int take_eq = 0, n_eq = K;  // keys equal to the threshold (all of them when none differ)
   const bool all = M >= K;
   if (!all && M > 0) {
-    uint32_t prefix = 0, mask = 0;
+    uint32_t prefix = kmin & ~((width < 32 ? (1u << width) : 0u) - 1u), mask = ~((width < 32 ? (1u << width) : 0u) - 1u);
     int need = M;
-    for (int pass = 0; pass < 3; ++pass) {
-      const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
-      const uint32_t dmask = pass == 2 ? 1023u : 2047u;
+    for (int top = width; top > 0; top -= kDigit) {
+      const int shift = max(0, top - kDigit);
+      const uint32_t dmask = (1u << (top - shift)) - 1u;
       for (int b = threadIdx.x; b < kBins; b += kSelThreads) hist[b] = 0;
       __syncthreads();
       if (in_lds) {
@@ -126,21 +197,28 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
         }
       }
       __syncthreads();
-      // Counts above each bin, from the top: thread t owns bins 2047-2t, 2046-2t.
-      const int b1 = kBins - 1 - 2 * (int)threadIdx.x, b2 = b1 - 1;
-      const int h1 = hist[b1], h2 = hist[b2];
-      const int incl = wave_inclusive(h1 + h2);
-      const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+      // Counts above each bin, from the top: thread t owns the kPer bins
+      // below kBins - 1 - kPer t.
+      constexpr int kPer = kBins / kSelThreads;
+      const int btop = kBins - 1 - kPer * (int)threadIdx.x;
+      int h[kPer], mine_h = 0;
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) { h[u] = hist[btop - u]; mine_h += h[u]; }
+      const int incl = wave_inclusive(mine_h);
       if (lane == 63) wave_tot[wave] = incl;
       __syncthreads();
-      int above = incl - (h1 + h2);
+      int above = incl - mine_h;
       for (int w = 0; w < wave; ++w) above += wave_tot[w];
-      if (above < need && need <= above + h1) { s_bin = b1; s_need = need - above; }
-      else if (above + h1 < need && need <= above + h1 + h2) { s_bin = b2; s_need = need - above - h1; }
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        if (above < need && need <= above + h[u]) { s_bin = btop - u; s_need = need - above; s_cnt = h[u]; }
+        above += h[u];
+      }
       __syncthreads();
       prefix |= (uint32_t)s_bin << shift;
       mask |= dmask << shift;
       need = s_need;
+      n_eq = s_cnt;
       __syncthreads();
     }
     thr = prefix;
@@ -148,21 +226,78 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   }
 
   // Ordered emission: rows above the threshold and the first `take_eq` rows
-  // equal to it, in ascending row order.
-  int eq_seen = 0, emitted = 0;
-  for (int t0 = 0; t0 < N; t0 += kSelThreads) {
-    const int j = t0 + threadIdx.x;
-    const bool member = j < N && (mod[j] ? 1 : 0) == mu;
-    const uint32_t key = member ? kg[j] : 0u;
-    const bool eq = member && !all && key == thr;
-    int eq_tot;
-    const int eq_rank = eq_seen + block_prefix(eq, wave_tot, &eq_tot);
-    const bool sel = member && (all || (M > 0 && (key > thr || (eq && eq_rank < take_eq))));
-    int sel_tot;
-    const int rank = emitted + block_prefix(sel, wave_tot, &sel_tot);
-    if (sel) ig[out0 + rank] = j;
-    eq_seen += eq_tot;
-    emitted += sel_tot;
+  // equal to it (ties to the lower row), in ascending row order.  Ranks
+  // among the equal keys are needed only when some of them are dropped.
+  const bool pick = !all && M > 0;
+  const bool eq_ranks = pick && n_eq > take_eq;
+  // Keys of steps i0 .. i0+kGrp-1 (members only), read together.
+  auto group_keys = [&](int i0, int run, uint32_t (&kk)[kGrp], unsigned long long (&bal)[kGrp]) {
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      const int j = wrow0 + (i0 + u) * 64 + lane;
+      const bool mb = i0 + u < R && member_at(i0 + u, j);
+      bal[u] = __ballot(mb);
+      kk[u] = mb ? (in_lds ? skey[run + __popcll(bal[u] & lt)] : kg[j]) : 0u;
+      run += __popcll(bal[u]);
+    }
+    return run;
+  };
+  int weq = 0;
+  if (eq_ranks) {
+    for (int i0 = 0, run = rank_base; i0 < R; i0 += kGrp) {
+      uint32_t kk[kGrp];
+      unsigned long long bal[kGrp];
+      run = group_keys(i0, run, kk, bal);
+#pragma unroll
+      for (int u = 0; u < kGrp; ++u) weq += __popcll(__ballot(((bal[u] >> lane) & 1ull) && kk[u] == thr));
+    }
+  }
+  int eq_tot;
+  const int eq_base = __shfl(block_scan(lane == 0 ? weq : 0, wave_tot, &eq_tot), 0, 64);
+  // selection bits of this lane's rows (bit i; past 64 steps they are
+  // recomputed in the writing pass)
+  unsigned long long sbits = 0;
+  int wsel = 0;
+  auto select_group = [&](int i0, int run, int& eqr, unsigned long long (&sb)[kGrp]) {
+    uint32_t kk[kGrp];
+    unsigned long long bal[kGrp];
+    run = group_keys(i0, run, kk, bal);
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      const bool mb = (bal[u] >> lane) & 1ull;
+      const bool eq = pick && mb && kk[u] == thr;
+      const unsigned long long eqb = eq_ranks ? __ballot(eq) : 0ull;
+      const bool sel = mb && (all || (pick && (kk[u] > thr || (eq && (!eq_ranks || eqr + __popcll(eqb & lt) < take_eq)))));
+      eqr += __popcll(eqb);
+      sb[u] = __ballot(sel);
+    }
+    return run;
+  };
+  for (int i0 = 0, run = rank_base, eqr = eq_base; i0 < R; i0 += kGrp) {
+    unsigned long long sb[kGrp];
+    run = select_group(i0, run, eqr, sb);
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      wsel += __popcll(sb[u]);
+      if (i0 + u < 64 && ((sb[u] >> lane) & 1ull)) sbits |= 1ull << (i0 + u);
+    }
+  }
+  int sel_tot;
+  const int out_base = __shfl(block_scan(lane == 0 ? wsel : 0, wave_tot, &sel_tot), 0, 64) + out0;
+  if (wsel == 0) return;
+  for (int i0 = 0, run = rank_base, eqr = eq_base, o = out_base; i0 < R; i0 += kGrp) {
+    unsigned long long sb[kGrp];
+    if (bits_ok) {
+#pragma unroll
+      for (int u = 0; u < kGrp; ++u) sb[u] = __ballot(((sbits >> min(i0 + u, 63)) & 1ull) && i0 + u < R);
+    } else {
+      run = select_group(i0, run, eqr, sb);
+    }
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      if ((sb[u] >> lane) & 1ull) ig[o + __popcll(sb[u] & lt)] = wrow0 + (i0 + u) * 64 + lane;
+      o += __popcll(sb[u]);
+    }
   }
 }
 
