@@ -81,19 +81,27 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
   __shared__ double c_l[kMaxLayers], w_v[kMaxLayers], p[kMaxLayers], x[kMaxLayers];
   __shared__ int n_l[kMaxLayers], k_v[kMaxLayers], lo[kMaxLayers], hi[kMaxLayers], b_l[kMaxLayers];
   __shared__ double s_kappa;
+  __shared__ double bk[2 * kMaxLayers], bf[2 * kMaxLayers];  // breakpoints and f there
   __shared__ double sums[kMaxSums];
   const int L = dm.L;
   const double B = (double)total;
   const double T = (double)temperature;
   const double r = (double)ratio_r;
 
-  // --- chunk partials summed per (layer, head, quantity), in chunk order ---
+  // --- chunk partials summed per (layer, head, quantity), in chunk order;
+  // eight chunks' loads in flight at a time ---
   const int nchunk = part_chunks(dm);
   for (int x = threadIdx.x; x < L * dm.Hkv * kStatSets * 4; x += blockDim.x) {
     const int lg = x / (kStatSets * 4), q = x % (kStatSets * 4);
     const double* src = part + (int64_t)lg * nchunk * kStatSets * 4 + q;
     double t = 0.0;
-    for (int c = 0; c < nchunk; ++c) t += src[c * kStatSets * 4];
+    for (int c0 = 0; c0 < nchunk; c0 += 8) {
+      double v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = c0 + u < nchunk ? src[(c0 + u) * kStatSets * 4] : 0.0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t += v[u];
+    }
     sums[x] = t;
   }
   __syncthreads();
@@ -131,14 +139,23 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
   }
   __syncthreads();
 
-  // --- Eq. (14): softmax over layers of C / T, bounds ---
+  // --- Eq. (14): softmax over layers of C / T (exps in parallel, the max
+  // and the sum in layer order), bounds ---
   if (threadIdx.x == 0) {
     double mx = -INFINITY;
     for (int l = 0; l < L; ++l) mx = fmax(mx, c_l[l] / T);
-    double sum = 0.0;
-    for (int l = 0; l < L; ++l) { p[l] = exp(c_l[l] / T - mx); sum += p[l]; }
-    for (int l = 0; l < L; ++l) p[l] /= sum;
+    s_kappa = mx;
   }
+  __syncthreads();
+  for (int l = threadIdx.x; l < L; l += blockDim.x) p[l] = exp(c_l[l] / T - s_kappa);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double sum = 0.0;
+    for (int l = 0; l < L; ++l) sum += p[l];
+    s_kappa = sum;
+  }
+  __syncthreads();
+  for (int l = threadIdx.x; l < L; l += blockDim.x) p[l] /= s_kappa;
   const int lo_base = (int)ceil(((double)bmin_frac * B) / L);
   const int hi_base = (int)floor(((double)bmax_frac * B) / L);
   for (int l = threadIdx.x; l < L; l += blockDim.x) {
@@ -154,36 +171,31 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
     __syncthreads();
   } else {
     // --- water-fill: kappa with sum_l clamp(kappa B p_l, lo_l, hi_l) = B ---
-    // Breakpoints kappa = lo_l / (B p_l) and hi_l / (B p_l); f is linear in
-    // between.  Thread 0 walks the sorted breakpoints (2L values).
+    // Breakpoints kappa = lo_l / (B p_l) and hi_l / (B p_l); f is
+    // non-decreasing and linear in between.  Each thread evaluates f at its
+    // breakpoints (summing over layers in order); kappa interpolates between
+    // the first breakpoint where f reaches B and the breakpoint before it.
+    auto f = [&](double kap) {
+      double t = 0.0;
+      for (int l = 0; l < L; ++l) t += fmin(fmax(kap * B * p[l], (double)lo[l]), (double)hi[l]);
+      return t;
+    };
+    for (int q = threadIdx.x; q < 2 * L; q += blockDim.x) {
+      const int l = q >> 1;
+      const double kb = p[l] > 0.0 ? ((q & 1) ? hi[l] : lo[l]) / (B * p[l]) : INFINITY;
+      bk[q] = kb;
+      bf[q] = kb < INFINITY ? f(kb) : INFINITY;
+    }
+    __syncthreads();
     if (threadIdx.x == 0) {
-      auto f = [&](double kap) {
-        double t = 0.0;
-        for (int l = 0; l < L; ++l) t += fmin(fmax(kap * B * p[l], (double)lo[l]), (double)hi[l]);
-        return t;
-      };
-      // walk the distinct breakpoints in increasing order
-      double prev_k = 0.0, prev_f = 0.0, kap = 0.0, last = -INFINITY;
-      bool have_prev = false;
-      for (;;) {
-        double kb = INFINITY;  // smallest breakpoint above `last`
-        for (int l = 0; l < L; ++l) {
-          if (!(p[l] > 0.0)) continue;
-          const double c0 = lo[l] / (B * p[l]), c1 = hi[l] / (B * p[l]);
-          if (c0 > last && c0 < kb) kb = c0;
-          if (c1 > last && c1 < kb) kb = c1;
-        }
-        if (kb == INFINITY) break;
-        const double fk = f(kb);
-        if (fk >= B) {
-          kap = have_prev ? prev_k + (B - prev_f) * (kb - prev_k) / (fk - prev_f) : kb;
-          break;
-        }
-        prev_k = kb;
-        prev_f = fk;
-        have_prev = true;
-        last = kb;
-      }
+      double k_hi = INFINITY, f_hi = 0.0;
+      for (int q = 0; q < 2 * L; ++q)
+        if (bf[q] >= B && bk[q] < k_hi) { k_hi = bk[q]; f_hi = bf[q]; }
+      double k_lo = -INFINITY, f_lo = 0.0;
+      for (int q = 0; q < 2 * L; ++q)
+        if (bk[q] < k_hi && bk[q] > k_lo) { k_lo = bk[q]; f_lo = bf[q]; }
+      double kap = 0.0;
+      if (k_hi < INFINITY) kap = k_lo > -INFINITY ? k_lo + (B - f_lo) * (k_hi - k_lo) / (f_hi - f_lo) : k_hi;
       s_kappa = kap;
     }
     __syncthreads();
