@@ -23,8 +23,8 @@ namespace {
 // --- modality lists --------------------------------------------------------
 // Per layer: pos[l][0][0 .. K_v) = visual rows ascending, pos[l][1][0 .. K_a)
 // = audio rows ascending; rank[j] = index of row j inside its modality's
-// list.  One pass, 16 rows per thread.
-constexpr int kListPer = 16;
+// list.  One workgroup per layer: a counting pass, one scan of the wave
+// counts, and a placing pass.
 
 
 __global__ __launch_bounds__(1024) void modality_lists(const LayerDesc* __restrict__ layers, Dims dm,
@@ -35,43 +35,52 @@ __global__ __launch_bounds__(1024) void modality_lists(const LayerDesc* __restri
   const uint8_t* mod = layers[l].mod;
   __shared__ int wave_tot[16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  const unsigned long long lt = (1ull << lane) - 1ull;
   int* Pv = pos + (int64_t)(2 * l) * dm.max_tokens;
   int* Pa = Pv + dm.max_tokens;
   int* R = rank + (int64_t)l * dm.max_tokens;
-  int carry = 0;  // visual rows before the current span
-  for (int base = 0; base < N; base += (int)blockDim.x * kListPer) {
-    const int j0 = base + (int)threadIdx.x * kListPer;
-    uint8_t m[kListPer];
-    int cnt = 0;
+  // Wave w owns rows [w * 64S, (w + 1) * 64S); step i covers the 64
+  // consecutive rows w * 64S + 64 i + lane, so reads and writes coalesce.
+  const int S = (N + (int)blockDim.x - 1) / (int)blockDim.x;
+  const int wrow0 = wave * 64 * S;
+  constexpr int kGrp = 8;
+  auto visual_group = [&](int i0, bool (&vis)[kGrp]) {
+    int m[kGrp];  // branch-free reads (index clamped), all issued before the first use
 #pragma unroll
-    for (int e = 0; e < kListPer; ++e) {
-      m[e] = j0 + e < N ? mod[j0 + e] : 1;
-      cnt += m[e] == 0;
-    }
-    int incl = cnt;  // inclusive scan over the wave
+    for (int u = 0; u < kGrp; ++u) m[u] = gload<uint8_t>(mod + min(wrow0 + (i0 + u) * 64 + lane, N - 1));
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int t = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += t;
+    for (int u = 0; u < kGrp; ++u) {
+      pin(m[u]);
+      vis[u] = i0 + u < S && wrow0 + (i0 + u) * 64 + lane < N && m[u] == 0;
     }
-    __syncthreads();
-    if (lane == 63) wave_tot[wave] = incl;
-    __syncthreads();
-    int rv = carry + incl - cnt, span = 0;
-    for (int w = 0; w < nwaves; ++w) {
-      rv += w < wave ? wave_tot[w] : 0;
-      span += wave_tot[w];
-    }
+  };
+  int wv = 0;  // visual rows of this wave
+  for (int i0 = 0; i0 < S; i0 += kGrp) {
+    bool vis[kGrp];
+    visual_group(i0, vis);
 #pragma unroll
-    for (int e = 0; e < kListPer; ++e) {
-      const int j = j0 + e;
-      if (j >= N) break;
-      if (m[e] == 0) { Pv[rv] = j; R[j] = rv; ++rv; }
-      else { const int ra = j - rv; Pa[ra] = j; R[j] = ra; }
-    }
-    carry += span;
+    for (int u = 0; u < kGrp; ++u) wv += __popcll(__ballot(vis[u]));
   }
-  const int kv = carry;
+  if (lane == 0) wave_tot[wave] = wv;
+  __syncthreads();
+  int vbase = 0, kv = 0;
+  for (int w = 0; w < nwaves; ++w) {
+    vbase += w < wave ? wave_tot[w] : 0;
+    kv += wave_tot[w];
+  }
+  for (int i0 = 0, run = vbase; i0 < S; i0 += kGrp) {
+    bool vis[kGrp];
+    visual_group(i0, vis);
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      const int j = wrow0 + (i0 + u) * 64 + lane;
+      const unsigned long long bal = __ballot(vis[u]);
+      const int rv = run + __popcll(bal & lt);  // visual rows before j
+      if (vis[u]) { Pv[rv] = j; R[j] = rv; }
+      else if (i0 + u < S && j < N) { Pa[j - rv] = j; R[j] = j - rv; }
+      run += __popcll(bal);
+    }
+  }
   if (threadIdx.x == 0) { counts[2 * l] = kv; counts[2 * l + 1] = N - kv; }
 }
 

@@ -328,6 +328,71 @@ def test_long_cache_workload_sampled():
 # Degenerate cases and argument validation
 # ---------------------------------------------------------------------------
 
+def _mixed_layers():
+    """Layers of very different shapes in one call: a long chunk, a cache
+    with a one-row chunk, a chunk without cache, a lone audio row, and a
+    layer larger than the others (different row counts per work plan)."""
+    shapes = [((300, 90), (2, 101, 37)), ((700, 260), (1, 1, 0)), ((0, 0), (3, 64, 21)),
+              ((130, 1), (1, 33, 0)), ((1500, 500), (4, 120, 40))]
+    out = []
+    for l, ((cv, ca), frames) in enumerate(shapes):
+        out.append(synth.make_layer([107, l], h_q=8, h_kv=2, d=128, n_cache_v=cv, n_cache_a=ca,
+                                    n_frames=frames[0], frame_v=frames[1], frame_a=frames[2],
+                                    dup_frac=0.3, head_scale=(0.5, 2.0), dtype="bf16",
+                                    sm_scale=1.0 / ((0.7 + 0.4 * l) * math.sqrt(128))))
+    return out
+
+
+def test_mixed_layer_shapes_in_one_call():
+    # Every stage on layers whose sizes differ widely, so the score-pass and
+    # Gram plans split rows across workgroups, mix layers in one chunk and
+    # meet one-row chunks, cache-free layers and a lone audio row.
+    layers = _mixed_layers()
+    budget = sum(len(x["modality"]) for x in layers) // 3
+    c = Case(layers, budget)
+    for l, lay in enumerate(c.layers64):
+        lse = om.attention_lse(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True)
+        P.assert_close_a(c.lse[l], lse, f"lse layer {l}")
+        a = om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True, lse=lse)
+        P.assert_close_a(c.a[l], a, f"a layer {l}")
+        P.assert_close_s(c.s[l], om.redundancy(lay["v"], lay["modality"], "max"), f"s layer {l}")
+    _chain_properties(c)
+    c.step.close()
+
+
+def test_mixed_shapes_with_caller_lse_on_some_layers():
+    # Layers with a caller-supplied lse drop out of the LSE pass's plan; the
+    # others must be unaffected.
+    layers = _mixed_layers()
+    lay64 = [P.as_f64(x) for x in layers]
+    ref_lse = [om.attention_lse(x["q"], x["k"], x["n_cache"], x["sm_scale"], True) for x in lay64]
+    step = DeviceStep(layers, 1000)
+    given = [torch.from_numpy(ref_lse[l].astype(np.float32)).contiguous().cuda() if l in (1, 3) else None
+             for l in range(len(layers))]
+    step.set_lse_inputs(given)
+    step.score(lse_out=True)
+    _sync()
+    for l, lay in enumerate(lay64):
+        P.assert_close_a(step.host("lse", l), ref_lse[l], f"lse layer {l}")
+        a = om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True, lse=ref_lse[l])
+        P.assert_close_a(step.host("a", l), a, f"a layer {l}")
+    step.close()
+
+
+def test_fp32_head_dim_128():
+    # fp32 inputs at d = 128 (the widest register footprint of the Gram pass).
+    layers = [synth.make_layer([108, 0], h_q=4, h_kv=2, d=128, n_cache_v=150, n_cache_a=50, n_frames=2,
+                               frame_v=40, frame_a=10, dup_frac=0.3, dtype="f32")]
+    c = Case(layers, 120)
+    lay = c.layers64[0]
+    lse = om.attention_lse(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True)
+    P.assert_close_a(c.a[0], om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True,
+                                                     lse=lse))
+    P.assert_close_s(c.s[0], om.redundancy(lay["v"], lay["modality"], "max"))
+    _chain_properties(c)
+    c.step.close()
+
+
 def test_visual_only_layer_and_budget_beyond_tokens():
     layers = ragged_layers(seed=104, caches=((150, 0),), frames=(2, 30, 0))
     c = Case(layers, 1000)   # more budget than the 210 rows: keep everything
