@@ -174,7 +174,7 @@ __device__ inline int64_t gram_seg_tiles(int K) {
   return nb * kt;
 }
 
-template <typename T, int D>
+template <typename T, int D, bool BY_XCD>
 __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict__ layers, Dims dm,
                                                     const int* __restrict__ counts, const T* __restrict__ perm,
                                                     const float* __restrict__ inv, int* __restrict__ best) {
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
   __shared__ __attribute__((aligned(16))) T jt1[Tl::ELEMS];
   __shared__ __attribute__((aligned(16))) float jinv[2][kScoreTile];
   __shared__ int64_t lbase[kMaxL + 1];  // first tile of each layer
-  __shared__ int64_t sc[2];             // chunk size, total tiles
+  __shared__ int64_t sc[3];             // chunk size, total tiles, longest row
 
   // Tile bases of the layers and the chunking (as the score passes choose it).
   if (threadIdx.x == 0) {
@@ -207,6 +207,7 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
     }
     sc[0] = c;
     sc[1] = w;
+    sc[2] = tmax;
   }
   __syncthreads();
   const int64_t c = sc[0], W = sc[1];
@@ -214,9 +215,8 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
   const int wave = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
   const typename Tl::Plan plan = Tl::plan(D);
   bool first = true;
-  for (int64_t chunk = i; chunk * c < W; chunk += gridDim.x) {
-    int64_t gt = chunk * c;
-    const int64_t gend = min(W, gt + c);
+  // Tiles [gt, gend) of the global sequence, row by row.
+  auto run_range = [&](int64_t gt, const int64_t gend) {
     while (gt < gend) {
       // the row holding tile gt: layer, KV head, modality, register block
       int l = 0;
@@ -314,6 +314,35 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
           atomicMax(best + seg_off + row, ord_f32(fminf(1.0f, fmaxf(-1.0f, m * gload<float>(invs + row)))));
       }
     }
+  };
+  if constexpr (BY_XCD) {
+    // Many (layer, KV head) units: unit u goes to the workgroups of XCD
+    // u % 8.  They take the XCD's units k at a time (k units hold about one
+    // longest row per workgroup) and split each group's tiles evenly, so an
+    // XCD's L2 holds the rows of k units at a time instead of those of a
+    // stretch of units spread over the whole chip.
+    const int units = dm.L * dm.Hkv;
+    const int px = (int)gridDim.x / kXcds, x = i / px, ix = i % px;
+    const int64_t per0 = max((int64_t)1, W / max(units, 1));
+    const int k = (int)max((int64_t)1, min((int64_t)8, (sc[2] * px + per0 - 1) / per0));
+    for (int u0 = x; u0 < units; u0 += k * kXcds) {
+      int64_t tot = 0;
+      for (int jj = 0; jj < k && u0 + jj * kXcds < units; ++jj) {
+        const int l = (u0 + jj * kXcds) / dm.Hkv;
+        tot += gram_seg_tiles(counts[2 * l]) + gram_seg_tiles(counts[2 * l + 1]);
+      }
+      const int64_t cu = (tot + px - 1) / px, ga = ix * cu, gb = min(tot, ga + cu);
+      int64_t off = 0;  // [ga, gb) of the concatenation of the group's tiles, unit by unit
+      for (int jj = 0; jj < k && u0 + jj * kXcds < units && off < gb; ++jj) {
+        const int u = u0 + jj * kXcds, l = u / dm.Hkv, g = u % dm.Hkv;
+        const int64_t per = gram_seg_tiles(counts[2 * l]) + gram_seg_tiles(counts[2 * l + 1]);
+        const int64_t lo = max(ga, off), hi = min(gb, off + per);
+        if (lo < hi) run_range(lbase[l] + g * per + (lo - off), lbase[l] + g * per + (hi - off));
+        off += per;
+      }
+    }
+  } else {
+    for (int64_t chunk = i; chunk * c < W; chunk += gridDim.x) run_range(chunk * c, min(W, chunk * c + c));
   }
 }
 
@@ -380,8 +409,12 @@ void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, c
   T* perm = reinterpret_cast<T*>(ws.perm);
   OMNIMEM_LAUNCH(ws, K_NORMS, st,
                  gather_norms<T, D><<<gnorm, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.counts, perm, ws.inv_norm, ws.best));
-  OMNIMEM_LAUNCH(ws, K_GRAM, st,
-                 gram_pass<T, D><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.counts, perm, ws.inv_norm, ws.best));
+  if (dm.L * dm.Hkv >= 2 * kXcds && ws.gram_grid % kXcds == 0)
+    OMNIMEM_LAUNCH(ws, K_GRAM, st,
+                   gram_pass<T, D, true><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.counts, perm, ws.inv_norm, ws.best));
+  else
+    OMNIMEM_LAUNCH(ws, K_GRAM, st,
+                   gram_pass<T, D, false><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.counts, perm, ws.inv_norm, ws.best));
   OMNIMEM_LAUNCH(ws, K_GRAM_FINISH, st, gram_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.pos, ws.counts, ws.best, s));
 }
 
