@@ -83,37 +83,48 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
   __shared__ double s_kappa;
   __shared__ double bk[2 * kMaxLayers], bf[2 * kMaxLayers];  // breakpoints and f there
   __shared__ double sums[kMaxSums];
+  __shared__ double ent[kMaxSums / (kStatSets * 4) * 3];  // per (layer, head): visual, audio, layer
   const int L = dm.L;
   const double B = (double)total;
   const double T = (double)temperature;
   const double r = (double)ratio_r;
 
   // --- chunk partials summed per (layer, head, quantity), in chunk order;
-  // eight chunks' loads in flight at a time ---
+  // sixteen chunks' loads in flight at a time ---
   const int nchunk = part_chunks(dm);
   for (int x = threadIdx.x; x < L * dm.Hkv * kStatSets * 4; x += blockDim.x) {
     const int lg = x / (kStatSets * 4), q = x % (kStatSets * 4);
     const double* src = part + (int64_t)lg * nchunk * kStatSets * 4 + q;
     double t = 0.0;
-    for (int c0 = 0; c0 < nchunk; c0 += 8) {
-      double v[8];
+    for (int c0 = 0; c0 < nchunk; c0 += 16) {
+      double v[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = c0 + u < nchunk ? src[(c0 + u) * kStatSets * 4] : 0.0;
+      for (int u = 0; u < 16; ++u) v[u] = c0 + u < nchunk ? src[(c0 + u) * kStatSets * 4] : 0.0;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) t += v[u];
+      for (int u = 0; u < 16; ++u) t += v[u];
     }
     sums[x] = t;
   }
   __syncthreads();
 
-  // --- per-layer statistics (Eqs. 9, 10, 13) ---
+  // --- per-layer statistics (Eqs. 9, 10, 13); the normalised entropies of
+  // every (layer, head, set) first, in parallel ---
+  for (int q = threadIdx.x; q < L * dm.Hkv * 3; q += blockDim.x) {
+    const double* P = sums + (q / 3) * kStatSets * 4;
+    const int set = q % 3;
+    ent[q] = set == 0 ? norm_entropy(P[0], P[1], P[3])
+                      : set == 1 ? norm_entropy(P[4], P[5], P[7])
+                                 : norm_entropy(P[0] + P[4], P[1] + P[5], P[3] + P[7]);
+  }
+  __syncthreads();
   for (int l = threadIdx.x; l < L; l += blockDim.x) {
     double hv = 0.0, ha = 0.0, hl = 0.0, sv = 0.0, sa = 0.0, cnt_v = 0.0, cnt_a = 0.0;
     for (int g = 0; g < dm.Hkv; ++g) {
       const double* P = sums + (l * dm.Hkv + g) * kStatSets * 4;
-      hv += norm_entropy(P[0], P[1], P[3]);
-      ha += norm_entropy(P[4], P[5], P[7]);
-      hl += norm_entropy(P[0] + P[4], P[1] + P[5], P[3] + P[7]);
+      const double* E = ent + (l * dm.Hkv + g) * 3;
+      hv += E[0];
+      ha += E[1];
+      hl += E[2];
       sv += P[2];
       sa += P[6];
       cnt_v = P[3];

@@ -44,13 +44,12 @@ __device__ inline int wave_inclusive(int v) {
   return v;
 }
 
-// Exclusive prefix of v over the block in thread order; *total gets the
-// sum.  Uses wave_tot[kSelWaves] and two barriers.
-__device__ inline int block_scan(int v, int* wave_tot, int* total) {
+// Exclusive prefix of the per-wave values v (taken from lane 0) over the
+// block in wave order; *total gets the sum.  One barrier; each call site
+// passes its own wave_tot array, so no barrier is needed before the writes.
+__device__ inline int wave_scan(int v, int* wave_tot, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int incl = wave_inclusive(v);
-  __syncthreads();
-  if (lane == 63) wave_tot[wave] = incl;
+  if (lane == 0) wave_tot[wave] = v;
   __syncthreads();
   int base = 0, tot = 0;
 #pragma unroll
@@ -60,7 +59,7 @@ __device__ inline int block_scan(int v, int* wave_tot, int* total) {
     tot += c;
   }
   *total = tot;
-  return base + incl - v;
+  return base;
 }
 
 // Rows are dealt to waves in contiguous spans: wave w owns rows
@@ -77,8 +76,9 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   __shared__ uint32_t skey[kLdsKeys];
   __shared__ int hist[kBins];
   __shared__ int wave_tot[kSelWaves];
-  __shared__ uint32_t wmin[kSelWaves], wmax[kSelWaves];
   __shared__ int s_bin, s_need, s_cnt;
+  __shared__ int wt_mem[kSelWaves], wt_eq[kSelWaves], wt_sel[kSelWaves];
+  __shared__ uint32_t wmin[kSelWaves], wmax[kSelWaves];
 
   const int mu = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
   const int N = layers[l].n;
@@ -96,18 +96,30 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
 
   // Membership of this lane's rows (bit i: row wrow0 + 64 i + lane), read in
   // groups of 8 steps so their loads are in flight together; with more than
-  // 64 rows per lane the flags are re-read where needed.
+  // 64 rows per lane the flags are re-read where needed.  With at most one
+  // group (R <= 8) the rows' a and s are read in the same round and the
+  // keys kept in registers.
   constexpr int kGrp = 8;
   const bool bits_ok = R <= 64;
+  const bool one_grp = R <= kGrp;
   unsigned long long mbits = 0;
   int wcount = 0;
+  uint32_t kreg[kGrp];
   for (int i0 = 0; i0 < R; i0 += kGrp) {
     // branch-free reads (index clamped into the working set), all issued
     // before the first use
     int mv[kGrp];
+    float av[kGrp], sv[kGrp];
     bool mb[kGrp];
 #pragma unroll
-    for (int u = 0; u < kGrp; ++u) mv[u] = gload<uint8_t>(mod + min(wrow0 + (i0 + u) * 64 + lane, N - 1));
+    for (int u = 0; u < kGrp; ++u) {
+      const int j = min(wrow0 + (i0 + u) * 64 + lane, N - 1);
+      mv[u] = gload<uint8_t>(mod + j);
+      if (one_grp) {
+        av[u] = gload<float>(ag + j);
+        sv[u] = gload<float>(sg + j);
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kGrp; ++u) {
       pin(mv[u]);
@@ -117,12 +129,12 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     for (int u = 0; u < kGrp; ++u) {
       wcount += __popcll(__ballot(mb[u]));
       if (mb[u] && i0 + u < 64) mbits |= 1ull << (i0 + u);
+      if (one_grp) kreg[u] = psi_key(av[u], sv[u], lambda);
     }
   }
   auto member_at = [&](int i, int j) { return bits_ok ? ((mbits >> i) & 1ull) != 0 : member(j); };
   int K;
-  const int wbase = block_scan(lane == 0 ? wcount : 0, wave_tot, &K);
-  const int rank_base = __shfl(wbase, 0, 64);
+  const int rank_base = wave_scan(wcount, wt_mem, &K);
   const bool in_lds = K <= kLdsKeys;
   // keys at their ranks, and the range they span
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
@@ -133,16 +145,20 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     for (int u = 0; u < kGrp; ++u) {
       const int j = wrow0 + (i0 + u) * 64 + lane;
       mb[u] = i0 + u < R && member_at(i0 + u, j);
-      av[u] = gload<float>(ag + min(j, N - 1));
-      sv[u] = gload<float>(sg + min(j, N - 1));
+      if (!one_grp) {
+        av[u] = gload<float>(ag + min(j, N - 1));
+        sv[u] = gload<float>(sg + min(j, N - 1));
+      }
     }
+    if (!one_grp) {
 #pragma unroll
-    for (int u = 0; u < kGrp; ++u) { pin(av[u]); pin(sv[u]); }
+      for (int u = 0; u < kGrp; ++u) { pin(av[u]); pin(sv[u]); }
+    }
 #pragma unroll
     for (int u = 0; u < kGrp; ++u) {
       const unsigned long long bal = __ballot(mb[u]);
       if (mb[u]) {
-        const uint32_t key = psi_key(av[u], sv[u], lambda);
+        const uint32_t key = one_grp ? kreg[u] : psi_key(av[u], sv[u], lambda);
         kmin = min(kmin, key);
         kmax = max(kmax, key);
         if (in_lds) skey[run + __popcll(bal & lt)] = key;
@@ -167,7 +183,7 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
   }
   if (lane == 0) { wmin[wave] = kmin; wmax[wave] = kmax; }
-  __syncthreads();
+  __syncthreads();  // keys and their range
 #pragma unroll
   for (int w = 0; w < kSelWaves; ++w) { kmin = min(kmin, wmin[w]); kmax = max(kmax, wmax[w]); }
   const int width = (kmin ^ kmax) ? 32 - __clz(kmin ^ kmax) : 0;  // low bits in which keys differ
@@ -237,13 +253,14 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       const int j = wrow0 + (i0 + u) * 64 + lane;
       const bool mb = i0 + u < R && member_at(i0 + u, j);
       bal[u] = __ballot(mb);
-      kk[u] = mb ? (in_lds ? skey[run + __popcll(bal[u] & lt)] : kg[j]) : 0u;
+      kk[u] = mb ? (one_grp ? kreg[u] : (in_lds ? skey[run + __popcll(bal[u] & lt)] : kg[j])) : 0u;
       run += __popcll(bal[u]);
     }
     return run;
   };
-  int weq = 0;
-  if (eq_ranks) {
+  int eq_base = 0;
+  if (eq_ranks) {  // uniform: every wave takes this branch or none
+    int weq = 0;
     for (int i0 = 0, run = rank_base; i0 < R; i0 += kGrp) {
       uint32_t kk[kGrp];
       unsigned long long bal[kGrp];
@@ -251,9 +268,9 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
 #pragma unroll
       for (int u = 0; u < kGrp; ++u) weq += __popcll(__ballot(((bal[u] >> lane) & 1ull) && kk[u] == thr));
     }
+    int eq_tot;
+    eq_base = wave_scan(weq, wt_eq, &eq_tot);
   }
-  int eq_tot;
-  const int eq_base = __shfl(block_scan(lane == 0 ? weq : 0, wave_tot, &eq_tot), 0, 64);
   // selection bits of this lane's rows (bit i; past 64 steps they are
   // recomputed in the writing pass)
   unsigned long long sbits = 0;
@@ -283,7 +300,7 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     }
   }
   int sel_tot;
-  const int out_base = __shfl(block_scan(lane == 0 ? wsel : 0, wave_tot, &sel_tot), 0, 64) + out0;
+  const int out_base = wave_scan(wsel, wt_sel, &sel_tot) + out0;
   if (wsel == 0) return;
   for (int i0 = 0, run = rank_base, eqr = eq_base, o = out_base; i0 < R; i0 += kGrp) {
     unsigned long long sb[kGrp];
@@ -318,15 +335,28 @@ __global__ __launch_bounds__(256) void gather_compact(const LayerDesc* __restric
   T* ko = reinterpret_cast<T*>(Ld.k_out) + (int64_t)g * Ld.out_hs;
   T* vo = reinterpret_cast<T*>(Ld.v_out) + (int64_t)g * Ld.out_hs;
   const int sub = threadIdx.x % CPR;
-  for (int r = threadIdx.x / CPR; r < ROWS; r += RPP) {
-    const int i = i0 + r;
-    if (i >= M) break;
-    const int src = ig[i];
-    if ((unsigned)src >= (unsigned)Ld.n) continue;  // never read outside the working set
-    const uint4 kx = *reinterpret_cast<const uint4*>(k + (int64_t)src * Ld.kv_rs + sub * (16 / sizeof(T)));
-    const uint4 vx = *reinterpret_cast<const uint4*>(v + (int64_t)src * Ld.kv_rs + sub * (16 / sizeof(T)));
-    *reinterpret_cast<uint4*>(ko + (int64_t)i * Ld.out_rs + sub * (16 / sizeof(T))) = kx;
-    *reinterpret_cast<uint4*>(vo + (int64_t)i * Ld.out_rs + sub * (16 / sizeof(T))) = vx;
+  constexpr int NP = ROWS / RPP;  // rows per lane, all loaded before the first store
+  int src[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int i = i0 + threadIdx.x / CPR + p * RPP;
+    src[p] = i < M ? ig[i] : -1;
+  }
+  uint4 kx[NP], vx[NP];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    if ((unsigned)src[p] < (unsigned)Ld.n) {  // never read outside the working set
+      kx[p] = gload16(k + (int64_t)src[p] * Ld.kv_rs + sub * (16 / sizeof(T)));
+      vx[p] = gload16(v + (int64_t)src[p] * Ld.kv_rs + sub * (16 / sizeof(T)));
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int i = i0 + threadIdx.x / CPR + p * RPP;
+    if ((unsigned)src[p] < (unsigned)Ld.n) {
+      *reinterpret_cast<uint4*>(ko + (int64_t)i * Ld.out_rs + sub * (16 / sizeof(T))) = kx[p];
+      *reinterpret_cast<uint4*>(vo + (int64_t)i * Ld.out_rs + sub * (16 / sizeof(T))) = vx[p];
+    }
   }
 }
 
