@@ -102,12 +102,11 @@ __device__ inline void online_update(const floatx16& acc, float sl2, float& m, f
 // exponents of the next group, so no instruction waits on one issued just
 // before it.
 //
-// Exponents are taken against the running reference m of the lane's query
-// (not the block maximum): every exp2 stays finite while a score exceeds m
-// by less than 2^7 in log2 units, and sums up to ~2^100 lose nothing in fp32.
-// A block whose sum reaches 2^60 (or overflows; always true for the first
-// block, where m = -1e30) is redone against its true maximum, which becomes
-// the new reference.  So the common path needs no maximum at all.
+// Exponents are taken against the fixed reference m of the lane's query
+// (not the block maximum), set by the caller from the segment's first keys:
+// every exp2 stays finite while a score exceeds m by less than 2^7 in log2
+// units, and sums up to ~2^100 lose nothing in fp32.  So the common path
+// needs no maximum at all; the caller checks the sums at the segment's end.
 //
 // `f` holds the row block's LDS fragments, already requested.  With PF the
 // phase also requests, spread over its groups, the fragments of row block
@@ -159,27 +158,8 @@ __device__ inline void lse_phase(floatx16 (&out)[2], typename M::frag (&f)[NKS],
   }
 #pragma unroll
   for (int i = 0; i < PER; ++i) s[1][i & 1] += e[(NG - 1) & 1][i];
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
-    const float tot = s[cb][0] + s[cb][1];
-    if (tot < 0x1p60f) {
-      lsum[cb] += tot;
-    } else {
-      float mx = in[cb][0];
-#pragma unroll
-      for (int r = 1; r < 15; r += 2) mx = max3f(mx, in[cb][r], in[cb][r + 1]);
-      mx = fmaxf(mx, in[cb][15]);
-      const float mnew = fmaxf(m[cb], mx * sl2);
-      float t0 = 0.0f, t1 = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        t0 += __builtin_amdgcn_exp2f(__builtin_fmaf(in[cb][r], sl2, -mnew));
-        t1 += __builtin_amdgcn_exp2f(__builtin_fmaf(in[cb][r + 1], sl2, -mnew));
-      }
-      lsum[cb] = lsum[cb] * __builtin_amdgcn_exp2f(m[cb] - mnew) + (t0 + t1);
-      m[cb] = mnew;
-    }
-  }
+  lsum[0] += s[0][0] + s[0][1];
+  lsum[1] += s[1][0] + s[1][1];
 }
 
 // Pass 1, one segment: for the 256 queries [q0, q0+256) of head h of layer
@@ -253,7 +233,18 @@ __device__ inline void lse_segment(const LayerDesc& Ld, const Dims& dm, int h, i
   __syncthreads();            // both first tiles landed in LDS for every wave
   if (active && kr0 < kend_wave) {
     mma_rows<M, Tl>(acc0, kt0, arow, half, qf);
-    if constexpr (kHandSched) load_frags<M, Tl>(fA, kt0, 32 + arow, half);
+    if constexpr (kHandSched) {
+      load_frags<M, Tl>(fA, kt0, 32 + arow, half);
+      // Reference of each query: the largest score among the segment's
+      // first 32 keys.  A lane's visible keys form a prefix of the
+      // segment's keys, so a lane with any visible key has one there.
+      if (need_mask(kr0)) apply_mask(acc0, kr0);
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+        const float mx = fmaxf(max16(acc0[cb]), wave_xor32(max16(acc0[cb])));
+        m[cb] = fmaxf(-1e30f, mx * sl2);
+      }
+    }
   }
   // One tile t in `cur`; tile t+1 is in (or on its way to) `nxt`.
   auto step = [&](int t, T* cur, const T* nxt) {
@@ -297,6 +288,31 @@ __device__ inline void lse_segment(const LayerDesc& Ld, const Dims& dm, int h, i
   for (int t = kr0; t < kr1; t += 2 * kTile) {
     step(t, kt0, kt1);
     if (t + kTile < kr1) step(t + kTile, kt1, kt0);
+  }
+  if constexpr (kHandSched) {
+    // Later scores exceed the reference by far less than the sums' headroom
+    // for any realistic input; a segment whose sums still leave it is redone
+    // tile by tile with the reference moved to every block's maximum.
+    const bool bad = active && !(lsum[0] < 0x1p100f && lsum[1] < 0x1p100f);
+    if (__syncthreads_or(bad)) {  // also: every wave is done with the stages
+      m[0] = m[1] = -1e30f;
+      lsum[0] = lsum[1] = 0.0f;
+      for (int t = kr0; t < kr1; t += kTile) {
+        Tl::copy(kt0, k + (int64_t)t * kv_rs, kv_rs, min(kTile, N - t), plan);
+        dma_wait();
+        __syncthreads();
+        if (active && t < kend_wave) {
+#pragma unroll
+          for (int rb = 0; rb < 2; ++rb) {
+            mma_rows<M, Tl>(acc0, kt0, rb * 32 + arow, half, qf);
+            if (need_mask(t + rb * 32)) apply_mask(acc0, t + rb * 32);
+            online_update(acc0[0], sl2, m[0], lsum[0]);
+            online_update(acc0[1], sl2, m[1], lsum[1]);
+          }
+        }
+        __syncthreads();
+      }
+    }
   }
   if (!active) return;
 #pragma unroll
