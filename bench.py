@@ -30,12 +30,12 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-layer-6144": {
-        "sources_sha256": "9973ebec9c23f8cab838e6ae7e471d0d557837ef571d7c65e478ff2c34c540d5",
-        "lse_pass": 31220284, "colsum_pass": 32932048, "gram_pass": 15429212, "psi_topk": 793362, "gather_compact": 16876510,
+        "sources_sha256": "995cc6e419478000c3a04afd823178465329129506e0ed3429a6703fa1fc4832",
+        "lse_pass": 31184159, "colsum_pass": 32956542, "gram_pass": 15431258, "psi_topk": 826743, "gather_compact": 16886544,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "9973ebec9c23f8cab838e6ae7e471d0d557837ef571d7c65e478ff2c34c540d5",
-        "lse_pass": 616071344, "colsum_pass": 613146115, "gram_pass": 2071009659, "psi_topk": 14569845, "gather_compact": 472113060,
+        "sources_sha256": "995cc6e419478000c3a04afd823178465329129506e0ed3429a6703fa1fc4832",
+        "lse_pass": 611444709, "colsum_pass": 616834306, "gram_pass": 812263019, "psi_topk": 14603045, "gather_compact": 471779962,
     },
 }
 
