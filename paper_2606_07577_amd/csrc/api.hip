@@ -50,7 +50,7 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 }  // namespace omnimem
 
 static const char* kKernelNames[K_COUNT] = {
-    "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "gather_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact"};
+    "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact"};
 
 struct omnimem_ctx {
   omnimem_config cfg;

@@ -84,11 +84,6 @@ __global__ __launch_bounds__(1024) void modality_lists(const LayerDesc* __restri
   if (threadIdx.x == 0) { counts[2 * l] = kv; counts[2 * l + 1] = N - kv; }
 }
 
-// --- gathered rows and inverse norms ------------------------------------------
-// For each (layer, KV head): perm[k] = u[row_k] with row_k the k-th row of
-// the segment order [visual rows ascending | audio rows ascending], its
-// inverse norm 1 / ||u|| in fp64 (0 for a zero row), and best[k] reset.
-// One 16-byte piece per lane.
 // 16 MFMAs: the 32-row block `row` of an LDS stage against two 32-column
 // blocks of register operands; each LDS fragment feeds two MFMAs.
 template <typename M, typename Tl, int NKS, typename T>
@@ -108,47 +103,138 @@ struct GatherShape {
   static constexpr int RPB = 256 / LPR;                 // rows per workgroup
 };
 
+// --- modality lists, gathered rows and inverse norms in one pass ---------------
+// For each (layer, KV head): perm[k] = u[row_k] with row_k the k-th row of
+// the segment order [visual rows ascending | audio rows ascending], its
+// inverse norm 1 / ||u|| in fp64 (0 for a zero row), and best[k] reset;
+// with the lists that modality_lists makes.  Indexed by working-set row:
+// each workgroup takes kListRows consecutive rows from j0 of one (layer, KV
+// head), counts the visual rows of the whole layer and those
+// before j0 from the modality mask itself, places its rows by a ballot
+// prefix, and copies them to their segment positions with their inverse
+// norms.  The workgroups of KV head 0 also write the lists (pos, rank,
+// counts) for the later kernels.
+constexpr int kListRows = 128;
+
 template <typename T, int D>
-__global__ __launch_bounds__(256) void gather_norms(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
-                                                    const int* __restrict__ pos, const int* __restrict__ counts,
-                                                    T* __restrict__ perm, float* __restrict__ inv,
-                                                    int* __restrict__ best) {
+__global__ __launch_bounds__(256) void lists_norms(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
+                                                   int* __restrict__ pos, int* __restrict__ rank,
+                                                   int* __restrict__ counts, T* __restrict__ perm,
+                                                   float* __restrict__ inv, int* __restrict__ best) {
   const int l = blockIdx.z, g = blockIdx.y;
   const LayerDesc Ld = layers[l];
   const int N = Ld.n;
+  const int j0 = blockIdx.x * kListRows;
+  if (j0 >= N) return;  // the whole workgroup leaves together
+  const uint8_t* mod = Ld.mod;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ int wv_before[4], wv_total[4];
+  __shared__ int dst[kListRows];
+  static_assert(kListRows % 64 == 0 && kListRows % 4 == 0, "whole waves of rows, word-aligned starts");
+  // The rows' pieces and the rows' own mask bytes do not depend on the
+  // counts: all are requested first, so that their latency overlaps the scan.
   constexpr int LPR = GatherShape<T, D>::LPR;
-  constexpr int EPL = D / LPR;                         // elements per lane
-  const int k = blockIdx.x * GatherShape<T, D>::RPB + threadIdx.x / LPR;
-  const int sub = threadIdx.x % LPR;
-  if (k >= N) return;  // whole row groups leave together
-  const int kv = counts[2 * l];
-  const int row = k < kv ? pos[(int64_t)(2 * l) * dm.max_tokens + k] : pos[(int64_t)(2 * l + 1) * dm.max_tokens + k - kv];
-  const T* u = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
-  const T* src = u + (int64_t)row * Ld.kv_rs + sub * EPL;
-  const int64_t o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + k;
-  T* dst = perm + o * D + sub * EPL;
-  double acc = 0.0;
+  constexpr int RPP = 256 / LPR;   // rows per pass
+  constexpr int EPL = D / LPR;     // elements per lane
   static_assert(EPL * sizeof(T) == 16, "one 16-byte piece per lane");
-  {
-    const uint4 v = gload16(src);
-    *reinterpret_cast<uint4*>(dst) = v;
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  const int sub = threadIdx.x % LPR;
+  const T* u = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
+  constexpr int NP = kListRows / RPP;
+  constexpr int NQ = kListRows / 64;
+  uint4 v[NP];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if constexpr (sizeof(T) == 2) {
-        const double a = __uint_as_float(w[e] << 16), b = __uint_as_float(w[e] & 0xFFFF0000u);
-        acc += a * a + b * b;
-      } else {
-        const double a = __uint_as_float(w[e]);
-        acc += a * a;
-      }
+  for (int p = 0; p < NP; ++p) {
+    const int r = p * RPP + (int)threadIdx.x / LPR;
+    if (j0 + r < N) v[p] = gload16(u + (int64_t)(j0 + r) * Ld.kv_rs + sub * EPL);
+  }
+  int own[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int j = j0 + q * 64 + lane;
+    own[q] = wave == 0 && j < N ? (int)gload<uint8_t>(mod + j) : 1;
+  }
+  // Visual rows before j0 and in the whole layer.  A 4-byte aligned mask is
+  // read a word at a time (zero bytes counted with the haszero trick, j0
+  // being a multiple of 4), eight words per thread in flight; the bytes of
+  // a last partial word, or of an unaligned mask, one at a time.
+  int before = 0, total = 0;
+  const bool aligned = (reinterpret_cast<uintptr_t>(mod) & 3u) == 0;
+  const int nw = aligned ? N / 4 : 0;
+  const uint32_t* mw = reinterpret_cast<const uint32_t*>(mod);
+  for (int w0 = (int)threadIdx.x * 8; w0 < nw; w0 += 256 * 8) {
+    uint32_t w[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) w[u] = w0 + u < nw ? gload<uint32_t>(mw + w0 + u) : 0x01010101u;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t z = ~(((w[u] & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | w[u] | 0x7F7F7F7Fu);  // 0x80 per zero byte
+      const int c = __popc(z);
+      total += c;
+      before += 4 * (w0 + u) < j0 ? c : 0;
     }
   }
+  for (int x = 4 * nw + (int)threadIdx.x; x < N; x += 256) {
+    const int vis = gload<uint8_t>(mod + x) == 0;
+    total += vis;
+    before += x < j0 ? vis : 0;
+  }
 #pragma unroll
-  for (int x = LPR / 2; x > 0; x >>= 1) acc += __shfl_xor(acc, x, 64);
-  if (sub == 0) {
-    inv[o] = acc > 0.0 ? (float)(1.0 / sqrt(acc)) : 0.0f;
-    best[o] = kNoPartner;  // the Gram pass merges maxima into this
+  for (int o = 32; o > 0; o >>= 1) {
+    before += __shfl_xor(before, o, 64);
+    total += __shfl_xor(total, o, 64);
+  }
+  if (lane == 0) { wv_before[wave] = before; wv_total[wave] = total; }
+  __syncthreads();
+  const int kv = wv_total[0] + wv_total[1] + wv_total[2] + wv_total[3];
+  if (wave == 0) {  // the 64-row steps of the workgroup's rows, in order
+    int vb = wv_before[0] + wv_before[1] + wv_before[2] + wv_before[3];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int j = j0 + q * 64 + lane;
+      const bool in = j < N;
+      const bool vis = in && own[q] == 0;
+      const unsigned long long bal = __ballot(vis);
+      const int rv = vb + __popcll(bal & ((1ull << lane) - 1ull));  // visual rows before j
+      const int r = vis ? rv : j - rv;                              // rank inside the modality
+      if (in) {
+        dst[q * 64 + lane] = vis ? r : kv + r;
+        if (g == 0) {
+          pos[(int64_t)(2 * l + (vis ? 0 : 1)) * dm.max_tokens + r] = j;
+          rank[(int64_t)l * dm.max_tokens + j] = r;
+        }
+      }
+      vb += __popcll(bal);
+    }
+    if (g == 0 && blockIdx.x == 0 && lane == 0) { counts[2 * l] = kv; counts[2 * l + 1] = N - kv; }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int r = p * RPP + (int)threadIdx.x / LPR;
+    const bool in = j0 + r < N;
+    double acc = 0.0;
+    int64_t o = 0;
+    if (in) {
+      o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + dst[r];
+      *reinterpret_cast<uint4*>(perm + o * D + sub * EPL) = v[p];
+      const uint32_t w[4] = {v[p].x, v[p].y, v[p].z, v[p].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if constexpr (sizeof(T) == 2) {
+          const double a = __uint_as_float(w[e] << 16), b = __uint_as_float(w[e] & 0xFFFF0000u);
+          acc += a * a + b * b;
+        } else {
+          const double a = __uint_as_float(w[e]);
+          acc += a * a;
+        }
+      }
+    }
+#pragma unroll
+    for (int x = LPR / 2; x > 0; x >>= 1) acc += __shfl_xor(acc, x, 64);
+    if (in && sub == 0) {
+      inv[o] = acc > 0.0 ? (float)(1.0 / sqrt(acc)) : 0.0f;
+      best[o] = kNoPartner;  // the Gram pass merges maxima into this
+    }
   }
 }
 
@@ -404,11 +490,11 @@ void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, c
     OMNIMEM_LAUNCH(ws, K_ADJ, st, adjacent_cos<T, D><<<gtok, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts, s));
     return;
   }
-  constexpr int RPB = GatherShape<T, D>::RPB;
-  const dim3 gnorm((unsigned)((dm.max_tokens + RPB - 1) / RPB), dm.Hkv, dm.L);
+  const dim3 glist((unsigned)((dm.max_tokens + kListRows - 1) / kListRows), dm.Hkv, dm.L);
   T* perm = reinterpret_cast<T*>(ws.perm);
   OMNIMEM_LAUNCH(ws, K_NORMS, st,
-                 gather_norms<T, D><<<gnorm, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.counts, perm, ws.inv_norm, ws.best));
+                 lists_norms<T, D><<<glist, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts, perm,
+                                                          ws.inv_norm, ws.best));
   if (dm.L * dm.Hkv >= 2 * kXcds && ws.gram_grid % kXcds == 0)
     OMNIMEM_LAUNCH(ws, K_GRAM, st,
                    gram_pass<T, D, true><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.counts, perm, ws.inv_norm, ws.best));
@@ -427,8 +513,10 @@ hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& 
 
 hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
                              const Workspace& ws, float* s, hipStream_t st) {
-  hipError_t e = launch_lists(dm, desc, ws, st);
-  if (e != hipSuccess) return e;
+  if (sim == 1) {  // the all-pairs mode computes the lists inside lists_norms
+    hipError_t e = launch_lists(dm, desc, ws, st);
+    if (e != hipSuccess) return e;
+  }
   if (dtype == 0) {
     if (dm.d == 128) launch_typed<uint16_t, 128>(dm, sim, on_keys, desc, ws, s, st);
     else launch_typed<uint16_t, 64>(dm, sim, on_keys, desc, ws, s, st);
