@@ -110,6 +110,23 @@ def test_lse_and_importance(name):
         np.testing.assert_allclose(c.a[l].sum(axis=1, dtype=np.float64), group * lay["q"].shape[1], rtol=1e-4)
 
 
+@pytest.mark.parametrize("h_q,h_kv,causal", [(3, 3, 1), (6, 2, 1), (6, 2, 0)])
+def test_importance_head_groups(h_q, h_kv, causal):
+    # The column-sum pass sums over the G query heads of a KV head inside
+    # one work row, the query head changing between streamed tiles (and
+    # chunk boundaries falling inside a head's tiles): G = 1 and G = 3.
+    layers = ragged_layers(seed=109, h_q=h_q, h_kv=h_kv, caches=((400, 130),), frames=(3, 90, 30))
+    step = DeviceStep(layers, 300, causal=causal)
+    step.score(lse_out=True)
+    _sync()
+    lay = P.as_f64(layers[0])
+    lse = om.attention_lse(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], bool(causal))
+    P.assert_close_a(step.host("lse", 0), lse, "lse")
+    a = om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], bool(causal), lse=lse)
+    P.assert_close_a(step.host("a", 0), a, "a")
+    step.close()
+
+
 @pytest.mark.parametrize("name", FULL_CASES)
 def test_redundancy(name):
     c = get_case(name)
