@@ -4,8 +4,9 @@
 //                  a^lambda (1 - s) as an order-preserving 32-bit key per
 //                  member row (rows dealt to waves in contiguous spans, read
 //                  coalesced), radix select of the M-th largest key (12-bit
-//                  digits below the bits all keys share, LDS histogram),
-//                  then an ordered emission that keeps every key above the
+//                  digits below the bits all keys share, LDS histogram;
+//                  the last few candidates ranked directly against each
+//                  other), then an ordered emission that keeps every key above the
 //                  threshold and the first ones equal to it (ties to the
 //                  lower row), in ascending row order, placed by ballots and
 //                  block-wide scans.
@@ -22,6 +23,7 @@ constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kLdsKeys = 32768;   // member keys of a segment held in LDS (128 KB)
 constexpr int kDigit = 12;        // radix digit bits
 constexpr int kBins = 1 << kDigit;
+constexpr int kListMax = 256;     // threshold-bin keys ranked directly instead of by more passes
 
 // a^lambda as exp2(lambda * log2 a) on the hardware transcendentals (about
 // 1e-7 relative error, far inside the ordering tolerance of the selection).
@@ -76,7 +78,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   __shared__ uint32_t skey[kLdsKeys];
   __shared__ int hist[kBins];
   __shared__ int wave_tot[kSelWaves];
-  __shared__ int s_bin, s_need, s_cnt;
+  __shared__ int s_bin, s_need, s_cnt, s_lcnt;
+  __shared__ uint32_t s_thr;
   __shared__ int wt_mem[kSelWaves], wt_eq[kSelWaves], wt_sel[kSelWaves];
   __shared__ uint32_t wmin[kSelWaves], wmax[kSelWaves];
 
@@ -93,6 +96,9 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   const int R = (N + kSelThreads - 1) / kSelThreads;   // rows per lane
   const int wrow0 = wave * 64 * R;
   auto member = [&](int j) { return j < N && (mod[j] ? 1 : 0) == mu; };
+  // the segment's budget (and the visual one, where the audio rows go),
+  // requested first so that their latency overlaps the reads below
+  const int bud_mu = budgets[2 * l + mu], bud_v = budgets[2 * l];
 
   // Membership of this lane's rows (bit i: row wrow0 + 64 i + lane), read in
   // groups of 8 steps so their loads are in flight together; with more than
@@ -167,9 +173,9 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       run += __popcll(bal);
     }
   }
-  const int M = min(max(budgets[2 * l + mu], 0), K);
+  const int M = min(max(bud_mu, 0), K);
   const int Kv = mu ? N - K : K;
-  const int Mv = mu ? min(max(budgets[2 * l], 0), Kv) : M;
+  const int Mv = mu ? min(max(bud_v, 0), Kv) : M;
   if (g == 0 && threadIdx.x == 0) eff[2 * l + mu] = M;
   const int out0 = mu ? Mv : 0;
 
@@ -199,6 +205,7 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       const int shift = max(0, top - kDigit);
       const uint32_t dmask = (1u << (top - shift)) - 1u;
       for (int b = threadIdx.x; b < kBins; b += kSelThreads) hist[b] = 0;
+      if (threadIdx.x == 0) s_lcnt = 0;
       __syncthreads();
       if (in_lds) {
         for (int r = threadIdx.x; r < K; r += kSelThreads) {
@@ -236,6 +243,40 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       need = s_need;
       n_eq = s_cnt;
       __syncthreads();
+      if (shift > 0 && in_lds && n_eq <= kListMax) {
+        // Few keys left in the threshold's bin: collect them (the histogram's
+        // memory is free now) and rank each against the others, instead of
+        // further passes over all keys.  The key with need - 1 candidates
+        // strictly above it, counting its equals, is the threshold.
+        int* cand = hist;
+        for (int r0 = 0; r0 < K; r0 += kSelThreads) {
+          const int r = r0 + (int)threadIdx.x;
+          const uint32_t key = r < K ? skey[r] : 0u;
+          const bool m = r < K && (key & mask) == prefix;
+          const unsigned long long b = __ballot(m);
+          int base = 0;
+          if (lane == 0 && b) base = atomicAdd(&s_lcnt, __popcll(b));
+          base = __shfl(base, 0, 64);
+          if (m) cand[base + __popcll(b & lt)] = (int)key;
+        }
+        __syncthreads();
+        if ((int)threadIdx.x < n_eq) {
+          const uint32_t c = (uint32_t)cand[threadIdx.x];
+          int gt = 0, eq = 0;
+          for (int u = 0; u < n_eq; ++u) {
+            const uint32_t x = (uint32_t)cand[u];
+            gt += x > c ? 1 : 0;
+            eq += x == c ? 1 : 0;
+          }
+          // every candidate equal to the threshold writes the same values
+          if (gt < need && need <= gt + eq) { s_thr = c; s_need = need - gt; s_cnt = eq; }
+        }
+        __syncthreads();
+        prefix = s_thr;
+        need = s_need;
+        n_eq = s_cnt;
+        break;
+      }
     }
     thr = prefix;
     take_eq = need;
