@@ -17,6 +17,9 @@ in the paper's order and notation:
   * Eqs. (11), (12)  audio/visual proportions w_v, w_a                -> modality_weights
   * Eq. (14) + the [B_min, B_max] constraint of Sec. 3.2              -> layer_budgets
   * "split according to w_v and w_a" (Sec. 3.2)                       -> split_budget
+  * budgets "determined offline ... on a small calibration set"
+    (end of Sec. 3.2)                                                 -> calibration_budgets,
+                                                                         fixed_split
   * Eqs. (4), (5) Select: top-M by psi per modality (Sec. 3.1)         -> select
   * Eq. (3) / Eq. (2): the retained pairs form the next caches         -> compact
 
@@ -42,6 +45,10 @@ listed with its justification in the design notes):
       gives none.  PARITY UNPINNED for those two constants.
   R17 integer layer budgets by largest remainder, ties to the lower layer.
   R18 M_v = round-half-up(w_v B_l) clamped so that both modalities fit.
+  R21 offline budgets: C^(l) of Eq. (13) averaged over the calibration
+      steps, then Eq. (14), the clamp and the integer rounding (R15-R17) on
+      the means, with no cap by a layer's token count; a step under these
+      budgets keeps min(B^(l), N_l) rows of layer l, split by its own w_v.
 """
 from __future__ import annotations
 
@@ -348,6 +355,39 @@ def split_budget(layer_budget, w_v, k_visual, k_audio):
 
 
 # ---------------------------------------------------------------------------
+# Offline budgets (end of Sec. 3.2): B^(l) fixed from a calibration set
+# ---------------------------------------------------------------------------
+
+def calibration_budgets(c_layer_steps, total_budget, temperature=DEFAULT_T,
+                        bmin_frac=DEFAULT_BMIN_FRAC, bmax_frac=DEFAULT_BMAX_FRAC):
+    """Per-layer budgets fixed in advance (reading R21).
+
+    c_layer_steps: [steps, L] values of C^(l) (Eq. 13), one row per
+    calibration step.  Their mean over the steps goes through Eq. (14) with
+    the clamp to [B_min, B_max] (R15, R16) and the integer rounding (R17).
+    Token counts of any one step do not cap these budgets, so the bounds are
+    taken with counts large enough never to bind.
+    """
+    c = np.asarray(c_layer_steps, dtype=np.float64)
+    if c.ndim != 2 or c.shape[0] == 0:
+        raise ValueError("calibration needs at least one step of per-layer values")
+    c_mean = c.mean(axis=0)
+    never_binding = (math.floor(float(bmax_frac) * float(total_budget))
+                     + math.ceil(float(bmin_frac) * float(total_budget)) + 1)
+    n_free = [never_binding] * c.shape[1]
+    shares = layer_shares(c_mean, n_free, total_budget, temperature, bmin_frac, bmax_frac)
+    return integer_budgets(shares, n_free, total_budget, bmin_frac, bmax_frac)
+
+
+def fixed_split(layer_budget, w_v, k_visual, k_audio):
+    """One layer of a step under offline budgets (reading R21): it keeps
+    min(B^(l), N_l) rows (a negative budget keeps none), split between the
+    modalities by this step's w_v as in the online mode (R18)."""
+    b = min(max(int(layer_budget), 0), int(k_visual) + int(k_audio))
+    return split_budget(b, w_v, k_visual, k_audio)
+
+
+# ---------------------------------------------------------------------------
 # Eqs. (4), (5): Select, and the compaction into the next caches
 # ---------------------------------------------------------------------------
 
@@ -382,9 +422,12 @@ def compact(x, idx):
 def compression_step(layers, total_budget, lam=DEFAULT_LAMBDA, r=DEFAULT_R,
                      temperature=DEFAULT_T, bmin_frac=DEFAULT_BMIN_FRAC,
                      bmax_frac=DEFAULT_BMAX_FRAC, mode="max", causal=True,
-                     use_keys=False):
+                     use_keys=False, layer_budgets=None):
     """Run the whole step.  `layers` is a list of dicts with keys
     q [H_q,C,d], k and v [H_kv,N,d], modality [N], n_cache, sm_scale.
+    With `layer_budgets` (offline budgets B^(l), reading R21) the layers
+    keep those, capped at their token counts, instead of the budgets of
+    Eq. (14) from this step.
 
     Returns a dict of per-layer lists: a, s, stats, budgets (M_v, M_a), idx,
     k_out, v_out, plus the real-valued shares x_l and integer B_l.
@@ -401,9 +444,13 @@ def compression_step(layers, total_budget, lam=DEFAULT_LAMBDA, r=DEFAULT_R,
         out["stats"].append(avba_statistics(a, s, layer["modality"]))
     c_layers = [st["C_l"] for st in out["stats"]]
     n_tokens = [len(layer["modality"]) for layer in layers]
-    shares = layer_shares(c_layers, n_tokens, total_budget, temperature,
-                          bmin_frac, bmax_frac)
-    budgets = integer_budgets(shares, n_tokens, total_budget, bmin_frac, bmax_frac)
+    if layer_budgets is None:
+        shares = layer_shares(c_layers, n_tokens, total_budget, temperature,
+                              bmin_frac, bmax_frac)
+        budgets = integer_budgets(shares, n_tokens, total_budget, bmin_frac, bmax_frac)
+    else:
+        budgets = np.minimum(np.maximum(np.asarray(layer_budgets, dtype=np.int64), 0), n_tokens)
+        shares = budgets.astype(np.float64)
     out["shares"] = shares
     out["layer_budgets"] = budgets
     for layer, st, b_l, a, s in zip(layers, out["stats"], budgets, out["a"], out["s"]):
