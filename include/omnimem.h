@@ -163,6 +163,44 @@ omnimem_status omnimem_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, c
                                 const float* s, int64_t total_budget, int32_t* budgets,
                                 float* stats, hipStream_t stream);
 
+/* Offline budgets (end of Sec. 3.2: the layer budgets are determined offline
+ * from a small calibration set).  The per-layer budgets B^(l) of Eq. (14)
+ * are fixed in advance; every step then only splits them between the
+ * modalities (Eqs. 11-12).
+ *
+ * omnimem_calibrate: adds each layer's C^(l) (Eq. 13) of one step, from a
+ * and s laid out as for omnimem_allocate, to the context's calibration sums
+ * (the first step after create or a reset starts them).  stats, if not
+ * null, receives the step's [L][10] statistics as omnimem_allocate writes
+ * them.  The sums live in the context's device workspace: calls on one
+ * context must be ordered on one stream. */
+omnimem_status omnimem_calibrate(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a,
+                                 const float* s, float* stats, hipStream_t stream);
+
+/* Forget the calibration steps added so far (host-side: no device work). */
+omnimem_status omnimem_calibration_reset(omnimem_ctx* ctx);
+
+/* Layer budgets of the calibration: with C^(l) the mean over the steps added
+ * since the last reset, x_l and the integer B_l as in omnimem_allocate, but
+ * with lo = ceil(b_min_frac*B_tot/L) and hi = floor(b_max_frac*B_tot/L) for
+ * every layer (no token count caps them).  Sum B_l = total_budget unless
+ * L*hi < total_budget, when every layer gets hi.
+ *   layer_budgets  [L] int32 device output.
+ * Errors: INVALID_ARG when no step was added or total_budget is outside
+ * [0, 2^31); INFEASIBLE when L*lo > total_budget (checked on the host). */
+omnimem_status omnimem_calibration_budgets(omnimem_ctx* ctx, int64_t total_budget,
+                                           int32_t* layer_budgets, hipStream_t stream);
+
+/* One step under offline budgets: B_l = min(max(layer_budgets[l], 0), N_l),
+ * then M_v, M_a as in omnimem_allocate from this step's w_v (Eq. 11).
+ *   a, s           [L][H_kv][max_tokens] fp32 inputs.
+ *   layer_budgets  [L] int32 device input (omnimem_calibration_budgets
+ *                  writes one).
+ *   budgets        [L][2] int32 output (M_v, M_a); stats as above. */
+omnimem_status omnimem_allocate_fixed(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a,
+                                      const float* s, const int32_t* layer_budgets, int32_t* budgets,
+                                      float* stats, hipStream_t stream);
+
 /* Eqs. (4)-(5), (8): per (layer, KV head, modality) keep the M rows with the
  * largest psi = a^lambda (1 - s) (0^lambda = 0; ties to the lower row), in
  * ascending row order, visual block first; then k_out[g][i] = k[g][idx[g][i]]

@@ -8,6 +8,12 @@
 //                 [B_min, B_max] with the sum kept (water-filling on the
 //                 scale kappa), largest-remainder integer budgets and the
 //                 per-modality split.  All in fp64.
+//                 Offline budgets (end of Sec. 3.2: fixed in advance from a
+//                 calibration set) use the same kernel in three more modes:
+//                 adding a step's C^(l) to the calibration sums, turning
+//                 their means into layer budgets by the same Eq. (14) path
+//                 (no token count caps them), and a step under given layer
+//                 budgets, which only caps them at N_l and splits them.
 #include "common.h"
 
 namespace omnimem {
@@ -73,11 +79,23 @@ __device__ inline double norm_entropy(double sum, double xlogx, double count) {
 constexpr int kMaxLayers = 1024;
 constexpr int kMaxSums = 2048;   // L * H_kv * 8 partial sums kept in LDS
 
+enum AllocMode : int {
+  kOnline = 0,       // Eq. (14) from this step's statistics, then the split
+  kCalibAdd = 1,     // calib[l] (+)= this step's C^(l); nothing else written
+  kFixed = 2,        // layer budgets given: capped at N_l, then the split
+  kCalibFinish = 3,  // layer budgets from calib[l] / steps (no statistics read)
+};
+
+// calib: [L] calibration sums; calib_first: a kCalibAdd step that starts
+// them (assigns instead of adding); steps: their count (kCalibFinish).
+// layer_budgets: read in kFixed, written in kCalibFinish.
 __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict__ layers, Dims dm,
                                                      const double* __restrict__ part, int64_t total,
                                                      float ratio_r, float temperature, float bmin_frac,
-                                                     float bmax_frac, int32_t* __restrict__ budgets,
-                                                     float* __restrict__ stats) {
+                                                     float bmax_frac, int mode, double* __restrict__ calib,
+                                                     int calib_first, double steps,
+                                                     int32_t* __restrict__ layer_budgets,
+                                                     int32_t* __restrict__ budgets, float* __restrict__ stats) {
   __shared__ double c_l[kMaxLayers], w_v[kMaxLayers], p[kMaxLayers], x[kMaxLayers];
   __shared__ int n_l[kMaxLayers], k_v[kMaxLayers], lo[kMaxLayers], hi[kMaxLayers], b_l[kMaxLayers];
   __shared__ double s_kappa;
@@ -89,6 +107,16 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
   const double T = (double)temperature;
   const double r = (double)ratio_r;
 
+  if (mode == kCalibFinish) {
+    // the mean compressibility of each layer; counts that never bind
+    for (int l = threadIdx.x; l < L; l += blockDim.x) {
+      c_l[l] = calib[l] / steps;
+      n_l[l] = 0x7fffffff;
+      k_v[l] = 0;
+      w_v[l] = 0.0;
+    }
+    __syncthreads();
+  } else {
   // --- chunk partials summed per (layer, head, quantity), in chunk order;
   // sixteen chunks' loads in flight at a time ---
   const int nchunk = part_chunks(dm);
@@ -149,6 +177,16 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
     }
   }
   __syncthreads();
+  }  // statistics of this step
+
+  if (mode == kCalibAdd) {
+    for (int l = threadIdx.x; l < L; l += blockDim.x) calib[l] = calib_first ? c_l[l] : calib[l] + c_l[l];
+    return;
+  }
+  if (mode == kFixed) {
+    for (int l = threadIdx.x; l < L; l += blockDim.x) b_l[l] = min(max(layer_budgets[l], 0), n_l[l]);
+    __syncthreads();
+  } else {
 
   // --- Eq. (14): softmax over layers of C / T (exps in parallel, the max
   // and the sum in layer order), bounds ---
@@ -235,6 +273,11 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
     }
     __syncthreads();
   }
+  }  // layer budgets of Eq. (14)
+  if (mode == kCalibFinish) {
+    for (int l = threadIdx.x; l < L; l += blockDim.x) layer_budgets[l] = b_l[l];
+    return;
+  }
 
   // --- per-modality split (Eqs. 11-12) ---
   for (int l = threadIdx.x; l < L; l += blockDim.x) {
@@ -258,7 +301,40 @@ hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspac
                  avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
                                                                                             ws.stat_part));
   OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, total, ratio_r,
-                                   temperature, bmin_frac, bmax_frac, budgets, stats));
+                                   temperature, bmin_frac, bmax_frac, kOnline, nullptr, 0, 0.0, nullptr,
+                                   budgets, stats));
+  return hipGetLastError();
+}
+
+hipError_t launch_calibrate(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
+                            const float* s, float ratio_r, bool first, float* stats, hipStream_t st) {
+  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st,
+                 avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
+                                                                                            ws.stat_part));
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, 0, ratio_r, 1.0f,
+                                   0.0f, 0.0f, kCalibAdd, ws.calib, first ? 1 : 0, 0.0, nullptr, nullptr,
+                                   stats));
+  return hipGetLastError();
+}
+
+hipError_t launch_calibration_budgets(const Dims& dm, const Workspace& ws, int64_t total, float temperature,
+                                      float bmin_frac, float bmax_frac, int steps, int32_t* layer_budgets,
+                                      hipStream_t st) {
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(nullptr, dm, nullptr, total, 1.0f,
+                                   temperature, bmin_frac, bmax_frac, kCalibFinish, ws.calib, 0,
+                                   (double)steps, layer_budgets, nullptr, nullptr));
+  return hipGetLastError();
+}
+
+hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
+                                 const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
+                                 float* stats, hipStream_t st) {
+  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st,
+                 avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
+                                                                                            ws.stat_part));
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, 0, ratio_r, 1.0f,
+                                   0.0f, 0.0f, kFixed, nullptr, 0, 0.0, const_cast<int32_t*>(layer_budgets),
+                                   budgets, stats));
   return hipGetLastError();
 }
 

@@ -65,6 +65,7 @@ struct omnimem_ctx {
   std::vector<LayerDesc> last_table;
   PassPlan lse_plan{0, 0}, cs_plan{0, 0};  // score-pass plans of the last table
   int max_workgroups = 512;               // persistent score-pass grid: 2 per compute unit
+  int calib_steps = 0;                    // steps in the calibration sums since the last reset
   std::string err;
   std::vector<void*> allocations;
   Profiler prof;
@@ -299,6 +300,7 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       (e = dalloc(ctx, &ws.best, L * Hkv * T)) != hipSuccess ||
       (e = dalloc(ctx, reinterpret_cast<char**>(&ws.perm), L * Hkv * T * (size_t)c.head_dim * elt)) != hipSuccess ||
       (e = dalloc(ctx, &ws.stat_part, L * Hkv * (size_t)allocate_part_chunks(dm) * 2 * 4)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.calib, L)) != hipSuccess ||
       (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.idx, L * Hkv * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.keys, L * Hkv * T)) != hipSuccess) {
@@ -384,6 +386,62 @@ omnimem_status omnimem_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, c
   return finish(ctx, launch_allocate(ctx->dm, dev, ctx->ws, a, s, total_budget, c.ratio_r, c.temperature,
                                      c.b_min_frac, c.b_max_frac, budgets, stats, stream),
                 stream, "omnimem_allocate launch");
+}
+
+omnimem_status omnimem_calibrate(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,
+                                 float* stats, hipStream_t stream) {
+  omnimem_status st = validate(ctx, layers, 0);
+  if (st != OMNIMEM_OK) return st;
+  if (!a || !s) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a or s");
+  if (ctx->calib_steps == INT32_MAX) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "too many calibration steps");
+  if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
+  const LayerDesc* dev = nullptr;
+  if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
+  st = finish(ctx, launch_calibrate(ctx->dm, dev, ctx->ws, a, s, ctx->cfg.ratio_r, ctx->calib_steps == 0, stats,
+                                    stream),
+              stream, "omnimem_calibrate launch");
+  if (st == OMNIMEM_OK) ++ctx->calib_steps;
+  return st;
+}
+
+omnimem_status omnimem_calibration_reset(omnimem_ctx* ctx) {
+  if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
+  ctx->calib_steps = 0;
+  return OMNIMEM_OK;
+}
+
+omnimem_status omnimem_calibration_budgets(omnimem_ctx* ctx, int64_t total_budget, int32_t* layer_budgets,
+                                           hipStream_t stream) {
+  if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
+  if (!layer_budgets) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null layer_budgets");
+  if (ctx->calib_steps == 0) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "no calibration step was added");
+  const omnimem_config& c = ctx->cfg;
+  if (total_budget < 0 || total_budget > (int64_t)INT32_MAX)
+    return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "total budget %lld out of range", (long long)total_budget);
+  const int64_t lo_base = (int64_t)std::ceil(((double)c.b_min_frac * (double)total_budget) / c.n_layers);
+  if (lo_base * c.n_layers > total_budget)
+    return fail(ctx, OMNIMEM_ERR_INFEASIBLE, "per-layer minimum budgets sum to %lld > total %lld",
+                (long long)(lo_base * c.n_layers), (long long)total_budget);
+  omnimem_status st = set_device(ctx);
+  if (st != OMNIMEM_OK) return st;
+  return finish(ctx, launch_calibration_budgets(ctx->dm, ctx->ws, total_budget, c.temperature, c.b_min_frac,
+                                                c.b_max_frac, ctx->calib_steps, layer_budgets, stream),
+                stream, "omnimem_calibration_budgets launch");
+}
+
+omnimem_status omnimem_allocate_fixed(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,
+                                      const int32_t* layer_budgets, int32_t* budgets, float* stats,
+                                      hipStream_t stream) {
+  omnimem_status st = validate(ctx, layers, 0);
+  if (st != OMNIMEM_OK) return st;
+  if (!a || !s || !layer_budgets || !budgets)
+    return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a, s, layer_budgets or budgets");
+  if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
+  const LayerDesc* dev = nullptr;
+  if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
+  return finish(ctx, launch_allocate_fixed(ctx->dm, dev, ctx->ws, a, s, layer_budgets, ctx->cfg.ratio_r, budgets,
+                                           stats, stream),
+                stream, "omnimem_allocate_fixed launch");
 }
 
 omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,

@@ -233,6 +233,7 @@ struct Workspace {
   void* perm;             // [L][Hkv][max_tokens][d] rows in segment order (visual, then audio)
   int gram_grid;          // persistent Gram workgroups
   double* stat_part;      // [L][Hkv][chunks][2][4]
+  double* calib;          // [L] sums of C^(l) over the calibration steps
   int* eff;               // [L][2] budgets as applied by select
   int* idx;               // [L][Hkv][max_tokens] fallback for the idx output
   uint32_t* keys;         // [L][Hkv][max_tokens]
@@ -252,6 +253,14 @@ hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspac
                            const float* a, const float* s, int64_t total, float ratio_r,
                            float temperature, float bmin_frac, float bmax_frac, int32_t* budgets,
                            float* stats, hipStream_t st);
+hipError_t launch_calibrate(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
+                            const float* s, float ratio_r, bool first, float* stats, hipStream_t st);
+hipError_t launch_calibration_budgets(const Dims& dm, const Workspace& ws, int64_t total, float temperature,
+                                      float bmin_frac, float bmax_frac, int steps, int32_t* layer_budgets,
+                                      hipStream_t st);
+hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
+                                 const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
+                                 float* stats, hipStream_t st);
 hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, const LayerDesc* desc,
                                  const Workspace& ws, const float* a, const float* s,
                                  const int32_t* budgets, int32_t* idx, hipStream_t st);

@@ -336,8 +336,11 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
         const int row = t * kScoreTile + (int)threadIdx.x;
         return row < K ? gload<float>(invs + row) : __builtin_nanf("");
       };
+      // No load is waited for before the tile loop: the first tile's norms
+      // and the register rows' own norms (for the final maxima) are held in
+      // registers meanwhile.
       Tl::copy(jt0, U + (int64_t)t0 * kScoreTile * D, D, tile_rows(t0), plan);
-      if (threadIdx.x < kScoreTile) jinv[0][threadIdx.x] = jinv_of(t0);
+      const float jinv_first = threadIdx.x < kScoreTile ? jinv_of(t0) : 0.0f;
       float jinv_next = 0.0f;
       if (t0 + 1 < t1) {
         Tl::copy(jt1, U + (int64_t)(t0 + 1) * kScoreTile * D, D, tile_rows(t0 + 1), plan);
@@ -345,6 +348,7 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
       }
       // this wave's 64 register rows (two 32-column blocks of the output)
       const int c0 = I * kGramBlock + wave * 64;
+      const float my_inv = gload<float>(invs + min(c0 + half * 32 + (lane & 31), K - 1));
       typename M::frag bf[2][NKS];
 #pragma unroll
       for (int cb = 0; cb < 2; ++cb) {
@@ -356,7 +360,7 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
       for (int t = t0; t < t1; ++t) {
         const int st = (t - t0) & 1;
         const T* cur = st ? jt1 : jt0;
-        if (t > t0 && threadIdx.x < kScoreTile) jinv[st][threadIdx.x] = jinv_next;
+        if (threadIdx.x < kScoreTile) jinv[st][threadIdx.x] = t > t0 ? jinv_next : jinv_first;
         dma_wait();
         __syncthreads();  // tile t and its norms landed; tile t-1's stage is free
         if (t > t0 && t + 1 < t1) {
@@ -397,7 +401,7 @@ __global__ __launch_bounds__(256, 2) void gram_pass(const LayerDesc* __restrict_
         const float m = fmaxf(rmax[cb], __shfl_xor(rmax[cb], 32, 64));
         const int row = c0 + cb * 32 + (lane & 31);
         if (half == cb && row < K && m > -INFINITY)
-          atomicMax(best + seg_off + row, ord_f32(fminf(1.0f, fmaxf(-1.0f, m * gload<float>(invs + row)))));
+          atomicMax(best + seg_off + row, ord_f32(fminf(1.0f, fmaxf(-1.0f, m * my_inv))));
       }
     }
   };

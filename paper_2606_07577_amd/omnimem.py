@@ -23,7 +23,8 @@ SIM_MAX, SIM_ADJ = 0, 1
 EXPORTED = [
     "omnimem_config_default", "omnimem_create", "omnimem_destroy", "omnimem_last_error",
     "omnimem_score", "omnimem_redundancy", "omnimem_allocate", "omnimem_select_compact",
-    "omnimem_profile", "omnimem_profile_report",
+    "omnimem_calibrate", "omnimem_calibration_reset", "omnimem_calibration_budgets",
+    "omnimem_allocate_fixed", "omnimem_profile", "omnimem_profile_report",
 ]
 
 
@@ -86,6 +87,14 @@ def load_library(path=LIB_PATH):
     lib.omnimem_allocate.restype = i32
     lib.omnimem_select_compact.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, vp, vp, vp]
     lib.omnimem_select_compact.restype = i32
+    lib.omnimem_calibrate.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, vp, vp]
+    lib.omnimem_calibrate.restype = i32
+    lib.omnimem_calibration_reset.argtypes = [vp]
+    lib.omnimem_calibration_reset.restype = i32
+    lib.omnimem_calibration_budgets.argtypes = [vp, i64, vp, vp]
+    lib.omnimem_calibration_budgets.restype = i32
+    lib.omnimem_allocate_fixed.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, vp, vp, vp, vp]
+    lib.omnimem_allocate_fixed.restype = i32
     lib.omnimem_profile.argtypes = [vp, ctypes.c_int32]
     lib.omnimem_profile.restype = i32
     lib.omnimem_profile_report.argtypes = [vp, ctypes.POINTER(KernelTime), ctypes.c_int32,
@@ -200,6 +209,23 @@ class Context:
     def omnimem_select_compact(self, layers, a, s, budgets, idx=None, stream=None):
         self._check(self._lib.omnimem_select_compact(self.handle, self._layers(layers), _ptr(a), _ptr(s),
                                                      _ptr(budgets), _ptr(idx), _stream(stream)))
+
+    # Offline budgets (calibration), same names as the C ABI.
+    def omnimem_calibrate(self, layers, a, s, stats=None, stream=None):
+        self._check(self._lib.omnimem_calibrate(self.handle, self._layers(layers), _ptr(a), _ptr(s), _ptr(stats),
+                                                _stream(stream)))
+
+    def omnimem_calibration_reset(self):
+        self._check(self._lib.omnimem_calibration_reset(self.handle))
+
+    def omnimem_calibration_budgets(self, total_budget, layer_budgets, stream=None):
+        self._check(self._lib.omnimem_calibration_budgets(self.handle, int(total_budget), _ptr(layer_budgets),
+                                                          _stream(stream)))
+
+    def omnimem_allocate_fixed(self, layers, a, s, layer_budgets, budgets, stats=None, stream=None):
+        self._check(self._lib.omnimem_allocate_fixed(self.handle, self._layers(layers), _ptr(a), _ptr(s),
+                                                     _ptr(layer_budgets), _ptr(budgets), _ptr(stats),
+                                                     _stream(stream)))
 
 
     def omnimem_profile(self, on):

@@ -44,6 +44,8 @@ class DeviceStep:
         self.lse = torch.zeros((self.n_layers, h_q, self.max_chunk), device=dev, dtype=torch.float32)
         self.budgets = torch.zeros((self.n_layers, 2), device=dev, dtype=torch.int32)
         self.stats = torch.zeros((self.n_layers, 10), device=dev, dtype=torch.float32)
+        self.layer_budgets = torch.zeros(self.n_layers, device=dev, dtype=torch.int32)
+        self.fixed_budgets = False          # run() splits self.layer_budgets instead of Eq. (14)
         self.lse_in = [None] * self.n_layers
         self.descs = self._descs()
 
@@ -72,10 +74,27 @@ class DeviceStep:
         self.ctx.omnimem_select_compact(self.descs, self.a if a is None else a, self.s if s is None else s,
                                         self.budgets if budgets is None else budgets, self.idx, stream)
 
+    # offline budgets (calibration) ----------------------------------------
+    def calibrate(self, stream=None, a=None, s=None):
+        self.ctx.omnimem_calibrate(self.descs, self.a if a is None else a, self.s if s is None else s,
+                                   self.stats, stream)
+
+    def calibration_budgets(self, stream=None):
+        """The calibration's layer budgets into self.layer_budgets."""
+        self.ctx.omnimem_calibration_budgets(self.total_budget, self.layer_budgets, stream)
+
+    def allocate_fixed(self, stream=None, a=None, s=None, layer_budgets=None):
+        self.ctx.omnimem_allocate_fixed(self.descs, self.a if a is None else a, self.s if s is None else s,
+                                        self.layer_budgets if layer_budgets is None else layer_budgets,
+                                        self.budgets, self.stats, stream)
+
     def run(self, stream=None):
         self.score(stream, lse_out=False)
         self.redundancy(stream)
-        self.allocate(stream)
+        if self.fixed_budgets:
+            self.allocate_fixed(stream)
+        else:
+            self.allocate(stream)
         self.select_compact(stream)
 
     # host views -----------------------------------------------------------

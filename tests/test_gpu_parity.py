@@ -342,6 +342,107 @@ def test_long_cache_workload_sampled():
 
 
 # ---------------------------------------------------------------------------
+# Offline budgets (end of Sec. 3.2; reading R21)
+# ---------------------------------------------------------------------------
+
+def _calib_layers():
+    # five layers of different sizes; the smallest has fewer rows (243) than
+    # the calibrated budgets can reach, so the cap of a fixed step is met
+    return ragged_layers(5, seed=110, caches=((200, 77), (333, 111), (64, 17), (500, 40), (150, 150)))
+
+
+def test_offline_budgets_teacher_forced():
+    # Calibration over four steps of generator-drawn a and s, then two steps
+    # under the fixed layer budgets: layer budgets and (M_v, M_a) exactly
+    # the oracle's, each step's statistics within tolerance.
+    layers = _calib_layers()
+    total = 5 * 200
+    st = DeviceStep(layers, total)
+    mods = [lay["modality"] for lay in layers]
+    st.ctx.omnimem_calibration_reset()
+    c_steps = []
+    for seed in range(4):
+        a_syn, s_syn = synth.make_scores(mods, st.h_kv, 500 + seed)
+        stats = torch.zeros_like(st.stats)
+        st.ctx.omnimem_calibrate(st.descs, st.to_device_f32(a_syn), st.to_device_f32(s_syn), stats)
+        _sync()
+        ref = [om.avba_statistics(a.astype(np.float64), s.astype(np.float64), m)
+               for a, s, m in zip(a_syn, s_syn, mods)]
+        got = stats.cpu().numpy()
+        for l, rs in enumerate(ref):
+            w_v, _ = om.modality_weights(rs["C_v"], rs["C_a"], P.RATIO)
+            rs["w_v"] = w_v
+            P.assert_close_a(got[l], [rs[k] for k in P.STAT_KEYS], f"calibration step {seed} stats layer {l}")
+        c_steps.append([rs["C_l"] for rs in ref])
+    st.calibration_budgets()
+    _sync()
+    ref_lb = om.calibration_budgets(c_steps, total, P.TEMPERATURE)
+    got_lb = st.layer_budgets.cpu().numpy()
+    np.testing.assert_array_equal(got_lb, ref_lb)
+    for seed in (600, 601):
+        a_syn, s_syn = synth.make_scores(mods, st.h_kv, seed)
+        budgets = torch.zeros_like(st.budgets)
+        st.ctx.omnimem_allocate_fixed(st.descs, st.to_device_f32(a_syn), st.to_device_f32(s_syn),
+                                      st.layer_budgets, budgets)
+        _sync()
+        want = []
+        for a, s, m, b in zip(a_syn, s_syn, mods, ref_lb):
+            rs = om.avba_statistics(a.astype(np.float64), s.astype(np.float64), m)
+            w_v, _ = om.modality_weights(rs["C_v"], rs["C_a"], P.RATIO)
+            want.append(om.fixed_split(int(b), w_v, int((m == 0).sum()), int((m == 1).sum())))
+        np.testing.assert_array_equal(budgets.cpu().numpy(), np.array(want))
+    # a reset and a single step: the budgets of that step's values alone
+    st.ctx.omnimem_calibration_reset()
+    a_syn, s_syn = synth.make_scores(mods, st.h_kv, 700)
+    st.ctx.omnimem_calibrate(st.descs, st.to_device_f32(a_syn), st.to_device_f32(s_syn))
+    st.calibration_budgets()
+    _sync()
+    one = [om.avba_statistics(a.astype(np.float64), s.astype(np.float64), m)["C_l"]
+           for a, s, m in zip(a_syn, s_syn, mods)]
+    np.testing.assert_array_equal(st.layer_budgets.cpu().numpy(), om.calibration_budgets([one], total,
+                                                                                           P.TEMPERATURE))
+    st.close()
+
+
+def test_step_under_fixed_budgets_end_to_end():
+    # The whole GPU step with the layer budgets fixed: each layer keeps
+    # min(B_l, N_l) rows, a valid top-M of the GPU's own psi, compacted.
+    layers = _calib_layers()
+    st = DeviceStep(layers, 1000)
+    lb = np.array([150, 400, 10**6, 0, 231], dtype=np.int32)
+    st.layer_budgets.copy_(torch.from_numpy(lb))
+    st.fixed_budgets = True
+    st.run()
+    _sync()
+    budgets = st.budgets.cpu().numpy()
+    for l, lay in enumerate(layers):
+        mod = np.asarray(lay["modality"])
+        mv, ma = budgets[l]
+        assert mv + ma == min(lb[l], len(mod))
+        assert 0 <= mv <= (mod == 0).sum() and 0 <= ma <= (mod == 1).sum()
+        a, s, idx = st.host("a", l), st.host("s", l), st.host("idx", l)
+        k_out = st.k_out[l].float().cpu().numpy()
+        for g in range(st.h_kv):
+            row = idx[g, : mv + ma]
+            P.check_topk_property(row, a[g], s[g], mod, mv, ma)
+            np.testing.assert_array_equal(k_out[g, : mv + ma], lay["k"][g, row])
+    st.close()
+
+
+def test_offline_budgets_errors():
+    layers = ragged_layers(seed=111)
+    st = DeviceStep(layers, 300)
+    st.ctx.omnimem_calibration_reset()
+    with pytest.raises(omnimem.OmnimemError) as e:
+        st.calibration_budgets()            # no calibration step yet
+    assert e.value.status == omnimem.ERR_INVALID_ARG
+    with pytest.raises(omnimem.OmnimemError) as e:
+        st.ctx.omnimem_allocate_fixed(st.descs, st.a, st.s, None, st.budgets)
+    assert e.value.status == omnimem.ERR_INVALID_ARG
+    st.close()
+
+
+# ---------------------------------------------------------------------------
 # Degenerate cases and argument validation
 # ---------------------------------------------------------------------------
 
