@@ -63,6 +63,10 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="qwen7b-layer-6144")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--offline-budgets", action="store_true",
+                   help="fix the layer budgets in advance from a calibration (end of Sec. 3.2): static "
+                        "workloads calibrate on their own step, streams on their warmup chunks; the timed "
+                        "steps only split the fixed budgets")
     p.add_argument("--lse-given", action="store_true",
                    help="take each layer's log-sum-exp as an input, as the model's chunk prefill attention "
                         "produces it (Eq. 1): the step then runs without the LSE pass")
@@ -149,6 +153,14 @@ def run_static(args, torch):
         torch.cuda.synchronize()
         step.set_lse_inputs([step.lse[l, :, : int(lay["q"].shape[1])].contiguous() for l, lay in enumerate(layers)])
         torch.cuda.synchronize()
+    if args.offline_budgets:
+        step.score(stream, lse_out=False)
+        step.redundancy(stream)
+        step.ctx.omnimem_calibration_reset()
+        step.calibrate(stream)
+        step.calibration_budgets(stream)
+        step.fixed_budgets = True
+        torch.cuda.synchronize()
     print(f"[bench] workload {args.workload}: inputs resident, warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
         step.run(stream)
@@ -177,7 +189,8 @@ def run_static(args, torch):
     config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "cache": spec["n_cache_v"] + spec["n_cache_a"],
               "chunk": spec["n_frames"] * (spec["frame_v"] + spec["frame_a"]), "budget": spec["total_budget"],
-              "lse": "input" if args.lse_given else "computed"}
+              "lse": "input" if args.lse_given else "computed",
+              "layer_budgets": "offline" if args.offline_budgets else "per step"}
     baseline = None
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
@@ -207,12 +220,25 @@ def run_stream(args, torch):
     print(f"[bench] stream {args.workload}: {steps} chunks resident, warmup {args.warmup} chunks",
           file=sys.stderr, flush=True)
     warm = runner()
+    warm.calibrating = args.offline_budgets
     for t in range(min(args.warmup, steps)):
         warm.push(chunks[t])
-    warm.close()
+    if args.offline_budgets:
+        if min(args.warmup, steps) == 0:
+            print("--offline-budgets calibrates on the warmup chunks: give --warmup >= 1", file=sys.stderr)
+            sys.exit(1)
+        warm.freeze_budgets()
+    fixed_lb = warm.layer_budgets.clone() if args.offline_budgets else None
     torch.cuda.synchronize()
+    warm.close()
 
-    run = runner()
+    def fix(r):
+        if fixed_lb is not None:
+            r.layer_budgets.copy_(fixed_lb)
+            r.fixed = True
+        return r
+
+    run = fix(runner())
     stream = torch.cuda.current_stream()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -227,7 +253,7 @@ def run_stream(args, torch):
 
     # The same stream again with per-kernel HIP events; per-step work from
     # the shapes each step saw.
-    run = runner()
+    run = fix(runner())
     run.ctx.omnimem_profile(True)
     tot = [0, 0, 0, 0]
     elt = 2 if spec["dtype"] == "bf16" else 4
@@ -247,7 +273,8 @@ def run_stream(args, torch):
     work = work_table(*[x / steps for x in tot])
     config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "chunks": steps,
-              "chunk": src.chunk_len, "budget": spec["total_budget"]}
+              "chunk": src.chunk_len, "budget": spec["total_budget"],
+              "layer_budgets": "offline" if args.offline_budgets else "per step"}
     return ms, tokens / (ms / 1e3), kernels, work, spec["dtype"], config, None
 
 

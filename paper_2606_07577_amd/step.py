@@ -156,6 +156,9 @@ class StreamRunner:
         self.idx = torch.full(shape, -1, device=dev, dtype=torch.int32)
         self.budgets = torch.zeros((n_layers, 2), device=dev, dtype=torch.int32)
         self.stats = torch.zeros((n_layers, 10), device=dev, dtype=torch.float32)
+        self.layer_budgets = torch.zeros(n_layers, device=dev, dtype=torch.int32)
+        self.calibrating = False   # each step also adds its C^(l) to the calibration
+        self.fixed = False         # steps split self.layer_budgets instead of Eq. (14)
         self.cur = 0
         self.n_cache = [0] * n_layers
         self.steps = 0
@@ -200,7 +203,13 @@ class StreamRunner:
         self._descs, self._qs = descs, qs
         self.ctx.omnimem_score(descs, self.a, None, stream)
         self.ctx.omnimem_redundancy(descs, self.s, stream)
-        self.ctx.omnimem_allocate(descs, self.a, self.s, self.total_budget, self.budgets, self.stats, stream)
+        if self.calibrating:
+            self.ctx.omnimem_calibrate(descs, self.a, self.s, None, stream)
+        if self.fixed:
+            self.ctx.omnimem_allocate_fixed(descs, self.a, self.s, self.layer_budgets, self.budgets, self.stats,
+                                            stream)
+        else:
+            self.ctx.omnimem_allocate(descs, self.a, self.s, self.total_budget, self.budgets, self.stats, stream)
         self.ctx.omnimem_select_compact(descs, self.a, self.s, self.budgets, self.idx, stream)
         budgets = self.budgets.cpu().numpy()
         for l in range(self.L):
@@ -212,6 +221,12 @@ class StreamRunner:
         self.cur = other
         self.steps += 1
         return budgets
+
+    def freeze_budgets(self, stream=None):
+        """Layer budgets from the steps calibrated so far; later steps split them."""
+        self.ctx.omnimem_calibration_budgets(self.total_budget, self.layer_budgets, stream)
+        self.calibrating = False
+        self.fixed = True
 
     def close(self):
         self.ctx.close()

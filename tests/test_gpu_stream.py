@@ -162,3 +162,72 @@ def _oracle_sampled(run, chunk, kept, l, t, rng):
     rows = np.sort(rng.choice(n, size=64, replace=False))
     s_ref = om.redundancy(v, mod, "max", rows=rows)
     P.assert_close_s(run.s[l, :, :n].cpu().numpy()[:, rows], s_ref, f"s chunk {t} layer {l}")
+
+
+def test_small_stream_with_offline_budgets():
+    # Offline budgets (end of Sec. 3.2; reading R21) on a stream: the first
+    # four chunks calibrate (their steps allocate online), the layer budgets
+    # are then frozen and the remaining chunks only split them.  The GPU's
+    # frozen budgets come from its own statistics, so they may differ from
+    # the oracle's by a rounding unit; from the freeze on the GPU takes the
+    # oracle's (teacher-forced) and each step must match the oracle's.
+    src = synth.StreamSource("small-stream")
+    sp = src.spec
+    L, h_kv, d = sp["n_layers"], sp["h_kv"], sp["d"]
+    total = sp["total_budget"]
+    n_cal = 4
+    run = _runner(src)
+    run.ctx.omnimem_calibration_reset()
+    run.calibrating = True
+    state = [dict(k=np.zeros((h_kv, 0, d)), v=np.zeros((h_kv, 0, d)), m_v=0, m_a=0) for _ in range(L)]
+    c_hist, ref_lb = [], None
+    for t in range(sp["n_chunks"]):
+        chunk = src.chunk(t)
+        layers = []
+        for l, ch in enumerate(chunk):
+            st = state[l]
+            mod = np.concatenate([np.zeros(st["m_v"], np.uint8), np.ones(st["m_a"], np.uint8), ch["modality"]])
+            layers.append({"q": ch["q"].astype(np.float64),
+                           "k": np.concatenate([st["k"], ch["k"]], axis=1).astype(np.float64),
+                           "v": np.concatenate([st["v"], ch["v"]], axis=1).astype(np.float64),
+                           "modality": mod, "n_cache": st["m_v"] + st["m_a"], "sm_scale": ch["sm_scale"]})
+            run.set_cache(l, st["k"], st["v"], st["m_v"], st["m_a"])
+        ref = om.compression_step(layers, total, lam=P.LAMBDA, temperature=P.TEMPERATURE, r=P.RATIO,
+                                  layer_budgets=ref_lb)
+        budgets = run.push(chunk).astype(np.int64)
+        torch.cuda.synchronize()
+        ref_b = np.array(ref["budgets"], dtype=np.int64)
+        n_tok = np.array([len(x["modality"]) for x in layers])
+        print(f"chunk {t}: N {n_tok.tolist()} budgets {budgets.tolist()}", flush=True)
+        if ref_lb is None:
+            c_hist.append([s["C_l"] for s in ref["stats"]])
+            assert np.abs(budgets - ref_b).max() <= 1
+        else:
+            np.testing.assert_array_equal(budgets.sum(axis=1), np.minimum(ref_lb, n_tok))
+            assert np.abs(budgets - ref_b).max() <= 1
+        prev = 1 - run.cur
+        for l, lay in enumerate(layers):
+            mv, ma = budgets[l]
+            idx = run.idx[l, :, : mv + ma].cpu().numpy()
+            k_out = run.kbuf[run.cur][l][:, : mv + ma].float().cpu().numpy()
+            np.testing.assert_array_equal(run.kbuf[prev][l][:, : len(lay["modality"])].float().cpu().numpy(),
+                                          lay["k"])
+            if (mv, ma) == tuple(ref_b[l]):
+                psi = om.retention_score(ref["a"][l], ref["s"][l], P.LAMBDA)
+                for g in range(h_kv):
+                    P.check_selection(idx[g], psi[g], lay["modality"], mv, ma, rel=5e-3)
+            for g in range(h_kv):
+                np.testing.assert_array_equal(k_out[g], lay["k"][g, idx[g]])
+        if t == n_cal - 1:
+            run.freeze_budgets()
+            ref_lb = om.calibration_budgets(c_hist, total, P.TEMPERATURE)
+            got_lb = run.layer_budgets.cpu().numpy().astype(np.int64)
+            print(f"frozen layer budgets: gpu {got_lb.tolist()} oracle {ref_lb.tolist()}", flush=True)
+            assert got_lb.sum() == ref_lb.sum() == total
+            assert np.abs(got_lb - ref_lb).max() <= 1
+            run.layer_budgets.copy_(torch.from_numpy(ref_lb.astype(np.int32)))
+        for l in range(L):
+            mv, ma = ref["budgets"][l]
+            state[l] = dict(k=ref["k_out"][l].astype(np.float32), v=ref["v_out"][l].astype(np.float32),
+                            m_v=int(mv), m_a=int(ma))
+    run.close()
