@@ -21,6 +21,7 @@ in the paper's order and notation:
     (end of Sec. 3.2)                                                 -> calibration_budgets,
                                                                          fixed_split
   * Eqs. (4), (5) Select: top-M by psi per modality (Sec. 3.1)         -> select
+    (one index set per layer, as Eqs. (4), (5) write it)              -> layer_shared_select
   * Eq. (3) / Eq. (2): the retained pairs form the next caches         -> compact
 
 Where the paper is silent the oracle takes these readings (each one is
@@ -49,6 +50,9 @@ listed with its justification in the design notes):
       steps, then Eq. (14), the clamp and the integer rounding (R15-R17) on
       the means, with no cap by a layer's token count; a step under these
       budgets keeps min(B^(l), N_l) rows of layer l, split by its own w_v.
+  R22 layer-shared selection: the layer's psi takes a summed over the KV
+      heads (every query head's attention, Eq. (6) over all heads) and s
+      averaged over them; every KV head keeps the rows chosen from it.
 """
 from __future__ import annotations
 
@@ -410,6 +414,18 @@ def select(psi, modality, m_visual, m_audio):
     return np.stack(rows)
 
 
+def layer_shared_select(a, s, modality, m_visual, m_audio, lam=DEFAULT_LAMBDA):
+    """One index set per layer (reading R22): rows ranked by psi of the
+    layer's importance sum_g a_g and redundancy mean_g s_g, top-M per
+    modality as in select(); every KV head keeps those rows.
+    a, s: [H_kv, N].  Returns int64 [H_kv, M_v + M_a] with identical rows.
+    """
+    a_layer = np.asarray(a, dtype=np.float64).sum(axis=0, keepdims=True)
+    s_layer = np.asarray(s, dtype=np.float64).mean(axis=0, keepdims=True)
+    idx = select(retention_score(a_layer, s_layer, lam), modality, m_visual, m_audio)
+    return np.repeat(idx, np.asarray(a).shape[0], axis=0)
+
+
 def compact(x, idx):
     """Next cache rows: x_out[g, i] = x[g, idx[g, i]]  ([H_kv, M, d])."""
     return np.stack([x[g, idx[g]] for g in range(x.shape[0])])
@@ -422,12 +438,13 @@ def compact(x, idx):
 def compression_step(layers, total_budget, lam=DEFAULT_LAMBDA, r=DEFAULT_R,
                      temperature=DEFAULT_T, bmin_frac=DEFAULT_BMIN_FRAC,
                      bmax_frac=DEFAULT_BMAX_FRAC, mode="max", causal=True,
-                     use_keys=False, layer_budgets=None):
+                     use_keys=False, layer_budgets=None, shared_selection=False):
     """Run the whole step.  `layers` is a list of dicts with keys
     q [H_q,C,d], k and v [H_kv,N,d], modality [N], n_cache, sm_scale.
     With `layer_budgets` (offline budgets B^(l), reading R21) the layers
     keep those, capped at their token counts, instead of the budgets of
-    Eq. (14) from this step.
+    Eq. (14) from this step.  With `shared_selection` every KV head of a
+    layer keeps the same rows (reading R22).
 
     Returns a dict of per-layer lists: a, s, stats, budgets (M_v, M_a), idx,
     k_out, v_out, plus the real-valued shares x_l and integer B_l.
@@ -459,8 +476,10 @@ def compression_step(layers, total_budget, lam=DEFAULT_LAMBDA, r=DEFAULT_R,
         st["w_v"] = w_v
         m_v, m_a = split_budget(int(b_l), w_v, int((mod == VISUAL).sum()),
                                 int((mod == AUDIO).sum()))
-        psi = retention_score(a, s, lam)
-        idx = select(psi, mod, m_v, m_a)
+        if shared_selection:
+            idx = layer_shared_select(a, s, mod, m_v, m_a, lam)
+        else:
+            idx = select(retention_score(a, s, lam), mod, m_v, m_a)
         out["budgets"].append((m_v, m_a))
         out["idx"].append(idx)
         out["k_out"].append(compact(layer["k"], idx))
