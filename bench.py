@@ -67,6 +67,9 @@ def parse_args():
                    help="fix the layer budgets in advance from a calibration (end of Sec. 3.2): static "
                         "workloads calibrate on their own step, streams on their warmup chunks; the timed "
                         "steps only split the fixed budgets")
+    p.add_argument("--shared-selection", action="store_true",
+                   help="keep one index set per layer (Eqs. 4-5), ranked by the importance summed and the "
+                        "redundancy averaged over the KV heads")
     p.add_argument("--lse-given", action="store_true",
                    help="take each layer's log-sum-exp as an input, as the model's chunk prefill attention "
                         "produces it (Eq. 1): the step then runs without the LSE pass")
@@ -144,7 +147,7 @@ def run_static(args, torch):
 
     spec = synth.WORKLOADS[args.workload]
     layers = synth.make_workload(args.workload)
-    step = DeviceStep(layers, spec["total_budget"])
+    step = DeviceStep(layers, spec["total_budget"], shared_selection=int(args.shared_selection))
     stream = torch.cuda.current_stream()
     if args.lse_given:
         # Stand-in for the prefill's log-sum-exp: the library's own, computed
@@ -190,7 +193,8 @@ def run_static(args, torch):
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "cache": spec["n_cache_v"] + spec["n_cache_a"],
               "chunk": spec["n_frames"] * (spec["frame_v"] + spec["frame_a"]), "budget": spec["total_budget"],
               "lse": "input" if args.lse_given else "computed",
-              "layer_budgets": "offline" if args.offline_budgets else "per step"}
+              "layer_budgets": "offline" if args.offline_budgets else "per step",
+              "selection": "per layer" if args.shared_selection else "per KV head"}
     baseline = None
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
@@ -215,7 +219,8 @@ def run_stream(args, torch):
 
     def runner():
         return StreamRunner(spec["n_layers"], spec["h_q"], spec["h_kv"], spec["d"], src.chunk_len,
-                            spec["total_budget"], dtype=spec["dtype"])
+                            spec["total_budget"], dtype=spec["dtype"],
+                            shared_selection=int(args.shared_selection))
 
     print(f"[bench] stream {args.workload}: {steps} chunks resident, warmup {args.warmup} chunks",
           file=sys.stderr, flush=True)
@@ -274,7 +279,8 @@ def run_stream(args, torch):
     config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "chunks": steps,
               "chunk": src.chunk_len, "budget": spec["total_budget"],
-              "layer_budgets": "offline" if args.offline_budgets else "per step"}
+              "layer_budgets": "offline" if args.offline_budgets else "per step",
+              "selection": "per layer" if args.shared_selection else "per KV head"}
     return ms, tokens / (ms / 1e3), kernels, work, spec["dtype"], config, None
 
 

@@ -81,6 +81,9 @@ typedef struct {
   int32_t causal;        /* 1: chunk row n_cache+t is visible to query i iff t <= i */
   int32_t sim;           /* omnimem_sim                                        */
   int32_t sim_on_keys;   /* 0: cosine of values (Sec. 3.1), 1: of keys         */
+  int32_t shared_selection; /* 0: kept rows per KV head; 1: one set per layer
+                             (Eqs. 4-5 carry no head index), ranked by a
+                             summed and s averaged over the KV heads      */
   int64_t max_tokens;    /* capacity: largest N = n_cache + n_chunk of a layer */
   int64_t max_chunk;     /* capacity: largest n_chunk of a layer               */
 } omnimem_config;
@@ -205,7 +208,10 @@ omnimem_status omnimem_allocate_fixed(omnimem_ctx* ctx, const omnimem_layer* lay
  * largest psi = a^lambda (1 - s) (0^lambda = 0; ties to the lower row), in
  * ascending row order, visual block first; then k_out[g][i] = k[g][idx[g][i]]
  * and the same for v, for i < M_v + M_a.  The next step's modality mask is
- * M_v zeros followed by M_a ones.
+ * M_v zeros followed by M_a ones.  With cfg.shared_selection the kept rows
+ * are chosen once per (layer, modality), by psi of the summed a and the mean
+ * s over the layer's KV heads (summed in head order, fp32), and every head
+ * keeps them: the idx rows of a layer are then identical.
  *   a, s     [L][H_kv][max_tokens] fp32; budgets [L][2] int32 (device).
  *   idx      optional [L][H_kv][max_tokens] int32 output of the kept rows.
  * k_out / v_out must not overlap k / v (ping-pong the cache buffers); the

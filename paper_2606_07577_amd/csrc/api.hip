@@ -452,7 +452,8 @@ omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* lay
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
-  return finish(ctx, launch_select_compact(ctx->dm, ctx->cfg.dtype, ctx->cfg.lambda, dev, ctx->ws, a, s, budgets,
+  return finish(ctx, launch_select_compact(ctx->dm, ctx->cfg.dtype, ctx->cfg.lambda, ctx->cfg.shared_selection ? 1 : 0,
+                                           dev, ctx->ws, a, s, budgets,
                                            idx, stream),
                 stream, "omnimem_select_compact launch");
 }

@@ -261,7 +261,7 @@ hipError_t launch_calibration_budgets(const Dims& dm, const Workspace& ws, int64
 hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
                                  const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
                                  float* stats, hipStream_t st);
-hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, const LayerDesc* desc,
+hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, const LayerDesc* desc,
                                  const Workspace& ws, const float* a, const float* s,
                                  const int32_t* budgets, int32_t* idx, hipStream_t st);
 

@@ -70,7 +70,11 @@ __device__ inline int wave_scan(int v, int* wave_tot, int* total) {
 // from ballots within the wave and one scan of the wave totals; the members'
 // keys sit at their ranks in LDS (or, for segments too large for LDS, by row
 // in global memory).
+// shared: one workgroup per (layer, modality) ranks rows by the layer's
+// importance (a summed over the KV heads) and redundancy (s averaged over
+// them, in head order) and writes the kept rows to every head's idx row.
 __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restrict__ layers, Dims dm, float lambda,
+                                                        int shared,
                                                         const float* __restrict__ a, const float* __restrict__ s,
                                                         const int32_t* __restrict__ budgets,
                                                         uint32_t* __restrict__ keys, int32_t* __restrict__ idx,
@@ -96,6 +100,18 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   const int R = (N + kSelThreads - 1) / kSelThreads;   // rows per lane
   const int wrow0 = wave * 64 * R;
   auto member = [&](int j) { return j < N && (mod[j] ? 1 : 0) == mu; };
+  // importance and redundancy of row j: this KV head's, or the layer's
+  const int nh = shared ? dm.Hkv : 1;
+  auto read_a = [&](int j) {
+    float t = 0.0f;
+    for (int h = 0; h < nh; ++h) t += gload<float>(ag + (int64_t)h * dm.max_tokens + j);
+    return t;
+  };
+  auto read_s = [&](int j) {
+    float t = 0.0f;
+    for (int h = 0; h < nh; ++h) t += gload<float>(sg + (int64_t)h * dm.max_tokens + j);
+    return nh == 1 ? t : t / (float)nh;
+  };
   // the segment's budget (and the visual one, where the audio rows go),
   // requested first so that their latency overlaps the reads below
   const int bud_mu = budgets[2 * l + mu], bud_v = budgets[2 * l];
@@ -122,8 +138,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       const int j = min(wrow0 + (i0 + u) * 64 + lane, N - 1);
       mv[u] = gload<uint8_t>(mod + j);
       if (one_grp) {
-        av[u] = gload<float>(ag + j);
-        sv[u] = gload<float>(sg + j);
+        av[u] = read_a(j);
+        sv[u] = read_s(j);
       }
     }
 #pragma unroll
@@ -152,8 +168,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       const int j = wrow0 + (i0 + u) * 64 + lane;
       mb[u] = i0 + u < R && member_at(i0 + u, j);
       if (!one_grp) {
-        av[u] = gload<float>(ag + min(j, N - 1));
-        sv[u] = gload<float>(sg + min(j, N - 1));
+        av[u] = read_a(min(j, N - 1));
+        sv[u] = read_s(min(j, N - 1));
       }
     }
     if (!one_grp) {
@@ -353,7 +369,10 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     }
 #pragma unroll
     for (int u = 0; u < kGrp; ++u) {
-      if ((sb[u] >> lane) & 1ull) ig[o + __popcll(sb[u] & lt)] = wrow0 + (i0 + u) * 64 + lane;
+      if ((sb[u] >> lane) & 1ull) {
+        const int slot = o + __popcll(sb[u] & lt), row = wrow0 + (i0 + u) * 64 + lane;
+        for (int h = 0; h < nh; ++h) ig[(int64_t)h * dm.max_tokens + slot] = row;
+      }
       o += __popcll(sb[u]);
     }
   }
@@ -409,11 +428,13 @@ void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, c
 
 }  // namespace
 
-hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, const LayerDesc* desc,
+hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, const LayerDesc* desc,
                                  const Workspace& ws, const float* a, const float* s, const int32_t* budgets,
                                  int32_t* idx, hipStream_t st) {
   int32_t* ix = idx ? idx : ws.idx;
-  OMNIMEM_LAUNCH(ws, K_TOPK, st, psi_topk<<<dim3(2, dm.Hkv, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets, ws.keys, ix, ws.eff));
+  OMNIMEM_LAUNCH(ws, K_TOPK, st,
+                 psi_topk<<<dim3(2, shared ? 1 : dm.Hkv, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, shared, a, s,
+                                                                                      budgets, ws.keys, ix, ws.eff));
   if (dtype == 0) {
     if (dm.d == 128) launch_gather<uint16_t, 128>(dm, desc, ws, ix, st);
     else launch_gather<uint16_t, 64>(dm, desc, ws, ix, st);

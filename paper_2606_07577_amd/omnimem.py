@@ -40,7 +40,8 @@ class Config(ctypes.Structure):
         ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("lambda_", ctypes.c_float),
         ("ratio_r", ctypes.c_float), ("temperature", ctypes.c_float), ("b_min_frac", ctypes.c_float),
         ("b_max_frac", ctypes.c_float), ("causal", ctypes.c_int32), ("sim", ctypes.c_int32),
-        ("sim_on_keys", ctypes.c_int32), ("max_tokens", ctypes.c_int64), ("max_chunk", ctypes.c_int64),
+        ("sim_on_keys", ctypes.c_int32), ("shared_selection", ctypes.c_int32), ("max_tokens", ctypes.c_int64),
+        ("max_chunk", ctypes.c_int64),
     ]
 
 

@@ -342,6 +342,71 @@ def test_long_cache_workload_sampled():
 
 
 # ---------------------------------------------------------------------------
+# Layer-shared selection (Eqs. 4-5 carry no head index; reading R22)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["ragged-bf16", "ragged-3layer", "qwen-layer"])
+def test_shared_selection_teacher_forced(name):
+    # The oracle's a and s through the GPU's selection with one index set per
+    # layer: every head keeps the same rows, a top-M of the oracle's layer
+    # psi (ties within the fp32 rounding of the head sums), compacted.
+    base = get_case(name)
+    layers = base.layers
+    st = DeviceStep(layers, base.budget, shared_selection=1)
+    a_ref, s_ref = [], []
+    for lay in base.layers64:
+        a_ref.append(om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], True)
+                     .astype(np.float32))
+        s_ref.append(om.redundancy(lay["v"], lay["modality"], "max").astype(np.float32))
+    _, _, budgets = P.oracle_allocation([x.astype(np.float64) for x in a_ref],
+                                        [x.astype(np.float64) for x in s_ref], layers, base.budget)
+    st.budgets.copy_(torch.from_numpy(budgets.astype(np.int32)))
+    st.select_compact(a=st.to_device_f32(a_ref), s=st.to_device_f32(s_ref))
+    _sync()
+    for l, lay in enumerate(layers):
+        mod = np.asarray(lay["modality"])
+        mv, ma = (int(x) for x in budgets[l])
+        idx = st.host("idx", l)[:, : mv + ma]
+        assert (idx == idx[0]).all(), f"layer {l}: heads keep different rows"
+        a64, s64 = a_ref[l].astype(np.float64), s_ref[l].astype(np.float64)
+        psi = om.retention_score(a64.sum(axis=0), s64.mean(axis=0), P.LAMBDA)
+        P.check_selection(idx[0], psi, mod, mv, ma, rel=1e-5)
+        k_out = st.k_out[l].float().cpu().numpy()
+        for g in range(st.h_kv):
+            np.testing.assert_array_equal(k_out[g, : mv + ma], lay["k"][g, idx[0]])
+    st.close()
+
+
+def test_shared_selection_chain_and_one_head_equivalence():
+    # The whole GPU step with shared selection keeps, per layer, a top-M of
+    # the layer psi of its own a and s; with one KV head it is the per-head
+    # step bit for bit.
+    layers = ragged_layers(2, seed=112, caches=((300, 90), (120, 60)))
+    st = DeviceStep(layers, 500, shared_selection=1)
+    st.run()
+    _sync()
+    budgets = st.budgets.cpu().numpy()
+    for l, lay in enumerate(layers):
+        mod = np.asarray(lay["modality"])
+        mv, ma = (int(x) for x in budgets[l])
+        idx = st.host("idx", l)[:, : mv + ma]
+        assert (idx == idx[0]).all()
+        a64, s64 = st.host("a", l).astype(np.float64), st.host("s", l).astype(np.float64)
+        P.check_topk_property(idx[0], a64.sum(axis=0), s64.mean(axis=0), mod, mv, ma)
+    st.close()
+    one = ragged_layers(1, seed=113, h_q=4, h_kv=1)
+    per_head, shared = DeviceStep(one, 200), DeviceStep(one, 200, shared_selection=1)
+    for x in (per_head, shared):
+        x.run()
+    _sync()
+    np.testing.assert_array_equal(per_head.idx.cpu().numpy(), shared.idx.cpu().numpy())
+    np.testing.assert_array_equal(per_head.k_out[0].view(torch.int16).cpu().numpy(),
+                                  shared.k_out[0].view(torch.int16).cpu().numpy())
+    per_head.close()
+    shared.close()
+
+
+# ---------------------------------------------------------------------------
 # Offline budgets (end of Sec. 3.2; reading R21)
 # ---------------------------------------------------------------------------
 
