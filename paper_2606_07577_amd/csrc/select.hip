@@ -70,11 +70,11 @@ __device__ inline int wave_scan(int v, int* wave_tot, int* total) {
 // from ballots within the wave and one scan of the wave totals; the members'
 // keys sit at their ranks in LDS (or, for segments too large for LDS, by row
 // in global memory).
-// shared: one workgroup per (layer, modality) ranks rows by the layer's
+// SHARED: one workgroup per (layer, modality) ranks rows by the layer's
 // importance (a summed over the KV heads) and redundancy (s averaged over
 // them, in head order) and writes the kept rows to every head's idx row.
+template <bool SHARED>
 __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restrict__ layers, Dims dm, float lambda,
-                                                        int shared,
                                                         const float* __restrict__ a, const float* __restrict__ s,
                                                         const int32_t* __restrict__ budgets,
                                                         uint32_t* __restrict__ keys, int32_t* __restrict__ idx,
@@ -101,16 +101,18 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   const int wrow0 = wave * 64 * R;
   auto member = [&](int j) { return j < N && (mod[j] ? 1 : 0) == mu; };
   // importance and redundancy of row j: this KV head's, or the layer's
-  const int nh = shared ? dm.Hkv : 1;
+  const int nh = SHARED ? dm.Hkv : 1;
   auto read_a = [&](int j) {
+    if constexpr (!SHARED) return gload<float>(ag + j);
     float t = 0.0f;
     for (int h = 0; h < nh; ++h) t += gload<float>(ag + (int64_t)h * dm.max_tokens + j);
     return t;
   };
   auto read_s = [&](int j) {
+    if constexpr (!SHARED) return gload<float>(sg + j);
     float t = 0.0f;
     for (int h = 0; h < nh; ++h) t += gload<float>(sg + (int64_t)h * dm.max_tokens + j);
-    return nh == 1 ? t : t / (float)nh;
+    return t / (float)nh;
   };
   // the segment's budget (and the visual one, where the audio rows go),
   // requested first so that their latency overlaps the reads below
@@ -371,7 +373,11 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     for (int u = 0; u < kGrp; ++u) {
       if ((sb[u] >> lane) & 1ull) {
         const int slot = o + __popcll(sb[u] & lt), row = wrow0 + (i0 + u) * 64 + lane;
-        for (int h = 0; h < nh; ++h) ig[(int64_t)h * dm.max_tokens + slot] = row;
+        if constexpr (SHARED) {
+          for (int h = 0; h < nh; ++h) ig[(int64_t)h * dm.max_tokens + slot] = row;
+        } else {
+          ig[slot] = row;
+        }
       }
       o += __popcll(sb[u]);
     }
@@ -432,9 +438,14 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int sh
                                  const Workspace& ws, const float* a, const float* s, const int32_t* budgets,
                                  int32_t* idx, hipStream_t st) {
   int32_t* ix = idx ? idx : ws.idx;
-  OMNIMEM_LAUNCH(ws, K_TOPK, st,
-                 psi_topk<<<dim3(2, shared ? 1 : dm.Hkv, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, shared, a, s,
-                                                                                      budgets, ws.keys, ix, ws.eff));
+  if (shared)
+    OMNIMEM_LAUNCH(ws, K_TOPK, st,
+                   psi_topk<true><<<dim3(2, 1, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets, ws.keys,
+                                                                            ix, ws.eff));
+  else
+    OMNIMEM_LAUNCH(ws, K_TOPK, st,
+                   psi_topk<false><<<dim3(2, dm.Hkv, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets,
+                                                                                  ws.keys, ix, ws.eff));
   if (dtype == 0) {
     if (dm.d == 128) launch_gather<uint16_t, 128>(dm, desc, ws, ix, st);
     else launch_gather<uint16_t, 64>(dm, desc, ws, ix, st);
