@@ -30,12 +30,12 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-layer-6144": {
-        "sources_sha256": "995cc6e419478000c3a04afd823178465329129506e0ed3429a6703fa1fc4832",
-        "lse_pass": 31184159, "colsum_pass": 32956542, "gram_pass": 15431258, "psi_topk": 826743, "gather_compact": 16886544,
+        "sources_sha256": "49b3c4e9a8ff56e4c54f367f8530341f7b89dad635741fb99f789d31dd6616dd",
+        "lse_pass": 31185273, "colsum_pass": 32952971, "gram_pass": 15426145, "psi_topk": 843742, "gather_compact": 16886957,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "995cc6e419478000c3a04afd823178465329129506e0ed3429a6703fa1fc4832",
-        "lse_pass": 611444709, "colsum_pass": 616834306, "gram_pass": 812263019, "psi_topk": 14603045, "gather_compact": 471779962,
+        "sources_sha256": "49b3c4e9a8ff56e4c54f367f8530341f7b89dad635741fb99f789d31dd6616dd",
+        "lse_pass": 614003358, "colsum_pass": 613147343, "gram_pass": 804707608, "psi_topk": 14620432, "gather_compact": 471772128,
     },
 }
 
