@@ -12,6 +12,7 @@ in the paper's order and notation:
   * Eq. (1)  chunk attention over [visual cache; audio cache; chunk]   -> attention_lse
   * Eq. (6)  accumulated attention importance a_k                     -> attention_importance
   * Eq. (7)  cosine redundancy s_k (value vectors, Sec. 3.1)          -> redundancy
+    (hidden states, as Eq. (7) is printed)                            -> hidden_redundancy
   * Eq. (8)  retention score psi_k = a_k^lambda (1 - s_k)              -> retention_score
   * Eqs. (9), (10), (13)  normalised entropy x (1 - mean cosine)      -> avba_statistics
   * Eqs. (11), (12)  audio/visual proportions w_v, w_a                -> modality_weights
@@ -53,6 +54,10 @@ listed with its justification in the design notes):
   R22 layer-shared selection: the layer's psi takes a summed over the KV
       heads (every query head's attention, Eq. (6) over all heads) and s
       averaged over them; every KV head keeps the rows chosen from it.
+  R23 hidden-state source: Eq. (7) on the layer's hidden states (one per
+      token, shared by its KV heads), adjacent form as printed; the kept
+      rows' hidden states are carried with the cache, which needs one
+      index set per layer (R22).
 """
 from __future__ import annotations
 
@@ -199,6 +204,14 @@ def redundancy(u, modality, mode="max", rows=None):
             else:
                 raise ValueError(mode)
     return out
+
+
+def hidden_redundancy(h, modality, h_kv, mode="adj"):
+    """Eq. (7) as printed (reading R23): s_k from the hidden states
+    h [N, d_model] of the layer's tokens, one value per token, repeated for
+    each of the h_kv KV heads.  Returns [h_kv, N]."""
+    s = redundancy(np.asarray(h, dtype=np.float64)[None], modality, mode)
+    return np.repeat(s, h_kv, axis=0)
 
 
 # ---------------------------------------------------------------------------
@@ -438,24 +451,33 @@ def compact(x, idx):
 def compression_step(layers, total_budget, lam=DEFAULT_LAMBDA, r=DEFAULT_R,
                      temperature=DEFAULT_T, bmin_frac=DEFAULT_BMIN_FRAC,
                      bmax_frac=DEFAULT_BMAX_FRAC, mode="max", causal=True,
-                     use_keys=False, layer_budgets=None, shared_selection=False):
+                     use_keys=False, layer_budgets=None, shared_selection=False,
+                     use_hidden=False):
     """Run the whole step.  `layers` is a list of dicts with keys
     q [H_q,C,d], k and v [H_kv,N,d], modality [N], n_cache, sm_scale.
     With `layer_budgets` (offline budgets B^(l), reading R21) the layers
     keep those, capped at their token counts, instead of the budgets of
     Eq. (14) from this step.  With `shared_selection` every KV head of a
-    layer keeps the same rows (reading R22).
+    layer keeps the same rows (reading R22).  With `use_hidden` the
+    redundancy comes from each layer's hidden states `h` [N, d_model]
+    (Eq. 7 as printed, reading R23; adjacent form) and the kept rows' hidden
+    states are compacted too (out["h_out"]), which needs shared_selection.
 
     Returns a dict of per-layer lists: a, s, stats, budgets (M_v, M_a), idx,
     k_out, v_out, plus the real-valued shares x_l and integer B_l.
     """
+    if use_hidden and not shared_selection:
+        raise ValueError("hidden states are carried per token: they need shared_selection")
     out = {"a": [], "s": [], "stats": [], "idx": [], "k_out": [], "v_out": [],
-           "budgets": []}
+           "budgets": [], "h_out": []}
     for layer in layers:
         a = attention_importance(layer["q"], layer["k"], layer["n_cache"],
                                  layer["sm_scale"], causal)
-        src = layer["k"] if use_keys else layer["v"]
-        s = redundancy(src, layer["modality"], mode)
+        if use_hidden:
+            s = hidden_redundancy(layer["h"], layer["modality"], layer["k"].shape[0], mode)
+        else:
+            src = layer["k"] if use_keys else layer["v"]
+            s = redundancy(src, layer["modality"], mode)
         out["a"].append(a)
         out["s"].append(s)
         out["stats"].append(avba_statistics(a, s, layer["modality"]))
@@ -483,5 +505,7 @@ def compression_step(layers, total_budget, lam=DEFAULT_LAMBDA, r=DEFAULT_R,
         out["budgets"].append((m_v, m_a))
         out["idx"].append(idx)
         out["k_out"].append(compact(layer["k"], idx))
+        if use_hidden:
+            out["h_out"].append(np.asarray(layer["h"])[idx[0]])
         out["v_out"].append(compact(layer["v"], idx))
     return out
