@@ -127,11 +127,14 @@ def cpu_baseline(layers, spec):
 
     from oracle import omnimem_oracle as orc
     lay = dict(layers[0])
-    for key in ("q", "k", "v"):
-        lay[key] = lay[key].astype(np.float64)
+    for key in ("q", "k", "v", "h"):
+        if key in lay:
+            lay[key] = lay[key].astype(np.float64)
     per_layer_budget = spec["total_budget"] // spec["n_layers"]
+    hidden = bool(spec.get("hidden_dim"))
     t0 = time.perf_counter()
-    orc.compression_step([lay], per_layer_budget)
+    orc.compression_step([lay], per_layer_budget, mode="adj" if hidden else "max", shared_selection=hidden,
+                         use_hidden=hidden)
     dt = time.perf_counter() - t0
     threads = max([x["num_threads"] for x in threadpoolctl.threadpool_info() if x["user_api"] == "blas"] or [1])
     n = lay["k"].shape[1]
@@ -147,7 +150,14 @@ def run_static(args, torch):
 
     spec = synth.WORKLOADS[args.workload]
     layers = synth.make_workload(args.workload)
-    step = DeviceStep(layers, spec["total_budget"], shared_selection=int(args.shared_selection))
+    options = {"shared_selection": int(args.shared_selection)}
+    if spec.get("hidden_dim"):
+        # redundancy from the hidden states (Eq. 7 as printed, adjacent form); their kept rows are
+        # carried with the cache, which takes one index set per layer
+        from paper_2606_07577_amd import omnimem as om
+        options.update(sim=om.SIM_ADJ, sim_source=om.SRC_HIDDEN, hidden_dim=spec["hidden_dim"],
+                       shared_selection=1)
+    step = DeviceStep(layers, spec["total_budget"], **options)
     stream = torch.cuda.current_stream()
     if args.lse_given:
         # Stand-in for the prefill's log-sum-exp: the library's own, computed
@@ -194,7 +204,9 @@ def run_static(args, torch):
               "chunk": spec["n_frames"] * (spec["frame_v"] + spec["frame_a"]), "budget": spec["total_budget"],
               "lse": "input" if args.lse_given else "computed",
               "layer_budgets": "offline" if args.offline_budgets else "per step",
-              "selection": "per layer" if args.shared_selection else "per KV head"}
+              "selection": "per layer" if options["shared_selection"] else "per KV head",
+              "redundancy": (f"hidden states ({spec['hidden_dim']}), adjacent" if spec.get("hidden_dim")
+                             else "values, all pairs")}
     baseline = None
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)

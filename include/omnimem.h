@@ -67,6 +67,12 @@ typedef enum { OMNIMEM_BF16 = 0, OMNIMEM_F32 = 1 } omnimem_dtype;
  * as printed; one neighbour at either end, 0 for a lone row). */
 typedef enum { OMNIMEM_SIM_MAX = 0, OMNIMEM_SIM_ADJ = 1 } omnimem_sim;
 
+/* Vectors the cosines of Eq. (7) are taken on.  Eq. (7) is printed on the
+ * hidden states; Sec. 3.1 allows the value vectors instead, which keeps the
+ * cache as it is.  Hidden states are per token, so one redundancy serves
+ * every KV head of the layer; they are supported with SIM_ADJ only. */
+typedef enum { OMNIMEM_SRC_VALUES = 0, OMNIMEM_SRC_KEYS = 1, OMNIMEM_SRC_HIDDEN = 2 } omnimem_source;
+
 typedef struct {
   int32_t n_layers;      /* L                                                 */
   int32_t n_q_heads;     /* H_q                                               */
@@ -80,12 +86,14 @@ typedef struct {
   float b_max_frac;      /* per-layer budget <= floor(b_max_frac*B_tot/L)      */
   int32_t causal;        /* 1: chunk row n_cache+t is visible to query i iff t <= i */
   int32_t sim;           /* omnimem_sim                                        */
-  int32_t sim_on_keys;   /* 0: cosine of values (Sec. 3.1), 1: of keys         */
+  int32_t sim_source;    /* omnimem_source                                     */
   int32_t shared_selection; /* 0: kept rows per KV head; 1: one set per layer
                              (Eqs. 4-5 carry no head index), ranked by a
                              summed and s averaged over the KV heads      */
   int64_t max_tokens;    /* capacity: largest N = n_cache + n_chunk of a layer */
   int64_t max_chunk;     /* capacity: largest n_chunk of a layer               */
+  int32_t hidden_dim;    /* d_model of the hidden states (SRC_HIDDEN); rows of
+                            whole 16-byte units                               */
 } omnimem_config;
 
 typedef struct {
@@ -107,6 +115,12 @@ typedef struct {
   void* v_out;              /* [H_kv][M_l][d] next values (select_compact)    */
   int64_t out_head_stride;  /* elements, shared by k_out and v_out            */
   int64_t out_row_stride;   /* elements, shared by k_out and v_out            */
+  const void* hidden;       /* [N][hidden_dim] hidden states of the working-set
+                               rows (SRC_HIDDEN), cfg.dtype                   */
+  int64_t hidden_row_stride;   /* elements                                   */
+  void* hidden_out;         /* optional [M_l][hidden_dim] hidden states of the
+                               kept rows (select_compact, shared selection)   */
+  int64_t hidden_out_row_stride; /* elements                                 */
 } omnimem_layer;
 
 typedef struct omnimem_ctx omnimem_ctx;
@@ -141,7 +155,9 @@ omnimem_status omnimem_score(omnimem_ctx* ctx, const omnimem_layer* layers, floa
                              float* lse_out, hipStream_t stream);
 
 /* Eq. (7): s[l][g][j] = redundancy of row j among the rows of its modality
- * in KV head g, from cfg.sim and cfg.sim_on_keys.  Cosine similarity is 0
+ * in KV head g, from cfg.sim and cfg.sim_source (with SRC_HIDDEN the one
+ * value of each token, from its hidden state, in every head's row).
+ * Cosine similarity is 0
  * when either vector is zero and is clamped to [-1, 1]; a modality with a
  * single row gives s = 0.
  *   s [L][H_kv][max_tokens] fp32, written for j < N_l. */
@@ -211,7 +227,10 @@ omnimem_status omnimem_allocate_fixed(omnimem_ctx* ctx, const omnimem_layer* lay
  * M_v zeros followed by M_a ones.  With cfg.shared_selection the kept rows
  * are chosen once per (layer, modality), by psi of the summed a and the mean
  * s over the layer's KV heads (summed in head order, fp32), and every head
- * keeps them: the idx rows of a layer are then identical.
+ * keeps them: the idx rows of a layer are then identical, and a layer whose
+ * hidden_out is given also gets hidden_out[i] = hidden[idx[l][0][i]]
+ * (INVALID_ARG without shared selection or with hidden_out overlapping
+ * hidden).
  *   a, s     [L][H_kv][max_tokens] fp32; budgets [L][2] int32 (device).
  *   idx      optional [L][H_kv][max_tokens] int32 output of the kept rows.
  * k_out / v_out must not overlap k / v (ping-pong the cache buffers); the

@@ -50,7 +50,8 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 }  // namespace omnimem
 
 static const char* kKernelNames[K_COUNT] = {
-    "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact"};
+    "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact",
+    "gather_hidden"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -162,6 +163,37 @@ omnimem_status validate(omnimem_ctx* ctx, const omnimem_layer* layers, int need)
   return OMNIMEM_OK;
 }
 
+// Hidden-state rows of each layer (the redundancy source of Eq. 7 as
+// printed) and, for select_compact, their optional output rows.
+omnimem_status validate_hidden(omnimem_ctx* ctx, const omnimem_layer* layers, bool outputs) {
+  const omnimem_config& c = ctx->cfg;
+  const int64_t dh = c.hidden_dim;
+  const size_t esz = elt_size(c);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const omnimem_layer& L = layers[l];
+    const int64_t n = L.n_cache + L.n_chunk;
+    if (!outputs || L.hidden_out) {
+      if (!L.hidden || !aligned16(L.hidden) || L.hidden_row_stride < dh || (L.hidden_row_stride * esz) % 16)
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: hidden states must be given, 16-byte aligned, with "
+                    "row stride >= hidden_dim in whole 16-byte units", l);
+    }
+    if (outputs && L.hidden_out) {
+      if (!c.shared_selection)
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: kept hidden states need shared_selection (one index "
+                    "set per layer)", l);
+      if (!aligned16(L.hidden_out) || L.hidden_out_row_stride < dh || (L.hidden_out_row_stride * esz) % 16)
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: hidden_out must be 16-byte aligned with row stride "
+                    ">= hidden_dim in whole 16-byte units", l);
+      uintptr_t h0, h1, o0, o1;
+      extent(L.hidden, 1, n, 0, L.hidden_row_stride, dh, esz, &h0, &h1);
+      extent(L.hidden_out, 1, n, 0, L.hidden_out_row_stride, dh, esz, &o0, &o1);
+      if (overlaps(o0, o1, h0, h1))
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: hidden_out overlaps hidden", l);
+    }
+  }
+  return OMNIMEM_OK;
+}
+
 // Copy the descriptor table to the device unless it equals the last one.
 omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t st, const LayerDesc** dev) {
   const int L = ctx->cfg.n_layers;
@@ -176,6 +208,10 @@ omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t
     x.q_hs = s.q_head_stride; x.q_rs = s.q_row_stride;
     x.kv_hs = s.kv_head_stride; x.kv_rs = s.kv_row_stride;
     x.out_hs = s.out_head_stride; x.out_rs = s.out_row_stride;
+    if (ctx->cfg.sim_source == OMNIMEM_SRC_HIDDEN) {
+      x.hidden = s.hidden; x.hidden_out = s.hidden_out;
+      x.hidden_rs = s.hidden_row_stride; x.hidden_out_rs = s.hidden_out_row_stride;
+    }
     x.n_cache = (int32_t)s.n_cache; x.n_chunk = (int32_t)s.n_chunk; x.n = (int32_t)(s.n_cache + s.n_chunk);
     const double scale = s.sm_scale != 0.0f ? (double)s.sm_scale : 1.0 / std::sqrt((double)ctx->cfg.head_dim);
     x.scale_log2 = (float)(scale * log2e);
@@ -247,7 +283,8 @@ void omnimem_config_default(omnimem_config* c) {
   c->b_max_frac = 2.0f;
   c->causal = 1;
   c->sim = OMNIMEM_SIM_MAX;
-  c->sim_on_keys = 0;
+  c->sim_source = OMNIMEM_SRC_VALUES;
+  c->hidden_dim = 0;
 }
 
 omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
@@ -268,6 +305,17 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
     return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "dtype %d", c.dtype);
   if (c.sim != OMNIMEM_SIM_MAX && c.sim != OMNIMEM_SIM_ADJ)
     return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "sim %d", c.sim);
+  if (c.sim_source < OMNIMEM_SRC_VALUES || c.sim_source > OMNIMEM_SRC_HIDDEN)
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "sim_source %d", c.sim_source);
+  if (c.sim_source == OMNIMEM_SRC_HIDDEN) {
+    const int64_t esz = c.dtype == OMNIMEM_BF16 ? 2 : 4;
+    if (c.hidden_dim < 1 || c.hidden_dim > 65536 || (c.hidden_dim * esz) % 16)
+      return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "hidden_dim %d: need 1..65536 and rows of whole 16-byte units",
+                  c.hidden_dim);
+    if (c.sim != OMNIMEM_SIM_ADJ)
+      return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "hidden states are supported with SIM_ADJ (Eq. 7 as printed) "
+                  "only; the all-pairs maximum on them is not built");
+  }
   if (!std::isfinite(c.lambda) || c.lambda < 0.0f || !(c.ratio_r > 0.0f) || !(c.temperature > 0.0f) ||
       !(c.b_min_frac >= 0.0f) || !(c.b_max_frac >= c.b_min_frac) || !std::isfinite(c.b_max_frac))
     return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "need lambda >= 0, r > 0, T > 0, 0 <= b_min_frac <= b_max_frac");
@@ -282,6 +330,7 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
   dm.causal = c.causal ? 1 : 0;
   dm.qb = (int)((dm.max_chunk + kScoreBlock - 1) / kScoreBlock);
   dm.kb = (int)((dm.max_tokens + kScoreBlock - 1) / kScoreBlock);
+  dm.dh = c.sim_source == OMNIMEM_SRC_HIDDEN ? c.hidden_dim : 0;
   int cus = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ctx->device) == hipSuccess && cus > 0)
     ctx->max_workgroups = 2 * cus;
@@ -355,13 +404,15 @@ omnimem_status omnimem_score(omnimem_ctx* ctx, const omnimem_layer* layers, floa
 
 omnimem_status omnimem_redundancy(omnimem_ctx* ctx, const omnimem_layer* layers, float* s, hipStream_t stream) {
   if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
-  omnimem_status st = validate(ctx, layers, ctx->cfg.sim_on_keys ? NEED_K : NEED_V);
+  const int src = ctx->cfg.sim_source;
+  omnimem_status st = validate(ctx, layers, src == OMNIMEM_SRC_KEYS ? NEED_K : src == OMNIMEM_SRC_VALUES ? NEED_V : 0);
   if (st != OMNIMEM_OK) return st;
   if (!s) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null s");
+  if (src == OMNIMEM_SRC_HIDDEN && (st = validate_hidden(ctx, layers, false)) != OMNIMEM_OK) return st;
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
-  return finish(ctx, launch_redundancy(ctx->dm, ctx->cfg.dtype, ctx->cfg.sim, ctx->cfg.sim_on_keys, dev, ctx->ws,
+  return finish(ctx, launch_redundancy(ctx->dm, ctx->cfg.dtype, ctx->cfg.sim, ctx->cfg.sim_source, dev, ctx->ws,
                                        s, stream),
                 stream, "omnimem_redundancy launch");
 }
@@ -449,12 +500,16 @@ omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* lay
   omnimem_status st = validate(ctx, layers, NEED_K | NEED_V | NEED_OUT);
   if (st != OMNIMEM_OK) return st;
   if (!a || !s || !budgets) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a, s or budgets");
+  bool hidden = false;  // some layer carries its kept rows' hidden states
+  if (ctx->cfg.sim_source == OMNIMEM_SRC_HIDDEN) {
+    if ((st = validate_hidden(ctx, layers, true)) != OMNIMEM_OK) return st;
+    for (int l = 0; l < ctx->cfg.n_layers; ++l) hidden = hidden || layers[l].hidden_out != nullptr;
+  }
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
   return finish(ctx, launch_select_compact(ctx->dm, ctx->cfg.dtype, ctx->cfg.lambda, ctx->cfg.shared_selection ? 1 : 0,
-                                           dev, ctx->ws, a, s, budgets,
-                                           idx, stream),
+                                           hidden, dev, ctx->ws, a, s, budgets, idx, stream),
                 stream, "omnimem_select_compact launch");
 }
 

@@ -35,6 +35,9 @@ struct LayerDesc {
   int64_t lse_base, cs_base;
   int32_t lse_th, cs_th;
   int64_t lse_rbase, cs_rbase;  // the layer's first row in each pass
+  const void* hidden;           // [N][dh] hidden states (redundancy source 2)
+  void* hidden_out;             // kept rows' hidden states, or null
+  int64_t hidden_rs, hidden_out_rs;
 };
 
 // Sizes fixed for a context.
@@ -44,6 +47,7 @@ struct Dims {
   int causal;
   int qb;       // 256-query blocks covering max_chunk
   int kb;       // 256-key blocks covering max_tokens
+  int dh;       // hidden-state width (0: none)
 };
 
 // Score-pass work decomposition.  A "row" is one 256-row block that a
@@ -204,7 +208,7 @@ constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
 // ---------------------------------------------------------------------------
 enum KernelId {
   K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
-  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_COUNT
+  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_COUNT
 };
 struct Profiler;
 void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
@@ -261,7 +265,7 @@ hipError_t launch_calibration_budgets(const Dims& dm, const Workspace& ws, int64
 hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
                                  const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
                                  float* stats, hipStream_t st);
-hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, const LayerDesc* desc,
+hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, const LayerDesc* desc,
                                  const Workspace& ws, const float* a, const float* s,
                                  const int32_t* budgets, int32_t* idx, hipStream_t st);
 

@@ -486,6 +486,79 @@ __global__ void adjacent_cos(const LayerDesc* __restrict__ layers, Dims dm, int 
   s[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = n ? (float)(sum / n) : 0.0f;
 }
 
+// --- Eq. (7) as printed: on the layer's hidden states ------------------------
+// One wave per working-set row j: the cosines of hidden state j with the
+// previous and the next row of its modality (fp64 sums over the 16-byte
+// pieces of the rows, lanes strided, then across the wave), their mean
+// written to every KV head's row of s: hidden states are per token.
+template <typename T>
+__device__ inline void add_piece(const uint4& p, float (&out)[16 / sizeof(T)]) {
+  const uint32_t w[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if constexpr (sizeof(T) == 2) {
+      out[2 * e] = __uint_as_float(w[e] << 16);
+      out[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    } else {
+      out[e] = __uint_as_float(w[e]);
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void adjacent_cos_hidden(const LayerDesc* __restrict__ layers, Dims dm,
+                                                           const int* __restrict__ pos, const int* __restrict__ rank,
+                                                           const int* __restrict__ counts, float* __restrict__ s) {
+  const int l = blockIdx.y;
+  const LayerDesc Ld = layers[l];
+  const int N = Ld.n;
+  const int lane = threadIdx.x & 63;
+  const int j = (int)blockIdx.x * 4 + wave_id();
+  if (j >= N) return;  // the whole wave leaves
+  const int mu = Ld.mod[j] ? 1 : 0;
+  const int K = counts[2 * l + mu];
+  const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
+  const int t = rank[(int64_t)l * dm.max_tokens + j];
+  const int jp = t > 0 ? P[t - 1] : -1, jn = t + 1 < K ? P[t + 1] : -1;
+  const T* H = reinterpret_cast<const T*>(Ld.hidden);
+  const T* x = H + (int64_t)j * Ld.hidden_rs;
+  const T* xp = H + (int64_t)(jp < 0 ? j : jp) * Ld.hidden_rs;
+  const T* xn = H + (int64_t)(jn < 0 ? j : jn) * Ld.hidden_rs;
+  constexpr int EPP = 16 / (int)sizeof(T);  // elements per 16-byte piece
+  const int pieces = dm.dh / EPP;
+  double xx = 0.0, pp = 0.0, nn = 0.0, xpd = 0.0, xnd = 0.0;
+  for (int c = lane; c < pieces; c += 64) {
+    float a[EPP], b[EPP], d[EPP];
+    add_piece<T>(gload16(x + c * EPP), a);
+    add_piece<T>(gload16(xp + c * EPP), b);
+    add_piece<T>(gload16(xn + c * EPP), d);
+#pragma unroll
+    for (int e = 0; e < EPP; ++e) {
+      const double u = a[e], v = b[e], w = d[e];
+      xx += u * u; pp += v * v; nn += w * w; xpd += u * v; xnd += u * w;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    xx += __shfl_xor(xx, o, 64);
+    pp += __shfl_xor(pp, o, 64);
+    nn += __shfl_xor(nn, o, 64);
+    xpd += __shfl_xor(xpd, o, 64);
+    xnd += __shfl_xor(xnd, o, 64);
+  }
+  auto cosv = [](double xy, double aa, double bb) {
+    if (aa <= 0.0 || bb <= 0.0) return 0.0;
+    const double c = xy / (sqrt(aa) * sqrt(bb));
+    return c > 1.0 ? 1.0 : (c < -1.0 ? -1.0 : c);
+  };
+  double sum = 0.0;
+  int n = 0;
+  if (jp >= 0) { sum += cosv(xpd, xx, pp); ++n; }
+  if (jn >= 0) { sum += cosv(xnd, xx, nn); ++n; }
+  const float v = n ? (float)(sum / n) : 0.0f;
+  for (int g = lane; g < dm.Hkv; g += 64) s[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = v;
+}
+
 template <typename T, int D>
 void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, const Workspace& ws, float* s,
                   hipStream_t st) {
@@ -515,12 +588,23 @@ hipError_t launch_lists(const Dims& dm, const LayerDesc* desc, const Workspace& 
   return hipGetLastError();
 }
 
-hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int on_keys, const LayerDesc* desc,
+hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int source, const LayerDesc* desc,
                              const Workspace& ws, float* s, hipStream_t st) {
   if (sim == 1) {  // the all-pairs mode computes the lists inside lists_norms
     hipError_t e = launch_lists(dm, desc, ws, st);
     if (e != hipSuccess) return e;
   }
+  if (source == 2) {  // hidden states (adjacent mode only, checked at create)
+    const dim3 grid((unsigned)((dm.max_tokens + 3) / 4), dm.L);
+    if (dtype == 0)
+      OMNIMEM_LAUNCH(ws, K_ADJ, st, adjacent_cos_hidden<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ws.pos, ws.rank,
+                                                                                       ws.counts, s));
+    else
+      OMNIMEM_LAUNCH(ws, K_ADJ, st, adjacent_cos_hidden<float><<<grid, 256, 0, st>>>(desc, dm, ws.pos, ws.rank,
+                                                                                    ws.counts, s));
+    return hipGetLastError();
+  }
+  const int on_keys = source == 1 ? 1 : 0;
   if (dtype == 0) {
     if (dm.d == 128) launch_typed<uint16_t, 128>(dm, sim, on_keys, desc, ws, s, st);
     else launch_typed<uint16_t, 64>(dm, sim, on_keys, desc, ws, s, st);

@@ -426,6 +426,25 @@ __global__ __launch_bounds__(256) void gather_compact(const LayerDesc* __restric
   }
 }
 
+// Kept rows' hidden states, for layers that give hidden_out (layer-shared
+// selection: the index rows of all heads are equal, head 0's is read):
+// hidden_out[i] = hidden[idx[l][0][i]], one wave per row, 16 bytes a lane.
+template <typename T>
+__global__ __launch_bounds__(256) void gather_hidden(const LayerDesc* __restrict__ layers, Dims dm,
+                                                     const int32_t* __restrict__ idx, const int* __restrict__ eff) {
+  const int l = blockIdx.y;
+  const LayerDesc Ld = layers[l];
+  if (!Ld.hidden_out) return;
+  const int M = eff[2 * l] + eff[2 * l + 1];
+  const int i = (int)blockIdx.x * 4 + wave_id(), lane = threadIdx.x & 63;
+  if (i >= M) return;
+  const int row = idx[(int64_t)l * dm.Hkv * dm.max_tokens + i];
+  constexpr int EPP = 16 / (int)sizeof(T);
+  const T* src = reinterpret_cast<const T*>(Ld.hidden) + (int64_t)row * Ld.hidden_rs;
+  T* dst = reinterpret_cast<T*>(Ld.hidden_out) + (int64_t)i * Ld.hidden_out_rs;
+  for (int c = lane; c < dm.dh / EPP; c += 64) *reinterpret_cast<uint4*>(dst + c * EPP) = gload16(src + c * EPP);
+}
+
 template <typename T, int D>
 void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const int32_t* idx, hipStream_t st) {
   dim3 grid((unsigned)((dm.max_tokens + 63) / 64), dm.Hkv, dm.L);
@@ -434,7 +453,7 @@ void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, c
 
 }  // namespace
 
-hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, const LayerDesc* desc,
+hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, const LayerDesc* desc,
                                  const Workspace& ws, const float* a, const float* s, const int32_t* budgets,
                                  int32_t* idx, hipStream_t st) {
   int32_t* ix = idx ? idx : ws.idx;
@@ -452,6 +471,13 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int sh
   } else {
     if (dm.d == 128) launch_gather<float, 128>(dm, desc, ws, ix, st);
     else launch_gather<float, 64>(dm, desc, ws, ix, st);
+  }
+  if (hidden) {
+    const dim3 grid((unsigned)((dm.max_tokens + 3) / 4), dm.L);
+    if (dtype == 0)
+      OMNIMEM_LAUNCH(ws, K_GATHER_H, st, gather_hidden<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ix, ws.eff));
+    else
+      OMNIMEM_LAUNCH(ws, K_GATHER_H, st, gather_hidden<float><<<grid, 256, 0, st>>>(desc, dm, ix, ws.eff));
   }
   return hipGetLastError();
 }

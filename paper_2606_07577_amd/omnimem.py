@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libomnimem.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_INFEASIBLE, ERR_CAPACITY, ERR_HIP = range(6)
 BF16, F32 = 0, 1
 SIM_MAX, SIM_ADJ = 0, 1
+SRC_VALUES, SRC_KEYS, SRC_HIDDEN = 0, 1, 2
 
 EXPORTED = [
     "omnimem_config_default", "omnimem_create", "omnimem_destroy", "omnimem_last_error",
@@ -40,8 +41,8 @@ class Config(ctypes.Structure):
         ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("lambda_", ctypes.c_float),
         ("ratio_r", ctypes.c_float), ("temperature", ctypes.c_float), ("b_min_frac", ctypes.c_float),
         ("b_max_frac", ctypes.c_float), ("causal", ctypes.c_int32), ("sim", ctypes.c_int32),
-        ("sim_on_keys", ctypes.c_int32), ("shared_selection", ctypes.c_int32), ("max_tokens", ctypes.c_int64),
-        ("max_chunk", ctypes.c_int64),
+        ("sim_source", ctypes.c_int32), ("shared_selection", ctypes.c_int32), ("max_tokens", ctypes.c_int64),
+        ("max_chunk", ctypes.c_int64), ("hidden_dim", ctypes.c_int32),
     ]
 
 
@@ -52,7 +53,8 @@ class Layer(ctypes.Structure):
         ("kv_row_stride", ctypes.c_int64), ("modality", ctypes.c_void_p), ("n_cache", ctypes.c_int64),
         ("n_chunk", ctypes.c_int64), ("sm_scale", ctypes.c_float), ("lse", ctypes.c_void_p),
         ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p), ("out_head_stride", ctypes.c_int64),
-        ("out_row_stride", ctypes.c_int64),
+        ("out_row_stride", ctypes.c_int64), ("hidden", ctypes.c_void_p), ("hidden_row_stride", ctypes.c_int64),
+        ("hidden_out", ctypes.c_void_p), ("hidden_out_row_stride", ctypes.c_int64),
     ]
 
 
@@ -118,11 +120,13 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def make_layer(q, k, v, modality, n_cache, sm_scale=0.0, lse=None, k_out=None, v_out=None):
+def make_layer(q, k, v, modality, n_cache, sm_scale=0.0, lse=None, k_out=None, v_out=None, hidden=None,
+               hidden_out=None):
     """Descriptor of one layer's working set from device tensors.
 
     q [H_q, C, d]; k, v [H_kv, N, d]; modality uint8 [N]; optional lse
-    [H_q, C] fp32; optional k_out, v_out [H_kv, >=N, d] (same strides).
+    [H_q, C] fp32; optional k_out, v_out [H_kv, >=N, d] (same strides);
+    optional hidden [N, d_model] and hidden_out [>=M, d_model].
     """
     if k.stride() != v.stride():
         raise ValueError("k and v must share strides")
@@ -144,6 +148,10 @@ def make_layer(q, k, v, modality, n_cache, sm_scale=0.0, lse=None, k_out=None, v
     if k_out is not None:
         lay.k_out, lay.v_out = _ptr(k_out), _ptr(v_out)
         lay.out_head_stride, lay.out_row_stride = k_out.stride(0), k_out.stride(1)
+    if hidden is not None:
+        lay.hidden, lay.hidden_row_stride = _ptr(hidden), hidden.stride(0)
+    if hidden_out is not None:
+        lay.hidden_out, lay.hidden_out_row_stride = _ptr(hidden_out), hidden_out.stride(0)
     return lay
 
 

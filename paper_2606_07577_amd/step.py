@@ -36,6 +36,10 @@ class DeviceStep:
         self.mod = [torch.from_numpy(np.ascontiguousarray(l["modality"])).to(dev) for l in layers]
         self.k_out = [torch.zeros_like(k) for k in self.k]
         self.v_out = [torch.zeros_like(v) for v in self.v]
+        # hidden states (redundancy source of Eq. 7 as printed), when the layers carry them
+        self.h = [torch.from_numpy(np.ascontiguousarray(l["h"])).to(dev, self.tdtype) if "h" in l else None
+                  for l in layers]
+        self.h_out = [torch.zeros_like(h) if h is not None else None for h in self.h]
         self.sm_scale = [float(l["sm_scale"]) for l in layers]
         shape = (self.n_layers, h_kv, self.max_tokens)
         self.a = torch.zeros(shape, device=dev, dtype=torch.float32)
@@ -51,7 +55,8 @@ class DeviceStep:
 
     def _descs(self):
         return [om.make_layer(self.q[l], self.k[l], self.v[l], self.mod[l], self.n_cache[l],
-                              self.sm_scale[l], self.lse_in[l], self.k_out[l], self.v_out[l])
+                              self.sm_scale[l], self.lse_in[l], self.k_out[l], self.v_out[l],
+                              self.h[l], self.h_out[l])
                 for l in range(self.n_layers)]
 
     def set_lse_inputs(self, lse_list):

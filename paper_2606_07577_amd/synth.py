@@ -41,23 +41,30 @@ def modality_mask(n_cache_v, n_cache_a, n_frames, frame_v, frame_a):
 
 def _plant_near_duplicates(rng, k, v, visual_rows, frac, noise):
     """Make `frac` of the visual rows (never the first) noisy copies of a
-    uniformly chosen earlier visual row, for K and V of every KV head."""
+    uniformly chosen earlier visual row, for K and V of every KV head.
+    Returns the (source, copy) row pairs."""
     n_vis = len(visual_rows)
     n_dup = int(round(frac * n_vis))
+    pairs = []
     if n_dup == 0 or n_vis < 2:
-        return
+        return pairs
     chosen = np.sort(rng.choice(np.arange(1, n_vis), size=min(n_dup, n_vis - 1), replace=False))
     for t in chosen:
         src = visual_rows[rng.integers(0, t)]
         dst = visual_rows[t]
         k[:, dst] = k[:, src] + noise * rng.standard_normal(k[:, dst].shape, dtype=np.float32)
         v[:, dst] = v[:, src] + noise * rng.standard_normal(v[:, dst].shape, dtype=np.float32)
+        pairs.append((int(src), int(dst)))
+    return pairs
 
 
 def make_layer(seed, *, h_q, h_kv, d, n_cache_v, n_cache_a, n_frames, frame_v, frame_a,
                dup_frac=0.0, dup_noise=0.05, head_scale=None, audio_key_std=1.0,
-               sm_scale=None, dtype="bf16", q_std=1.0):
-    """One layer's working set: q [H_q, C, d], k and v [H_kv, N, d], modality [N]."""
+               sm_scale=None, dtype="bf16", q_std=1.0, hidden_dim=0):
+    """One layer's working set: q [H_q, C, d], k and v [H_kv, N, d], modality [N];
+    with hidden_dim, also hidden states h [N, hidden_dim] ~ N(0, 1) in which
+    the near-duplicate rows of K and V are noisy copies too (drawn from a
+    stream of their own, so q, k and v do not depend on hidden_dim)."""
     rng = np.random.default_rng(seed)
     modality = modality_mask(n_cache_v, n_cache_a, n_frames, frame_v, frame_a)
     n = len(modality)
@@ -69,20 +76,30 @@ def make_layer(seed, *, h_q, h_kv, d, n_cache_v, n_cache_a, n_frames, frame_v, f
     audio = modality == AUDIO
     if audio_key_std != 1.0:
         k[:, audio] *= np.float32(audio_key_std)
-    _plant_near_duplicates(rng, k, v, np.flatnonzero(~audio), dup_frac, dup_noise)
+    pairs = _plant_near_duplicates(rng, k, v, np.flatnonzero(~audio), dup_frac, dup_noise)
     if head_scale is not None:
         lo, hi = head_scale
         k *= rng.uniform(lo, hi, size=(h_kv, 1, 1)).astype(np.float32)
         v *= rng.uniform(lo, hi, size=(h_kv, 1, 1)).astype(np.float32)
+    h = None
+    if hidden_dim:
+        hrng = np.random.default_rng([*np.atleast_1d(seed).tolist(), 4093])
+        h = hrng.standard_normal((n, hidden_dim), dtype=np.float32)
+        for src, dst in pairs:
+            h[dst] = h[src] + dup_noise * hrng.standard_normal(hidden_dim, dtype=np.float32)
     if dtype == "bf16":
         q, k, v = round_to_bf16(q), round_to_bf16(k), round_to_bf16(v)
+        h = None if h is None else round_to_bf16(h)
     elif dtype != "f32":
         raise ValueError(dtype)
-    return {
+    out = {
         "q": q, "k": k, "v": v, "modality": modality, "n_cache": n_cache,
         "sm_scale": float(1.0 / math.sqrt(d)) if sm_scale is None else float(sm_scale),
         "dtype": dtype,
     }
+    if h is not None:
+        out["h"] = h
+    return out
 
 
 # The measured and tested workloads.  Chunks are laid out as frames of
@@ -107,6 +124,13 @@ WORKLOADS = {
         n_layers=28, h_q=28, h_kv=4, d=128, n_cache_v=3072, n_cache_a=1024, n_frames=4,
         frame_v=384, frame_a=128, dup_frac=0.30, head_scale=(0.5, 2.0), audio_key_std=1.0,
         temperature=(0.3, 3.0), dtype="bf16", total_budget=28 * 4096, seed=2),
+    "qwen7b-layer-6144-hidden": dict(
+        desc="the 6144-token Qwen-7B-shaped layer with hidden states of width 3584 (Qwen2.5-7B's "
+             "d_model) carrying the same near-duplicates; redundancy from them (Eq. 7 as printed), "
+             "one index set per layer",
+        n_layers=1, h_q=28, h_kv=4, d=128, n_cache_v=3072, n_cache_a=1024, n_frames=4,
+        frame_v=384, frame_a=128, dup_frac=0.30, head_scale=(0.5, 2.0), audio_key_std=1.0,
+        temperature=None, dtype="bf16", total_budget=4096, seed=1, hidden_dim=3584),
     "qwen7b-longcache-40960": dict(
         desc="1 layer, 28 query / 4 KV heads, head_dim 128, bf16, cache 32768 (24576 v, 8192 a) "
              "+ chunk 8192 (6144 v, 2048 a), audio keys 3x smaller norm, 30% near-duplicate "
@@ -140,7 +164,8 @@ def make_workload(name, layers=None, **overrides):
             n_frames=spec["n_frames"], frame_v=spec["frame_v"], frame_a=spec["frame_a"],
             dup_frac=spec["dup_frac"], head_scale=spec["head_scale"],
             audio_key_std=spec["audio_key_std"],
-            sm_scale=1.0 / (taus[l] * math.sqrt(spec["d"])), dtype=spec["dtype"]))
+            sm_scale=1.0 / (taus[l] * math.sqrt(spec["d"])), dtype=spec["dtype"],
+            hidden_dim=spec.get("hidden_dim", 0)))
     return out
 
 

@@ -59,14 +59,14 @@ class Case:
 
 
 def ragged_layers(n_layers=1, d=128, dtype="bf16", seed=100, caches=((200, 77),), frames=(3, 41, 13),
-                  h_q=8, h_kv=2):
+                  h_q=8, h_kv=2, hidden_dim=0):
     out = []
     for l in range(n_layers):
         cv, ca = caches[l % len(caches)]
         out.append(synth.make_layer([seed, l], h_q=h_q, h_kv=h_kv, d=d, n_cache_v=cv, n_cache_a=ca,
                                     n_frames=frames[0], frame_v=frames[1], frame_a=frames[2],
                                     dup_frac=0.3, head_scale=(0.5, 2.0), dtype=dtype,
-                                    sm_scale=1.0 / ((0.5 + l) * math.sqrt(d))))
+                                    sm_scale=1.0 / ((0.5 + l) * math.sqrt(d)), hidden_dim=hidden_dim))
     return out
 
 
@@ -404,6 +404,86 @@ def test_shared_selection_chain_and_one_head_equivalence():
                                   shared.k_out[0].view(torch.int16).cpu().numpy())
     per_head.close()
     shared.close()
+
+
+# ---------------------------------------------------------------------------
+# Redundancy from hidden states (Eq. 7 as printed; reading R23)
+# ---------------------------------------------------------------------------
+
+def _hidden_step(layers, budget, dh):
+    return DeviceStep(layers, budget, sim=omnimem.SIM_ADJ, sim_source=omnimem.SRC_HIDDEN, hidden_dim=dh,
+                      shared_selection=1)
+
+
+@pytest.mark.parametrize("dtype,dh", [("bf16", 3584), ("f32", 200)])
+def test_hidden_state_redundancy(dtype, dh):
+    # One value per token from its hidden state, in every KV head's row.
+    layers = ragged_layers(2, dtype=dtype, seed=114, caches=((200, 77), (90, 31)), hidden_dim=dh)
+    st = _hidden_step(layers, 300, dh)
+    st.redundancy()
+    _sync()
+    for l, lay in enumerate(layers):
+        ref = om.hidden_redundancy(lay["h"].astype(np.float64), lay["modality"], st.h_kv, "adj")
+        P.assert_close_s(st.host("s", l), ref, f"s layer {l}")
+    st.close()
+
+
+def test_hidden_state_step_carries_kept_rows():
+    # The whole step with hidden states: shared kept rows, the hidden states
+    # of exactly those rows compacted bit for bit, K and V too.
+    layers = ragged_layers(2, seed=115, caches=((300, 90), (120, 60)), hidden_dim=1024)
+    st = _hidden_step(layers, 500, 1024)
+    st.run()
+    _sync()
+    budgets = st.budgets.cpu().numpy()
+    for l, lay in enumerate(layers):
+        mod = np.asarray(lay["modality"])
+        mv, ma = (int(x) for x in budgets[l])
+        idx = st.host("idx", l)[:, : mv + ma]
+        s = st.host("s", l)
+        assert (idx == idx[0]).all() and (s == s[0]).all()
+        a64 = st.host("a", l).astype(np.float64)
+        P.check_topk_property(idx[0], a64.sum(axis=0), s[0].astype(np.float64), mod, mv, ma)
+        h_out = st.h_out[l][: mv + ma].view(torch.int16).cpu().numpy()
+        h_in = st.h[l].view(torch.int16).cpu().numpy()
+        np.testing.assert_array_equal(h_out, h_in[idx[0]])
+        k_out = st.k_out[l].float().cpu().numpy()
+        for g in range(st.h_kv):
+            np.testing.assert_array_equal(k_out[g, : mv + ma], lay["k"][g, idx[0]])
+    st.close()
+
+
+def test_hidden_state_workload_full_size():
+    layers = synth.make_workload("qwen7b-layer-6144-hidden")
+    st = _hidden_step(layers, 4096, 3584)
+    st.run()
+    _sync()
+    lay = layers[0]
+    ref = om.hidden_redundancy(lay["h"].astype(np.float64), lay["modality"], st.h_kv, "adj")
+    P.assert_close_s(st.host("s", 0), ref, "s")
+    mv, ma = (int(x) for x in st.budgets.cpu().numpy()[0])
+    assert mv + ma == 4096
+    idx = st.host("idx", 0)[:, :4096]
+    np.testing.assert_array_equal(st.h_out[0][:4096].view(torch.int16).cpu().numpy(),
+                                  st.h[0].view(torch.int16).cpu().numpy()[idx[0]])
+    st.close()
+
+
+def test_hidden_state_errors():
+    layers = ragged_layers(seed=116, hidden_dim=512)
+    with pytest.raises(omnimem.OmnimemError) as e:   # all-pairs form on hidden states: not built
+        DeviceStep(layers, 300, sim=omnimem.SIM_MAX, sim_source=omnimem.SRC_HIDDEN, hidden_dim=512)
+    assert e.value.status == omnimem.ERR_UNSUPPORTED
+    with pytest.raises(omnimem.OmnimemError) as e:
+        DeviceStep(layers, 300, sim=omnimem.SIM_ADJ, sim_source=omnimem.SRC_HIDDEN, hidden_dim=100)  # 200 B rows
+    assert e.value.status == omnimem.ERR_INVALID_ARG
+    st = DeviceStep(layers, 300, sim=omnimem.SIM_ADJ, sim_source=omnimem.SRC_HIDDEN, hidden_dim=512)
+    st.redundancy()
+    st.allocate()
+    with pytest.raises(omnimem.OmnimemError) as e:   # kept hidden states need one index set per layer
+        st.select_compact()
+    assert e.value.status == omnimem.ERR_INVALID_ARG
+    st.close()
 
 
 # ---------------------------------------------------------------------------
