@@ -78,6 +78,7 @@ __device__ inline double norm_entropy(double sum, double xlogx, double count) {
 
 constexpr int kMaxLayers = 1024;
 constexpr int kMaxSums = 2048;   // L * H_kv * 8 partial sums kept in LDS
+constexpr int kAllocThreads = 1024;  // the per-head entropies take fp64 logs: all the lanes of a CU
 
 enum AllocMode : int {
   kOnline = 0,       // Eq. (14) from this step's statistics, then the split
@@ -89,7 +90,7 @@ enum AllocMode : int {
 // calib: [L] calibration sums; calib_first: a kCalibAdd step that starts
 // them (assigns instead of adding); steps: their count (kCalibFinish).
 // layer_budgets: read in kFixed, written in kCalibFinish.
-__global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict__ layers, Dims dm,
+__global__ __launch_bounds__(kAllocThreads) void avba_allocate(const LayerDesc* __restrict__ layers, Dims dm,
                                                      const double* __restrict__ part, int64_t total,
                                                      float ratio_r, float temperature, float bmin_frac,
                                                      float bmax_frac, int mode, double* __restrict__ calib,
@@ -290,6 +291,14 @@ __global__ __launch_bounds__(256) void avba_allocate(const LayerDesc* __restrict
   }
 }
 
+// Partial sums over a and s for the allocation kernel.
+void launch_sums(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a, const float* s,
+                 hipStream_t st) {
+  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st,
+                 avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
+                                                                                            ws.stat_part));
+}
+
 }  // namespace
 
 int allocate_part_chunks(const Dims& dm) { return part_chunks(dm); }
@@ -297,44 +306,42 @@ int allocate_part_chunks(const Dims& dm) { return part_chunks(dm); }
 hipError_t launch_allocate(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
                            const float* s, int64_t total, float ratio_r, float temperature, float bmin_frac,
                            float bmax_frac, int32_t* budgets, float* stats, hipStream_t st) {
-  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st,
-                 avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
-                                                                                            ws.stat_part));
-  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, total, ratio_r,
-                                   temperature, bmin_frac, bmax_frac, kOnline, nullptr, 0, 0.0, nullptr,
-                                   budgets, stats));
+  launch_sums(dm, desc, ws, a, s, st);
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st,
+                 avba_allocate<<<1, kAllocThreads, 0, st>>>(desc, dm, ws.stat_part, total, ratio_r, temperature,
+                                                            bmin_frac, bmax_frac, kOnline, nullptr, 0, 0.0, nullptr,
+                                                            budgets, stats));
   return hipGetLastError();
 }
 
 hipError_t launch_calibrate(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
                             const float* s, float ratio_r, bool first, float* stats, hipStream_t st) {
-  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st,
-                 avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
-                                                                                            ws.stat_part));
-  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, 0, ratio_r, 1.0f,
-                                   0.0f, 0.0f, kCalibAdd, ws.calib, first ? 1 : 0, 0.0, nullptr, nullptr,
-                                   stats));
+  launch_sums(dm, desc, ws, a, s, st);
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st,
+                 avba_allocate<<<1, kAllocThreads, 0, st>>>(desc, dm, ws.stat_part, 0, ratio_r, 1.0f, 0.0f,
+                                                            0.0f, kCalibAdd, ws.calib, first ? 1 : 0, 0.0, nullptr,
+                                                            nullptr, stats));
   return hipGetLastError();
 }
 
 hipError_t launch_calibration_budgets(const Dims& dm, const Workspace& ws, int64_t total, float temperature,
                                       float bmin_frac, float bmax_frac, int steps, int32_t* layer_budgets,
                                       hipStream_t st) {
-  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(nullptr, dm, nullptr, total, 1.0f,
-                                   temperature, bmin_frac, bmax_frac, kCalibFinish, ws.calib, 0,
-                                   (double)steps, layer_budgets, nullptr, nullptr));
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st,
+                 avba_allocate<<<1, kAllocThreads, 0, st>>>(nullptr, dm, nullptr, total, 1.0f,
+                                                            temperature, bmin_frac, bmax_frac, kCalibFinish, ws.calib,
+                                                            0, (double)steps, layer_budgets, nullptr, nullptr));
   return hipGetLastError();
 }
 
 hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
                                  const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
                                  float* stats, hipStream_t st) {
-  OMNIMEM_LAUNCH(ws, K_AVBA_PART, st,
-                 avba_partials<<<dim3(part_chunks(dm), dm.Hkv, dm.L), kPartThreads, 0, st>>>(desc, dm, a, s,
-                                                                                            ws.stat_part));
-  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st, avba_allocate<<<1, 256, 0, st>>>(desc, dm, ws.stat_part, 0, ratio_r, 1.0f,
-                                   0.0f, 0.0f, kFixed, nullptr, 0, 0.0, const_cast<int32_t*>(layer_budgets),
-                                   budgets, stats));
+  launch_sums(dm, desc, ws, a, s, st);
+  OMNIMEM_LAUNCH(ws, K_AVBA_ALLOC, st,
+                 avba_allocate<<<1, kAllocThreads, 0, st>>>(desc, dm, ws.stat_part, 0, ratio_r, 1.0f, 0.0f,
+                                                            0.0f, kFixed, nullptr, 0, 0.0,
+                                                            const_cast<int32_t*>(layer_budgets), budgets, stats));
   return hipGetLastError();
 }
 
