@@ -67,6 +67,9 @@ def parse_args():
                    help="fix the layer budgets in advance from a calibration (end of Sec. 3.2): static "
                         "workloads calibrate on their own step, streams on their warmup chunks; the timed "
                         "steps only split the fixed budgets")
+    p.add_argument("--sim", choices=["max", "adj"], default=None,
+                   help="redundancy form: all-pairs maximum (default on values) or the adjacent form of Eq. 7 "
+                        "(default on hidden states)")
     p.add_argument("--shared-selection", action="store_true",
                    help="keep one index set per layer (Eqs. 4-5), ranked by the importance summed and the "
                         "redundancy averaged over the KV heads")
@@ -105,17 +108,21 @@ def layer_work(h_q, c, n_cache, h_kv, n, d, elt, k_v, k_a, m, causal=True):
 def work_table(score, gram, topk, compact):
     """Per-launch algorithmic units of each counted kernel."""
     return {"lse_pass": ("mfma", score), "colsum_pass": ("mfma", score), "gram_pass": ("mfma", gram),
+            "gram_wide": ("mfma", gram),
             "gather_compact": ("hbm", compact), "psi_topk": ("hbm", topk)}
 
 
-def static_work(layers, budgets):
+def static_work(layers, budgets, hidden_dim=0):
     tot = [0, 0, 0, 0]
     for lay, (mv, ma) in zip(layers, budgets):
         h_q, c, d = lay["q"].shape
         h_kv, n, _ = lay["k"].shape
         mod = lay["modality"]
+        k_v, k_a = int((mod == 0).sum()), int((mod == 1).sum())
         w = layer_work(h_q, c, lay["n_cache"], h_kv, n, d, 2 if lay["dtype"] == "bf16" else 4,
-                       int((mod == 0).sum()), int((mod == 1).sum()), int(mv) + int(ma))
+                       k_v, k_a, int(mv) + int(ma))
+        if hidden_dim:  # the Gram on the layer's hidden states: one per layer, d_model wide
+            w = (w[0], (k_v * (k_v - 1) + k_a * (k_a - 1)) * hidden_dim, w[2], w[3])
         tot = [x + y for x, y in zip(tot, w)]
     return work_table(*tot)
 
@@ -155,8 +162,11 @@ def run_static(args, torch):
         # redundancy from the hidden states (Eq. 7 as printed, adjacent form); their kept rows are
         # carried with the cache, which takes one index set per layer
         from paper_2606_07577_amd import omnimem as om
-        options.update(sim=om.SIM_ADJ, sim_source=om.SRC_HIDDEN, hidden_dim=spec["hidden_dim"],
-                       shared_selection=1)
+        options.update(sim=om.SIM_MAX if args.sim == "max" else om.SIM_ADJ, sim_source=om.SRC_HIDDEN,
+                       hidden_dim=spec["hidden_dim"], shared_selection=1)
+    elif args.sim == "adj":
+        from paper_2606_07577_amd import omnimem as om
+        options.update(sim=om.SIM_ADJ)
     step = DeviceStep(layers, spec["total_budget"], **options)
     stream = torch.cuda.current_stream()
     if args.lse_given:
@@ -198,15 +208,15 @@ def run_static(args, torch):
     torch.cuda.synchronize()
     kernels = step.ctx.omnimem_profile_report()
     step.ctx.omnimem_profile(False)
-    work = static_work(layers, step.budgets.cpu().numpy())
+    work = static_work(layers, step.budgets.cpu().numpy(), spec.get("hidden_dim", 0))
     config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "cache": spec["n_cache_v"] + spec["n_cache_a"],
               "chunk": spec["n_frames"] * (spec["frame_v"] + spec["frame_a"]), "budget": spec["total_budget"],
               "lse": "input" if args.lse_given else "computed",
               "layer_budgets": "offline" if args.offline_budgets else "per step",
               "selection": "per layer" if options["shared_selection"] else "per KV head",
-              "redundancy": (f"hidden states ({spec['hidden_dim']}), adjacent" if spec.get("hidden_dim")
-                             else "values, all pairs")}
+              "redundancy": ("hidden states (%d), " % spec["hidden_dim"] if spec.get("hidden_dim") else "values, ")
+                            + ("all pairs" if options.get("sim", 0) == 0 else "adjacent")}
     baseline = None
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
@@ -344,7 +354,8 @@ def main():
         return round(u / t / scale / peak_units, 4) if t > 0 else None
 
     fractions = {
-        "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_pass"], PEAK_MFMA_TFLOPS[dtype], 1e12),
+        "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_pass", "gram_wide"],
+                                           PEAK_MFMA_TFLOPS[dtype], 1e12),
         "hbm_frac_topk_compact": stage_frac(["psi_topk", "gather_compact"], PEAK_HBM_GBS, 1e9),
     }
     out = {

@@ -51,7 +51,7 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 
 static const char* kKernelNames[K_COUNT] = {
     "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact",
-    "gather_hidden"};
+    "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -312,9 +312,9 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
     if (c.hidden_dim < 1 || c.hidden_dim > 65536 || (c.hidden_dim * esz) % 16)
       return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "hidden_dim %d: need 1..65536 and rows of whole 16-byte units",
                   c.hidden_dim);
-    if (c.sim != OMNIMEM_SIM_ADJ)
-      return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "hidden states are supported with SIM_ADJ (Eq. 7 as printed) "
-                  "only; the all-pairs maximum on them is not built");
+    if (c.sim == OMNIMEM_SIM_MAX && c.hidden_dim % 64)
+      return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "hidden_dim %d: the all-pairs maximum on hidden states takes "
+                  "multiples of 64", c.hidden_dim);
   }
   if (!std::isfinite(c.lambda) || c.lambda < 0.0f || !(c.ratio_r > 0.0f) || !(c.temperature > 0.0f) ||
       !(c.b_min_frac >= 0.0f) || !(c.b_max_frac >= c.b_min_frac) || !std::isfinite(c.b_max_frac))

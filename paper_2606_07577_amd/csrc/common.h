@@ -110,6 +110,9 @@ __device__ inline uint4 gload16(const void* p) {
 
 // Index of the calling wavefront in its workgroup, as a scalar.
 __device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+// A value that is the same in every lane (read from LDS, say), kept in a
+// scalar register.
+__device__ inline int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // ---------------------------------------------------------------------------
 // MFMA operand traits.  A 32x32 output tile D[M][N] += A[M][k] B[k][N] is
@@ -208,7 +211,7 @@ constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
 // ---------------------------------------------------------------------------
 enum KernelId {
   K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
-  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_COUNT
+  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_COUNT
 };
 struct Profiler;
 void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);

@@ -559,6 +559,235 @@ __global__ __launch_bounds__(256) void adjacent_cos_hidden(const LayerDesc* __re
   for (int g = lane; g < dm.Hkv; g += 64) s[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = v;
 }
 
+// --- all-pairs maximum on hidden states (the R6 reading of Eq. 7 on them) ----
+// d_model does not fit the register-resident operand of gram_pass, so both
+// operands stream through LDS.  Work item: a pair (I <= J) of 128-row blocks
+// of one segment (layer, modality), rows gathered through the segment's row
+// list; persistent workgroups take the pairs of all segments round-robin.
+// The d axis goes by chunks of 64 (four MFMA k-steps), DMA-copied into two
+// LDS stages (the next chunk lands while the current one is used).  Each of
+// the four waves owns a 64 x 64 quarter of the 128 x 128 block.  After the
+// last chunk the products become cosines (inverse norms from LDS; a row's
+// pair with itself and rows past the segment masked as NaN), and both the
+// block rows' maxima (over the block's columns: halving exchanges across the
+// lanes) and the columns' maxima (in-lane) are merged, first in LDS across
+// waves, then into the rows' best values by atomicMax: each pair is
+// computed once.
+constexpr int kWideBlock = 128;
+constexpr int kWideChunk = 64;  // d elements per LDS stage row
+
+__device__ inline float swz_xor(float v, int m) {
+  // ds_swizzle bit mode (and-mask 0x1F, xor-mask m): within groups of 32 lanes
+  switch (m) {
+    case 16: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1F | (16 << 10)));
+    case 8: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1F | (8 << 10)));
+    case 4: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1F | (4 << 10)));
+    case 2: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1F | (2 << 10)));
+    default: return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1F | (1 << 10)));
+  }
+}
+// Maximum of w[r] over the 32 lanes of each half-wave, for every r: after
+// halving exchanges (xor 16, 8, 4, 2, then 1) w[0] of lane k holds the
+// maximum for r = (k >> 1) & 15, in lanes k and k ^ 1 alike.
+__device__ inline void half_wave_max16(float (&w)[16], int lane) {
+#pragma unroll
+  for (int m = 16, n = 16; m >= 2; m >>= 1, n >>= 1) {
+    const bool hi = (lane & m) != 0;
+#pragma unroll
+    for (int i = 0; i < n / 2; ++i) {
+      const float send = hi ? w[i] : w[i + n / 2];
+      const float keep = hi ? w[i + n / 2] : w[i];
+      w[i] = fmaxf(keep, swz_xor(send, m));
+    }
+  }
+  w[0] = fmaxf(w[0], swz_xor(w[0], 1));
+}
+
+// inv[l][j] = 1 / ||h_j|| (fp64 sum of squares; 0 for a zero row) and best
+// reset, one wave per working-set row.
+template <typename T>
+__global__ __launch_bounds__(256) void hidden_norms(const LayerDesc* __restrict__ layers, Dims dm,
+                                                    float* __restrict__ inv, int* __restrict__ best) {
+  const int l = blockIdx.y;
+  const LayerDesc Ld = layers[l];
+  const int j = (int)blockIdx.x * 4 + wave_id(), lane = threadIdx.x & 63;
+  if (j >= Ld.n) return;
+  constexpr int EPP = 16 / (int)sizeof(T);
+  const T* x = reinterpret_cast<const T*>(Ld.hidden) + (int64_t)j * Ld.hidden_rs;
+  double ss = 0.0;
+  for (int c = lane; c < dm.dh / EPP; c += 64) {
+    float a[EPP];
+    add_piece<T>(gload16(x + c * EPP), a);
+#pragma unroll
+    for (int e = 0; e < EPP; ++e) ss += (double)a[e] * a[e];
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  if (lane == 0) {
+    inv[(int64_t)l * dm.max_tokens + j] = ss > 0.0 ? (float)(1.0 / sqrt(ss)) : 0.0f;
+    best[(int64_t)l * dm.max_tokens + j] = kNoPartner;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256, 2) void gram_wide(const LayerDesc* __restrict__ layers, Dims dm,
+                                                    const int* __restrict__ pos, const int* __restrict__ counts,
+                                                    const float* __restrict__ inv, int* __restrict__ best) {
+  using M = Mfma<T>;
+  using Tl = SwzTile<T, kWideChunk>;  // one stage: 64 rows of a 64-element chunk
+  constexpr int KS = kWideChunk / M::KSTEP;
+  constexpr int EPC = 16 / (int)sizeof(T);
+  constexpr int CPR = kWideChunk / EPC;  // 16-byte pieces per stage row
+  constexpr int kMaxSegs = 2048;
+  __shared__ __attribute__((aligned(16))) T stage[2][4][Tl::ELEMS];  // [buffer][A lo, A hi, B lo, B hi]
+  __shared__ int seg_first[kMaxSegs + 1];  // first pair of each segment (pair counts fit 31 bits)
+  __shared__ float inv_a[kWideBlock], inv_b[kWideBlock];
+  __shared__ int row_a[kWideBlock], row_b[kWideBlock];
+  __shared__ int mx_a[kWideBlock], mx_b[kWideBlock];
+  const int S = 2 * dm.L;
+  for (int q = threadIdx.x; q < S; q += blockDim.x) {
+    const int nb = (counts[q] + kWideBlock - 1) / kWideBlock;
+    seg_first[q + 1] = nb * (nb + 1) / 2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    seg_first[0] = 0;
+    for (int q = 0; q < S; ++q) seg_first[q + 1] += seg_first[q];
+  }
+  __syncthreads();
+  const int total = uniform(seg_first[S]);
+  const int w = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
+  const int wr = w >> 1, wc = w & 1;  // the wave's 64 block rows (A) and 64 block columns (B)
+  const int nchunks = dm.dh / kWideChunk;
+  for (int p = blockIdx.x; p < total; p += gridDim.x) {
+    // segment and block pair of p
+    int q = 0;
+    for (int lo = 0, hi = S - 1; lo < hi;) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (uniform(seg_first[mid]) <= p) lo = mid; else hi = mid - 1;
+      q = lo;
+    }
+    const int l = q >> 1;
+    const int K = counts[q];
+    const int nb = (K + kWideBlock - 1) / kWideBlock;
+    int r = p - uniform(seg_first[q]);
+    int bi = 0;
+    while (r >= nb - bi) { r -= nb - bi; ++bi; }
+    const int bj = bi + r;
+    const LayerDesc Ld = layers[l];
+    const int* P = pos + (int64_t)q * dm.max_tokens;
+    __syncthreads();  // every wave is done with the previous pair's LDS
+    for (int t = threadIdx.x; t < 2 * kWideBlock; t += blockDim.x) {
+      const int side = t / kWideBlock, k = t % kWideBlock;
+      const int m = (side ? bj : bi) * kWideBlock + k;
+      const int row = P[min(m, K - 1)];
+      const float iv = m < K ? inv[(int64_t)l * dm.max_tokens + row] : __builtin_nanf("");
+      if (side) { row_b[k] = row; inv_b[k] = iv; mx_b[k] = kNoPartner; }
+      else { row_a[k] = row; inv_a[k] = iv; mx_a[k] = kNoPartner; }
+    }
+    __syncthreads();
+    // this thread's DMA pieces: 16 per chunk (4 tiles x 64 rows x CPR pieces / 256)
+    constexpr int kPieces = 4 * kScoreTile * CPR / 256;
+    const T* H = reinterpret_cast<const T*>(Ld.hidden);
+    const T* src[kPieces];
+#pragma unroll
+    for (int u = 0; u < kPieces; ++u) {
+      const int J = w * kPieces + u;             // DMA instruction of the workgroup
+      const int tile = J / (kScoreTile * CPR / 64), slot = (J % (kScoreTile * CPR / 64)) * 64 + lane;
+      const int rr = slot / CPR, c = (slot % CPR) ^ (rr & (CPR - 1));
+      const int k = (tile & 1) * kScoreTile + rr;
+      const int row = (tile < 2) ? row_a[k] : row_b[k];
+      src[u] = H + (int64_t)row * Ld.hidden_rs + c * EPC;
+    }
+    auto dma_chunk = [&](int ch, int buf) {
+#pragma unroll
+      for (int u = 0; u < kPieces; ++u) {
+        const int J = w * kPieces + u;
+        const int tile = J / (kScoreTile * CPR / 64), jt = J % (kScoreTile * CPR / 64);
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(src[u] + ch * kWideChunk),
+                                         (__attribute__((address_space(3))) void*)(&stage[buf][tile][jt * 64 * EPC]),
+                                         16, 0, 0);
+      }
+    };
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = floatx16{};
+    dma_chunk(0, 0);
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int buf = ch & 1;
+      dma_wait();
+      __syncthreads();  // chunk ch landed; every wave is done with the other stage
+      if (ch + 1 < nchunks) dma_chunk(ch + 1, buf ^ 1);
+      const T* A = stage[buf][wr];      // the wave's 64 A rows: tile wr (rows wr*64 ..)
+      const T* B = stage[buf][2 + wc];  // its 64 B rows
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        typename M::frag fa[2], fb[2];
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          fa[x] = Tl::template frag<M>(A, x * 32 + (lane & 31), ks, half);
+          fb[x] = Tl::template frag<M>(B, x * 32 + (lane & 31), ks, half);
+        }
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = M::mma(fa[rb], fb[cb], acc[rb][cb]);
+      }
+    }
+    // cosines; row (A) maxima across the lanes, column (B) maxima in-lane
+    float cmax[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      float wv[16];
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) wv[rr] = -INFINITY;
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+        const int jb = wc * 64 + cb * 32 + (lane & 31);  // block column
+        const float ib = inv_b[jb];
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int ia_k = wr * 64 + rb * 32 + acc_row(rr, lane);  // block row
+          float c = acc[rb][cb][rr] * inv_a[ia_k] * ib;
+          if (bi == bj && ia_k == jb) c = __builtin_nanf("");
+          wv[rr] = fmaxf(wv[rr], c);
+          cmax[cb] = fmaxf(cmax[cb], c);
+        }
+      }
+      half_wave_max16(wv, lane);
+      const int rr = (lane >> 1) & 15;
+      const int ia_k = wr * 64 + rb * 32 + acc_row(rr, lane);
+      if ((lane & 1) == 0 && wv[0] > -INFINITY) atomicMax(&mx_a[ia_k], ord_f32(fminf(1.0f, fmaxf(-1.0f, wv[0]))));
+    }
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      const float m = fmaxf(cmax[cb], __shfl_xor(cmax[cb], 32, 64));
+      const int jb = wc * 64 + cb * 32 + (lane & 31);
+      if (half == 0 && m > -INFINITY) atomicMax(&mx_b[jb], ord_f32(fminf(1.0f, fmaxf(-1.0f, m))));
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < 2 * kWideBlock; t += blockDim.x) {
+      const int side = t / kWideBlock, k = t % kWideBlock;
+      const int m = (side ? bj : bi) * kWideBlock + k;
+      const int v = side ? mx_b[k] : mx_a[k];
+      if (m < K && v != kNoPartner) atomicMax(best + (int64_t)l * dm.max_tokens + (side ? row_b[k] : row_a[k]), v);
+    }
+  }
+}
+
+// s[l][g][j] of every KV head from the hidden states' maxima.
+__global__ void hidden_finish(const LayerDesc* __restrict__ layers, Dims dm, const int* __restrict__ best,
+                              float* __restrict__ s) {
+  const int l = blockIdx.y;
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= layers[l].n) return;
+  const int b = best[(int64_t)l * dm.max_tokens + j];
+  const float v = b == kNoPartner ? 0.0f : fminf(1.0f, fmaxf(-1.0f, unord_f32(b)));
+  for (int g = 0; g < dm.Hkv; ++g) s[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = v;
+}
+
 template <typename T, int D>
 void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, const Workspace& ws, float* s,
                   hipStream_t st) {
@@ -594,13 +823,30 @@ hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int source, con
     hipError_t e = launch_lists(dm, desc, ws, st);
     if (e != hipSuccess) return e;
   }
-  if (source == 2) {  // hidden states (adjacent mode only, checked at create)
+  if (source == 2 && sim == 0) {  // hidden states, all pairs
+    hipError_t e = launch_lists(dm, desc, ws, st);
+    if (e != hipSuccess) return e;
+    const dim3 grid((unsigned)((dm.max_tokens + 3) / 4), dm.L);
+    const dim3 gtok((unsigned)((dm.max_tokens + 255) / 256), dm.L);
+    if (dtype == 0) {
+      OMNIMEM_LAUNCH(ws, K_NORMS_H, st, hidden_norms<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ws.inv_norm, ws.best));
+      OMNIMEM_LAUNCH(ws, K_GRAM_H, st, gram_wide<uint16_t><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.pos, ws.counts,
+                                                                                       ws.inv_norm, ws.best));
+    } else {
+      OMNIMEM_LAUNCH(ws, K_NORMS_H, st, hidden_norms<float><<<grid, 256, 0, st>>>(desc, dm, ws.inv_norm, ws.best));
+      OMNIMEM_LAUNCH(ws, K_GRAM_H, st, gram_wide<float><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.pos, ws.counts,
+                                                                                    ws.inv_norm, ws.best));
+    }
+    OMNIMEM_LAUNCH(ws, K_FINISH_H, st, hidden_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.best, s));
+    return hipGetLastError();
+  }
+  if (source == 2) {  // hidden states, adjacent
     const dim3 grid((unsigned)((dm.max_tokens + 3) / 4), dm.L);
     if (dtype == 0)
-      OMNIMEM_LAUNCH(ws, K_ADJ, st, adjacent_cos_hidden<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ws.pos, ws.rank,
+      OMNIMEM_LAUNCH(ws, K_ADJ_H, st, adjacent_cos_hidden<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ws.pos, ws.rank,
                                                                                        ws.counts, s));
     else
-      OMNIMEM_LAUNCH(ws, K_ADJ, st, adjacent_cos_hidden<float><<<grid, 256, 0, st>>>(desc, dm, ws.pos, ws.rank,
+      OMNIMEM_LAUNCH(ws, K_ADJ_H, st, adjacent_cos_hidden<float><<<grid, 256, 0, st>>>(desc, dm, ws.pos, ws.rank,
                                                                                     ws.counts, s));
     return hipGetLastError();
   }

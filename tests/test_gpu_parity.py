@@ -410,20 +410,22 @@ def test_shared_selection_chain_and_one_head_equivalence():
 # Redundancy from hidden states (Eq. 7 as printed; reading R23)
 # ---------------------------------------------------------------------------
 
-def _hidden_step(layers, budget, dh):
-    return DeviceStep(layers, budget, sim=omnimem.SIM_ADJ, sim_source=omnimem.SRC_HIDDEN, hidden_dim=dh,
-                      shared_selection=1)
+def _hidden_step(layers, budget, dh, sim=omnimem.SIM_ADJ):
+    return DeviceStep(layers, budget, sim=sim, sim_source=omnimem.SRC_HIDDEN, hidden_dim=dh, shared_selection=1)
 
 
-@pytest.mark.parametrize("dtype,dh", [("bf16", 3584), ("f32", 200)])
-def test_hidden_state_redundancy(dtype, dh):
-    # One value per token from its hidden state, in every KV head's row.
+@pytest.mark.parametrize("dtype,dh,mode", [("bf16", 3584, "adj"), ("f32", 200, "adj"),
+                                           ("bf16", 3584, "max"), ("f32", 192, "max")])
+def test_hidden_state_redundancy(dtype, dh, mode):
+    # One value per token from its hidden state, in every KV head's row;
+    # 'max' spans several 128-row blocks per segment (pairs on and off the
+    # diagonal, a ragged last block).
     layers = ragged_layers(2, dtype=dtype, seed=114, caches=((200, 77), (90, 31)), hidden_dim=dh)
-    st = _hidden_step(layers, 300, dh)
+    st = _hidden_step(layers, 300, dh, omnimem.SIM_ADJ if mode == "adj" else omnimem.SIM_MAX)
     st.redundancy()
     _sync()
     for l, lay in enumerate(layers):
-        ref = om.hidden_redundancy(lay["h"].astype(np.float64), lay["modality"], st.h_kv, "adj")
+        ref = om.hidden_redundancy(lay["h"].astype(np.float64), lay["modality"], st.h_kv, mode)
         P.assert_close_s(st.host("s", l), ref, f"s layer {l}")
     st.close()
 
@@ -453,13 +455,14 @@ def test_hidden_state_step_carries_kept_rows():
     st.close()
 
 
-def test_hidden_state_workload_full_size():
+@pytest.mark.parametrize("mode", ["adj", "max"])
+def test_hidden_state_workload_full_size(mode):
     layers = synth.make_workload("qwen7b-layer-6144-hidden")
-    st = _hidden_step(layers, 4096, 3584)
+    st = _hidden_step(layers, 4096, 3584, omnimem.SIM_ADJ if mode == "adj" else omnimem.SIM_MAX)
     st.run()
     _sync()
     lay = layers[0]
-    ref = om.hidden_redundancy(lay["h"].astype(np.float64), lay["modality"], st.h_kv, "adj")
+    ref = om.hidden_redundancy(lay["h"].astype(np.float64), lay["modality"], st.h_kv, mode)
     P.assert_close_s(st.host("s", 0), ref, "s")
     mv, ma = (int(x) for x in st.budgets.cpu().numpy()[0])
     assert mv + ma == 4096
@@ -471,8 +474,8 @@ def test_hidden_state_workload_full_size():
 
 def test_hidden_state_errors():
     layers = ragged_layers(seed=116, hidden_dim=512)
-    with pytest.raises(omnimem.OmnimemError) as e:   # all-pairs form on hidden states: not built
-        DeviceStep(layers, 300, sim=omnimem.SIM_MAX, sim_source=omnimem.SRC_HIDDEN, hidden_dim=512)
+    with pytest.raises(omnimem.OmnimemError) as e:   # all pairs on hidden states: d_model in multiples of 64
+        DeviceStep(layers, 300, sim=omnimem.SIM_MAX, sim_source=omnimem.SRC_HIDDEN, hidden_dim=520)
     assert e.value.status == omnimem.ERR_UNSUPPORTED
     with pytest.raises(omnimem.OmnimemError) as e:
         DeviceStep(layers, 300, sim=omnimem.SIM_ADJ, sim_source=omnimem.SRC_HIDDEN, hidden_dim=100)  # 200 B rows
