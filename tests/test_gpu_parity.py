@@ -430,6 +430,22 @@ def test_hidden_state_redundancy(dtype, dh, mode):
     st.close()
 
 
+@pytest.mark.parametrize("mode", ["adj", "max"])
+def test_hidden_state_small_segments(mode):
+    # A visual segment of 129 rows (a last block of one row) and a lone
+    # audio row (no partner: s = 0), next to a layer of two rows per modality.
+    layers = (ragged_layers(1, seed=117, caches=((128, 1),), frames=(1, 1, 0), hidden_dim=256)
+              + ragged_layers(1, seed=118, caches=((1, 1),), frames=(1, 1, 1), hidden_dim=256))
+    st = _hidden_step(layers, 100, 256, omnimem.SIM_ADJ if mode == "adj" else omnimem.SIM_MAX)
+    st.redundancy()
+    _sync()
+    for l, lay in enumerate(layers):
+        ref = om.hidden_redundancy(lay["h"].astype(np.float64), lay["modality"], st.h_kv, mode)
+        P.assert_close_s(st.host("s", l), ref, f"s layer {l}")
+    assert (st.host("s", 0)[:, np.asarray(layers[0]["modality"]) == 1] == 0).all()
+    st.close()
+
+
 def test_hidden_state_step_carries_kept_rows():
     # The whole step with hidden states: shared kept rows, the hidden states
     # of exactly those rows compacted bit for bit, K and V too.
