@@ -73,6 +73,9 @@ def parse_args():
     p.add_argument("--shared-selection", action="store_true",
                    help="keep one index set per layer (Eqs. 4-5), ranked by the importance summed and the "
                         "redundancy averaged over the KV heads")
+    p.add_argument("--no-graph", dest="graph", action="store_false",
+                   help="time the four calls launched on the stream instead of replays of one HIP graph of "
+                        "the whole step")
     p.add_argument("--lse-given", action="store_true",
                    help="take each layer's log-sum-exp as an input, as the model's chunk prefill attention "
                         "produces it (Eq. 1): the step then runs without the LSE pass")
@@ -189,13 +192,40 @@ def run_static(args, torch):
         step.run(stream)
     torch.cuda.synchronize()
 
+    graph, launch = None, "stream"
+    if args.graph:
+        # The step's layer table is uploaded by the warmup: the captured calls
+        # launch kernels only.  A capture that fails leaves the stream mode.
+        try:
+            graph_stream = torch.cuda.Stream()
+            graph_stream.wait_stream(stream)
+            with torch.cuda.stream(graph_stream):
+                step.run(graph_stream)
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=graph_stream):
+                step.run(graph_stream)
+            torch.cuda.synchronize()
+            with torch.cuda.stream(graph_stream):
+                graph.replay()
+            torch.cuda.synchronize()
+            stream, launch = graph_stream, "graph replay"
+        except Exception as e:  # noqa: BLE001 - report and measure the stream launches instead
+            print(f"[bench] graph capture failed ({e}); timing stream launches", file=sys.stderr, flush=True)
+            graph, launch = None, "stream (graph capture failed)"
+            torch.cuda.synchronize()
+
     # Timed region: K whole steps, nothing else.
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    start.record(stream)
-    for _ in range(args.steps):
-        step.run(stream)
-    stop.record(stream)
+    with torch.cuda.stream(stream):  # graph replays launch on the current stream
+        start.record(stream)
+        for _ in range(args.steps):
+            if graph is not None:
+                graph.replay()
+            else:
+                step.run(stream)
+        stop.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
     tokens = sum(int(l["k"].shape[1]) for l in layers)
@@ -215,6 +245,7 @@ def run_static(args, torch):
               "lse": "input" if args.lse_given else "computed",
               "layer_budgets": "offline" if args.offline_budgets else "per step",
               "selection": "per layer" if options["shared_selection"] else "per KV head",
+              "launch": launch,
               "redundancy": ("hidden states (%d), " % spec["hidden_dim"] if spec.get("hidden_dim") else "values, ")
                             + ("all pairs" if options.get("sim", 0) == 0 else "adjacent")}
     baseline = None
@@ -300,7 +331,7 @@ def run_stream(args, torch):
     work = work_table(*[x / steps for x in tot])
     config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "chunks": steps,
-              "chunk": src.chunk_len, "budget": spec["total_budget"],
+              "chunk": src.chunk_len, "budget": spec["total_budget"], "launch": "stream",
               "layer_budgets": "offline" if args.offline_budgets else "per step",
               "selection": "per layer" if args.shared_selection else "per KV head"}
     return ms, tokens / (ms / 1e3), kernels, work, spec["dtype"], config, None
