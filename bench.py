@@ -30,12 +30,12 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-layer-6144": {
-        "sources_sha256": "49b3c4e9a8ff56e4c54f367f8530341f7b89dad635741fb99f789d31dd6616dd",
-        "lse_pass": 31185273, "colsum_pass": 32952971, "gram_pass": 15426145, "psi_topk": 843742, "gather_compact": 16886957,
+        "sources_sha256": "3fa67d7b49db6995e326bc84dfcb0d3298cfd0432671ad8bc14d1b7ee4f4d966",
+        "lse_pass": 31184126, "colsum_pass": 32957198, "gram_pass": 15436971, "psi_topk": 844678, "gather_compact": 16886969,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "49b3c4e9a8ff56e4c54f367f8530341f7b89dad635741fb99f789d31dd6616dd",
-        "lse_pass": 614003358, "colsum_pass": 613147343, "gram_pass": 804707608, "psi_topk": 14620432, "gather_compact": 471772128,
+        "sources_sha256": "3fa67d7b49db6995e326bc84dfcb0d3298cfd0432671ad8bc14d1b7ee4f4d966",
+        "lse_pass": 610043601, "colsum_pass": 615865551, "gram_pass": 807284508, "psi_topk": 14622631, "gather_compact": 471776380,
     },
 }
 
