@@ -347,6 +347,22 @@ struct SwzTile {
   }
 };
 
+// The same 16-byte-per-lane global-to-LDS copy (to lds + 16 * lane) as
+// inline assembly.  The compiler does not see an LDS store, so it adds no
+// wait for the copy before later LDS reads (with the builtin it waits before
+// any read it cannot prove disjoint, such as the other half of a
+// double-buffered array); the caller orders every read of the destination
+// after dma_wait() and a barrier.  Its own vector-memory waits stay correct:
+// copies it does not count only make them stricter.  The statement sets M0,
+// a register the compiler reserves and does not take as clobbered: use it
+// only in kernels where the compiler itself emits no M0 use (no builtin LDS
+// copies; on gfx950 ordinary LDS instructions do not read M0).
+__device__ inline void dma16_opaque(const void* g, void* lds) {
+  const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane(
+      (int)(uintptr_t)(__attribute__((address_space(3))) void*)lds);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(m0) : "memory");
+}
+
 // A wave's DMA copies count as vector-memory loads; s_barrier does not wait
 // for them on gfx950, so each wave drains its own copies before the barrier
 // that hands the tile to the other waves.

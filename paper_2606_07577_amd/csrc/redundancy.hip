@@ -559,22 +559,29 @@ __global__ __launch_bounds__(256) void adjacent_cos_hidden(const LayerDesc* __re
   for (int g = lane; g < dm.Hkv; g += 64) s[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = v;
 }
 
-// --- all-pairs maximum on hidden states (the R6 reading of Eq. 7 on them) ----
+// --- all-pairs maximum on hidden states (Eq. 7's redundancy as the maximum
+// cosine over all pairs of the modality, applied to them) ----
 // d_model does not fit the register-resident operand of gram_pass, so both
-// operands stream through LDS.  Work item: a pair (I <= J) of 128-row blocks
+// operands stream through LDS.  Work item: a pair (I <= J) of row blocks
 // of one segment (layer, modality), rows gathered through the segment's row
 // list; persistent workgroups take the pairs of all segments round-robin.
 // The d axis goes by chunks of 64 (four MFMA k-steps), DMA-copied into two
-// LDS stages (the next chunk lands while the current one is used).  Each of
-// the four waves owns a 64 x 64 quarter of the 128 x 128 block.  After the
+// LDS stages (the next chunk lands while the current one is used).  The
+// rows of the hidden states do not stay in L2, so the stages are fed at the
+// bandwidth of the next cache level: the larger the block, the fewer bytes
+// per MFMA.  Each wave owns 64 block rows and half the block's columns.  After the
 // last chunk the products become cosines (inverse norms from LDS; a row's
 // pair with itself and rows past the segment masked as NaN), and both the
 // block rows' maxima (over the block's columns: halving exchanges across the
 // lanes) and the columns' maxima (in-lane) are merged, first in LDS across
 // waves, then into the rows' best values by atomicMax: each pair is
 // computed once.
-constexpr int kWideBlock = 128;
 constexpr int kWideChunk = 64;  // d elements per LDS stage row
+// Rows per block side: 256 for bf16 (eight waves, each a 64 x 128 tile; the
+// double-buffered stage takes 128 KB, one workgroup per compute unit), 128
+// for fp32 (four waves of 64 x 64; a 256-row fp32 stage would not fit LDS).
+template <typename T> constexpr int wide_block() { return sizeof(T) == 2 ? 256 : 128; }
+template <typename T> constexpr int wide_threads() { return wide_block<T>() / 32 * 64; }
 
 __device__ inline float swz_xor(float v, int m) {
   // ds_swizzle bit mode (and-mask 0x1F, xor-mask m): within groups of 32 lanes
@@ -630,23 +637,28 @@ __global__ __launch_bounds__(256) void hidden_norms(const LayerDesc* __restrict_
 }
 
 template <typename T>
-__global__ __launch_bounds__(256, 2) void gram_wide(const LayerDesc* __restrict__ layers, Dims dm,
-                                                    const int* __restrict__ pos, const int* __restrict__ counts,
-                                                    const float* __restrict__ inv, int* __restrict__ best) {
+__global__ __launch_bounds__(wide_threads<T>(), 2) void gram_wide(
+    const LayerDesc* __restrict__ layers, Dims dm, const int* __restrict__ pos, const int* __restrict__ counts,
+    const float* __restrict__ inv, int* __restrict__ best) {
   using M = Mfma<T>;
-  using Tl = SwzTile<T, kWideChunk>;  // one stage: 64 rows of a 64-element chunk
+  using Tl = SwzTile<T, kWideChunk>;  // one stage tile: 64 rows of a 64-element chunk
+  constexpr int BR = wide_block<T>();
+  constexpr int kThr = wide_threads<T>();
+  constexpr int TPS = BR / kScoreTile;  // stage tiles per block side
+  constexpr int WC = BR / 2;            // block columns per wave
+  constexpr int CB = WC / 32;           // 32-column MFMA blocks per wave
   constexpr int KS = kWideChunk / M::KSTEP;
   constexpr int EPC = 16 / (int)sizeof(T);
   constexpr int CPR = kWideChunk / EPC;  // 16-byte pieces per stage row
   constexpr int kMaxSegs = 2048;
-  __shared__ __attribute__((aligned(16))) T stage[2][4][Tl::ELEMS];  // [buffer][A lo, A hi, B lo, B hi]
+  __shared__ __attribute__((aligned(16))) T stage[2][2 * TPS][Tl::ELEMS];  // [buffer][A tiles, B tiles]
   __shared__ int seg_first[kMaxSegs + 1];  // first pair of each segment (pair counts fit 31 bits)
-  __shared__ float inv_a[kWideBlock], inv_b[kWideBlock];
-  __shared__ int row_a[kWideBlock], row_b[kWideBlock];
-  __shared__ int mx_a[kWideBlock], mx_b[kWideBlock];
+  __shared__ float inv_a[BR], inv_b[BR];
+  __shared__ int row_a[BR], row_b[BR];
+  __shared__ int mx_a[BR], mx_b[BR];
   const int S = 2 * dm.L;
   for (int q = threadIdx.x; q < S; q += blockDim.x) {
-    const int nb = (counts[q] + kWideBlock - 1) / kWideBlock;
+    const int nb = (counts[q] + BR - 1) / BR;
     seg_first[q + 1] = nb * (nb + 1) / 2;
   }
   __syncthreads();
@@ -657,7 +669,7 @@ __global__ __launch_bounds__(256, 2) void gram_wide(const LayerDesc* __restrict_
   __syncthreads();
   const int total = uniform(seg_first[S]);
   const int w = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
-  const int wr = w >> 1, wc = w & 1;  // the wave's 64 block rows (A) and 64 block columns (B)
+  const int wr = w >> 1, wc = w & 1;  // the wave's 64 block rows (A) and WC block columns (B)
   const int nchunks = dm.dh / kWideChunk;
   for (int p = blockIdx.x; p < total; p += gridDim.x) {
     // segment and block pair of p
@@ -669,7 +681,7 @@ __global__ __launch_bounds__(256, 2) void gram_wide(const LayerDesc* __restrict_
     }
     const int l = q >> 1;
     const int K = counts[q];
-    const int nb = (K + kWideBlock - 1) / kWideBlock;
+    const int nb = (K + BR - 1) / BR;
     int r = p - uniform(seg_first[q]);
     int bi = 0;
     while (r >= nb - bi) { r -= nb - bi; ++bi; }
@@ -677,75 +689,81 @@ __global__ __launch_bounds__(256, 2) void gram_wide(const LayerDesc* __restrict_
     const LayerDesc Ld = layers[l];
     const int* P = pos + (int64_t)q * dm.max_tokens;
     __syncthreads();  // every wave is done with the previous pair's LDS
-    for (int t = threadIdx.x; t < 2 * kWideBlock; t += blockDim.x) {
-      const int side = t / kWideBlock, k = t % kWideBlock;
-      const int m = (side ? bj : bi) * kWideBlock + k;
+    for (int t = threadIdx.x; t < 2 * BR; t += blockDim.x) {
+      const int side = t / BR, k = t % BR;
+      const int m = (side ? bj : bi) * BR + k;
       const int row = P[min(m, K - 1)];
       const float iv = m < K ? inv[(int64_t)l * dm.max_tokens + row] : __builtin_nanf("");
       if (side) { row_b[k] = row; inv_b[k] = iv; mx_b[k] = kNoPartner; }
       else { row_a[k] = row; inv_a[k] = iv; mx_a[k] = kNoPartner; }
     }
     __syncthreads();
-    // this thread's DMA pieces: 16 per chunk (4 tiles x 64 rows x CPR pieces / 256)
-    constexpr int kPieces = 4 * kScoreTile * CPR / 256;
+    // this thread's DMA pieces of a chunk: 2 TPS tiles x 64 rows x CPR pieces
+    // over the workgroup
+    constexpr int kInstrPerTile = kScoreTile * CPR / 64;
+    constexpr int kPieces = 2 * TPS * kInstrPerTile / (kThr / 64);
     const T* H = reinterpret_cast<const T*>(Ld.hidden);
     const T* src[kPieces];
 #pragma unroll
     for (int u = 0; u < kPieces; ++u) {
-      const int J = w * kPieces + u;             // DMA instruction of the workgroup
-      const int tile = J / (kScoreTile * CPR / 64), slot = (J % (kScoreTile * CPR / 64)) * 64 + lane;
+      const int J = w * kPieces + u;  // DMA instruction of the workgroup
+      const int tile = J / kInstrPerTile, slot = (J % kInstrPerTile) * 64 + lane;
       const int rr = slot / CPR, c = (slot % CPR) ^ (rr & (CPR - 1));
-      const int k = (tile & 1) * kScoreTile + rr;
-      const int row = (tile < 2) ? row_a[k] : row_b[k];
+      const int k = (tile % TPS) * kScoreTile + rr;
+      const int row = tile < TPS ? row_a[k] : row_b[k];
       src[u] = H + (int64_t)row * Ld.hidden_rs + c * EPC;
     }
+    // Copies of chunk ch into stage buffer buf, issued with dma16_opaque: the
+    // compiler does not see them write LDS, so reads of the other buffer do
+    // not wait for them (a buffer is read only after dma_wait and a barrier).
     auto dma_chunk = [&](int ch, int buf) {
 #pragma unroll
       for (int u = 0; u < kPieces; ++u) {
         const int J = w * kPieces + u;
-        const int tile = J / (kScoreTile * CPR / 64), jt = J % (kScoreTile * CPR / 64);
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(src[u] + ch * kWideChunk),
-                                         (__attribute__((address_space(3))) void*)(&stage[buf][tile][jt * 64 * EPC]),
-                                         16, 0, 0);
+        const int tile = J / kInstrPerTile, jt = J % kInstrPerTile;
+        dma16_opaque(src[u] + ch * kWideChunk, &stage[buf][tile][jt * 64 * EPC]);
       }
     };
-    floatx16 acc[2][2];
+    floatx16 acc[2][CB];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = floatx16{};
+      for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = floatx16{};
     dma_chunk(0, 0);
     for (int ch = 0; ch < nchunks; ++ch) {
       const int buf = ch & 1;
       dma_wait();
       __syncthreads();  // chunk ch landed; every wave is done with the other stage
       if (ch + 1 < nchunks) dma_chunk(ch + 1, buf ^ 1);
-      const T* A = stage[buf][wr];      // the wave's 64 A rows: tile wr (rows wr*64 ..)
-      const T* B = stage[buf][2 + wc];  // its 64 B rows
+      const T* A = stage[buf][wr];  // the wave's 64 A rows: tile wr
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        typename M::frag fa[2], fb[2];
+        typename M::frag fa[2], fb[CB];
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
-          fa[x] = Tl::template frag<M>(A, x * 32 + (lane & 31), ks, half);
-          fb[x] = Tl::template frag<M>(B, x * 32 + (lane & 31), ks, half);
+        for (int x = 0; x < 2; ++x) fa[x] = Tl::template frag<M>(A, x * 32 + (lane & 31), ks, half);
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {  // B column block wc * WC + cb * 32
+          const int bc = wc * WC + cb * 32;
+          fb[cb] = Tl::template frag<M>(stage[buf][TPS + bc / kScoreTile], bc % kScoreTile + (lane & 31), ks, half);
         }
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-          for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = M::mma(fa[rb], fb[cb], acc[rb][cb]);
+          for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = M::mma(fa[rb], fb[cb], acc[rb][cb]);
       }
     }
     // cosines; row (A) maxima across the lanes, column (B) maxima in-lane
-    float cmax[2] = {-INFINITY, -INFINITY};
+    float cmax[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) cmax[cb] = -INFINITY;
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       float wv[16];
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) wv[rr] = -INFINITY;
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
-        const int jb = wc * 64 + cb * 32 + (lane & 31);  // block column
+      for (int cb = 0; cb < CB; ++cb) {
+        const int jb = wc * WC + cb * 32 + (lane & 31);  // block column
         const float ib = inv_b[jb];
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
@@ -762,15 +780,15 @@ __global__ __launch_bounds__(256, 2) void gram_wide(const LayerDesc* __restrict_
       if ((lane & 1) == 0 && wv[0] > -INFINITY) atomicMax(&mx_a[ia_k], ord_f32(fminf(1.0f, fmaxf(-1.0f, wv[0]))));
     }
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < CB; ++cb) {
       const float m = fmaxf(cmax[cb], __shfl_xor(cmax[cb], 32, 64));
-      const int jb = wc * 64 + cb * 32 + (lane & 31);
+      const int jb = wc * WC + cb * 32 + (lane & 31);
       if (half == 0 && m > -INFINITY) atomicMax(&mx_b[jb], ord_f32(fminf(1.0f, fmaxf(-1.0f, m))));
     }
     __syncthreads();
-    for (int t = threadIdx.x; t < 2 * kWideBlock; t += blockDim.x) {
-      const int side = t / kWideBlock, k = t % kWideBlock;
-      const int m = (side ? bj : bi) * kWideBlock + k;
+    for (int t = threadIdx.x; t < 2 * BR; t += blockDim.x) {
+      const int side = t / BR, k = t % BR;
+      const int m = (side ? bj : bi) * BR + k;
       const int v = side ? mx_b[k] : mx_a[k];
       if (m < K && v != kNoPartner) atomicMax(best + (int64_t)l * dm.max_tokens + (side ? row_b[k] : row_a[k]), v);
     }
@@ -830,12 +848,14 @@ hipError_t launch_redundancy(const Dims& dm, int dtype, int sim, int source, con
     const dim3 gtok((unsigned)((dm.max_tokens + 255) / 256), dm.L);
     if (dtype == 0) {
       OMNIMEM_LAUNCH(ws, K_NORMS_H, st, hidden_norms<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ws.inv_norm, ws.best));
-      OMNIMEM_LAUNCH(ws, K_GRAM_H, st, gram_wide<uint16_t><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.pos, ws.counts,
-                                                                                       ws.inv_norm, ws.best));
+      OMNIMEM_LAUNCH(ws, K_GRAM_H, st,
+                     gram_wide<uint16_t><<<ws.gram_grid / 2, wide_threads<uint16_t>(), 0, st>>>(
+                         desc, dm, ws.pos, ws.counts, ws.inv_norm, ws.best));
     } else {
       OMNIMEM_LAUNCH(ws, K_NORMS_H, st, hidden_norms<float><<<grid, 256, 0, st>>>(desc, dm, ws.inv_norm, ws.best));
-      OMNIMEM_LAUNCH(ws, K_GRAM_H, st, gram_wide<float><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.pos, ws.counts,
-                                                                                    ws.inv_norm, ws.best));
+      OMNIMEM_LAUNCH(ws, K_GRAM_H, st,
+                     gram_wide<float><<<ws.gram_grid, wide_threads<float>(), 0, st>>>(desc, dm, ws.pos, ws.counts,
+                                                                                      ws.inv_norm, ws.best));
     }
     OMNIMEM_LAUNCH(ws, K_FINISH_H, st, hidden_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.best, s));
     return hipGetLastError();

@@ -539,16 +539,18 @@ __device__ inline void colsum_segment(const LayerDesc& Ld, const Dims& dm, int l
   const int kw = k0 + wave * kRowsPerWave;
   const bool active = kw < N;
   const int qfirst_wave = dm.causal ? max(0, kw - nc) : 0;
-  // normaliser of tile row threadIdx.x (+inf past the slice: probability 0)
-  auto load_lse = [&](int qt) {
-    const int i = qt + (int)threadIdx.x;
-    return (threadIdx.x < kTile && i < C) ? gload<float>(lse2_lh + i) : INFINITY;
-  };
-  float lse_next = INFINITY;
+  // Normaliser of tile row threadIdx.x % 64, loaded unconditionally from an
+  // index clamped into the slice; rows past it get +inf (probability 0)
+  // where the value is stored.  (A conditional load into a register first
+  // set to +inf would make the compiler wait for the tile copies issued
+  // before it.)
+  auto load_lse = [&](int qt) { return gload<float>(lse2_lh + min(qt + (int)(threadIdx.x & 63), C - 1)); };
+  auto lse_or_inf = [&](int qt, float v) { return qt + (int)threadIdx.x < C ? v : INFINITY; };
+  float lse_next = 0.0f;
   const typename Tl::Plan plan = Tl::plan(q_rs);
   if (qstart < C) {
     Tl::copy(qt0, q + (int64_t)qstart * q_rs, q_rs, min(kTile, C - qstart), plan);
-    if (threadIdx.x < kTile) lse2[0][threadIdx.x] = load_lse(qstart);
+    if (threadIdx.x < kTile) lse2[0][threadIdx.x] = lse_or_inf(qstart, load_lse(qstart));
     if (qstart + kTile < C) {
       Tl::copy(qt1, q + (int64_t)(qstart + kTile) * q_rs, q_rs, min(kTile, C - qstart - kTile), plan);
       lse_next = load_lse(qstart + kTile);
@@ -587,7 +589,13 @@ __device__ inline void colsum_segment(const LayerDesc& Ld, const Dims& dm, int l
     __syncthreads();  // first tiles landed in LDS for every wave
     if (busy_at(qstart)) mma_rows<M, Tl>(acc0, qt0, arow, half, kf);
     int slot = 0;
-    auto step = [&](int qt, T* cur, const T* nxt) {
+    // One tile in two halves: part_a (phase A and the store of the next
+    // tile's normalisers) and part_b (the barrier, the next DMA, phase B).
+    // The loop below starts each iteration with part_b, at the barrier that
+    // waits for every copy anyway: at a loop header the compiler no longer
+    // tells the two LDS stages apart and would make phase A wait for the
+    // copy into the other stage.
+    auto part_a = [&](int qt, T* cur) {
       const int next_slot = slot == 2 ? 0 : slot + 1;
       const bool has_next = qt + kTile < C;
       const bool busy = busy_at(qt);
@@ -602,7 +610,12 @@ __device__ inline void colsum_segment(const LayerDesc& Ld, const Dims& dm, int l
           OMNIMEM_INTERLEAVE(16, NV);
         }
       }
-      if (has_next && threadIdx.x < kTile) lse2[next_slot][threadIdx.x] = lse_next;
+      if (has_next && threadIdx.x < kTile) lse2[next_slot][threadIdx.x] = lse_or_inf(qt + kTile, lse_next);
+    };
+    auto part_b = [&](int qt, T* cur, const T* nxt) {
+      const int next_slot = slot == 2 ? 0 : slot + 1;
+      const bool has_next = qt + kTile < C;
+      const bool busy = busy_at(qt);
       dma_wait();
       __syncthreads();  // tile qt+1 landed; every wave is done with `cur`
       if (qt + 2 * kTile < C) {
@@ -629,9 +642,14 @@ __device__ inline void colsum_segment(const LayerDesc& Ld, const Dims& dm, int l
       }
       slot = next_slot;
     };
-    for (int qt = qstart; qt < C; qt += 2 * kTile) {
-      step(qt, qt0, qt1);
-      if (qt + kTile < C) step(qt + kTile, qt1, qt0);
+    part_a(qstart, qt0);
+    for (int qt = qstart;; qt += 2 * kTile) {
+      part_b(qt, qt0, qt1);
+      if (qt + kTile >= C) break;
+      part_a(qt + kTile, qt1);
+      part_b(qt + kTile, qt1, qt0);
+      if (qt + 2 * kTile >= C) break;
+      part_a(qt + 2 * kTile, qt0);
     }
   }
   if (!active) return;
