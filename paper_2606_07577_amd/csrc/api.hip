@@ -51,7 +51,7 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 
 static const char* kKernelNames[K_COUNT] = {
     "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact",
-    "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish"};
+    "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish", "layer_inputs"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -352,7 +352,8 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       (e = dalloc(ctx, &ws.calib, L)) != hipSuccess ||
       (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.idx, L * Hkv * T)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.keys, L * Hkv * T)) != hipSuccess) {
+      (e = dalloc(ctx, &ws.keys, L * Hkv * T)) != hipSuccess ||
+      (c.shared_selection && (e = dalloc(ctx, &ws.layer_as, 2 * L * T)) != hipSuccess)) {
     omnimem_destroy(ctx);
     return fail(nullptr, OMNIMEM_ERR_HIP, "workspace allocation: %s", hipGetErrorString(e));
   }

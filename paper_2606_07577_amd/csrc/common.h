@@ -211,7 +211,7 @@ constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
 // ---------------------------------------------------------------------------
 enum KernelId {
   K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
-  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_COUNT
+  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_LAYER_IN, K_COUNT
 };
 struct Profiler;
 void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
@@ -244,6 +244,7 @@ struct Workspace {
   int* eff;               // [L][2] budgets as applied by select
   int* idx;               // [L][Hkv][max_tokens] fallback for the idx output
   uint32_t* keys;         // [L][Hkv][max_tokens]
+  float* layer_as;        // [2][L][max_tokens] layer-shared selection inputs (null without it)
   Profiler* prof;         // null unless timing is on
 };
 

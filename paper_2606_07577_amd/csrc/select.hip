@@ -71,8 +71,9 @@ __device__ inline int wave_scan(int v, int* wave_tot, int* total) {
 // keys sit at their ranks in LDS (or, for segments too large for LDS, by row
 // in global memory).
 // SHARED: one workgroup per (layer, modality) ranks rows by the layer's
-// importance (a summed over the KV heads) and redundancy (s averaged over
-// them, in head order) and writes the kept rows to every head's idx row.
+// importance and redundancy (a and s as reduced over the KV heads by
+// layer_inputs, [L][max_tokens] each) and writes the kept rows to every
+// head's idx row.
 template <bool SHARED>
 __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restrict__ layers, Dims dm, float lambda,
                                                         const float* __restrict__ a, const float* __restrict__ s,
@@ -91,8 +92,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   const int N = layers[l].n;
   const uint8_t* mod = layers[l].mod;
   const int64_t off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
-  const float* ag = a + off;
-  const float* sg = s + off;
+  const float* ag = a + (SHARED ? (int64_t)l * dm.max_tokens : off);
+  const float* sg = s + (SHARED ? (int64_t)l * dm.max_tokens : off);
   uint32_t* kg = keys + off;   // keys by working-set row (segments past LDS)
   int32_t* ig = idx + off;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -100,20 +101,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   const int R = (N + kSelThreads - 1) / kSelThreads;   // rows per lane
   const int wrow0 = wave * 64 * R;
   auto member = [&](int j) { return j < N && (mod[j] ? 1 : 0) == mu; };
-  // importance and redundancy of row j: this KV head's, or the layer's
-  const int nh = SHARED ? dm.Hkv : 1;
-  auto read_a = [&](int j) {
-    if constexpr (!SHARED) return gload<float>(ag + j);
-    float t = 0.0f;
-    for (int h = 0; h < nh; ++h) t += gload<float>(ag + (int64_t)h * dm.max_tokens + j);
-    return t;
-  };
-  auto read_s = [&](int j) {
-    if constexpr (!SHARED) return gload<float>(sg + j);
-    float t = 0.0f;
-    for (int h = 0; h < nh; ++h) t += gload<float>(sg + (int64_t)h * dm.max_tokens + j);
-    return t / (float)nh;
-  };
+  auto read_a = [&](int j) { return gload<float>(ag + j); };
+  auto read_s = [&](int j) { return gload<float>(sg + j); };
   // the segment's budget (and the visual one, where the audio rows go),
   // requested first so that their latency overlaps the reads below
   const int bud_mu = budgets[2 * l + mu], bud_v = budgets[2 * l];
@@ -374,7 +363,7 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       if ((sb[u] >> lane) & 1ull) {
         const int slot = o + __popcll(sb[u] & lt), row = wrow0 + (i0 + u) * 64 + lane;
         if constexpr (SHARED) {
-          for (int h = 0; h < nh; ++h) ig[(int64_t)h * dm.max_tokens + slot] = row;
+          for (int h = 0; h < dm.Hkv; ++h) ig[(int64_t)h * dm.max_tokens + slot] = row;
         } else {
           ig[slot] = row;
         }
@@ -426,6 +415,25 @@ __global__ __launch_bounds__(256) void gather_compact(const LayerDesc* __restric
   }
 }
 
+// Inputs of layer-shared selection, one thread per working-set row: the
+// layer's importance, a summed over the KV heads, and its redundancy, s
+// summed over them and divided by their count (fp32, in head order).
+__global__ __launch_bounds__(256) void layer_inputs(const LayerDesc* __restrict__ layers, Dims dm,
+                                                    const float* __restrict__ a, const float* __restrict__ s,
+                                                    float* __restrict__ la, float* __restrict__ ls) {
+  const int l = blockIdx.y;
+  const int j = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (j >= layers[l].n) return;
+  float ta = 0.0f, ts = 0.0f;
+  for (int h = 0; h < dm.Hkv; ++h) {
+    const int64_t o = ((int64_t)l * dm.Hkv + h) * dm.max_tokens + j;
+    ta += a[o];
+    ts += s[o];
+  }
+  la[(int64_t)l * dm.max_tokens + j] = ta;
+  ls[(int64_t)l * dm.max_tokens + j] = ts / (float)dm.Hkv;
+}
+
 // Kept rows' hidden states, for layers that give hidden_out (layer-shared
 // selection: the index rows of all heads are equal, head 0's is read):
 // hidden_out[i] = hidden[idx[l][0][i]], one wave per row, 16 bytes a lane.
@@ -457,11 +465,15 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int sh
                                  const Workspace& ws, const float* a, const float* s, const int32_t* budgets,
                                  int32_t* idx, hipStream_t st) {
   int32_t* ix = idx ? idx : ws.idx;
-  if (shared)
+  if (shared) {
+    float* la = ws.layer_as;
+    float* ls = ws.layer_as + (size_t)dm.L * dm.max_tokens;
+    const dim3 gtok((unsigned)((dm.max_tokens + 255) / 256), dm.L);
+    OMNIMEM_LAUNCH(ws, K_LAYER_IN, st, layer_inputs<<<gtok, 256, 0, st>>>(desc, dm, a, s, la, ls));
     OMNIMEM_LAUNCH(ws, K_TOPK, st,
-                   psi_topk<true><<<dim3(2, 1, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets, ws.keys,
+                   psi_topk<true><<<dim3(2, 1, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, la, ls, budgets, ws.keys,
                                                                             ix, ws.eff));
-  else
+  } else
     OMNIMEM_LAUNCH(ws, K_TOPK, st,
                    psi_topk<false><<<dim3(2, dm.Hkv, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets,
                                                                                   ws.keys, ix, ws.eff));
