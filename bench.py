@@ -30,12 +30,16 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-layer-6144": {
-        "sources_sha256": "3fa67d7b49db6995e326bc84dfcb0d3298cfd0432671ad8bc14d1b7ee4f4d966",
-        "lse_pass": 31184126, "colsum_pass": 32957198, "gram_pass": 15436971, "psi_topk": 844678, "gather_compact": 16886969,
+        "sources_sha256": "04275c45c27241221a0ac274a87187296e9cc4fa345a16bd98dddf2f237795a0",
+        "lse_pass": 31187529, "colsum_pass": 32993402, "gram_pass": 15433890, "psi_topk": 818054, "gather_compact": 16887001,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "3fa67d7b49db6995e326bc84dfcb0d3298cfd0432671ad8bc14d1b7ee4f4d966",
-        "lse_pass": 610043601, "colsum_pass": 615865551, "gram_pass": 807284508, "psi_topk": 14622631, "gather_compact": 471776380,
+        "sources_sha256": "04275c45c27241221a0ac274a87187296e9cc4fa345a16bd98dddf2f237795a0",
+        "lse_pass": 611394974, "colsum_pass": 615848918, "gram_pass": 808967164, "psi_topk": 14596421, "gather_compact": 471770704,
+    },
+    "qwen7b-layer-6144-hidden": {
+        "sources_sha256": "04275c45c27241221a0ac274a87187296e9cc4fa345a16bd98dddf2f237795a0",
+        "lse_pass": 31185590, "colsum_pass": 32991519, "gram_wide": 327765967, "psi_topk": 254395, "gather_compact": 16887659,
     },
 }
 
