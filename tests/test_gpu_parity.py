@@ -418,8 +418,8 @@ def _hidden_step(layers, budget, dh, sim=omnimem.SIM_ADJ):
                                            ("bf16", 3584, "max"), ("f32", 192, "max")])
 def test_hidden_state_redundancy(dtype, dh, mode):
     # One value per token from its hidden state, in every KV head's row;
-    # 'max' spans several 128-row blocks per segment (pairs on and off the
-    # diagonal, a ragged last block).
+    # 'max' spans several row blocks per segment (256 rows for bf16, 128 for
+    # fp32: pairs on and off the diagonal, a ragged last block).
     layers = ragged_layers(2, dtype=dtype, seed=114, caches=((200, 77), (90, 31)), hidden_dim=dh)
     st = _hidden_step(layers, 300, dh, omnimem.SIM_ADJ if mode == "adj" else omnimem.SIM_MAX)
     st.redundancy()
@@ -431,10 +431,12 @@ def test_hidden_state_redundancy(dtype, dh, mode):
 
 
 @pytest.mark.parametrize("mode", ["adj", "max"])
-def test_hidden_state_small_segments(mode):
-    # A visual segment of 129 rows (a last block of one row) and a lone
-    # audio row (no partner: s = 0), next to a layer of two rows per modality.
-    layers = (ragged_layers(1, seed=117, caches=((128, 1),), frames=(1, 1, 0), hidden_dim=256)
+@pytest.mark.parametrize("cache_v", [128, 256])
+def test_hidden_state_small_segments(mode, cache_v):
+    # A visual segment of cache_v + 1 rows (a last block of one row for the
+    # all-pairs kernel's 128- and 256-row blocks) and a lone audio row (no
+    # partner: s = 0), next to a layer of two rows per modality.
+    layers = (ragged_layers(1, seed=117, caches=((cache_v, 1),), frames=(1, 1, 0), hidden_dim=256)
               + ragged_layers(1, seed=118, caches=((1, 1),), frames=(1, 1, 1), hidden_dim=256))
     st = _hidden_step(layers, 100, 256, omnimem.SIM_ADJ if mode == "adj" else omnimem.SIM_MAX)
     st.redundancy()
