@@ -671,7 +671,18 @@ __global__ __launch_bounds__(wide_threads<T>(), 2) void gram_wide(
   const int w = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
   const int wr = w >> 1, wc = w & 1;  // the wave's 64 block rows (A) and WC block columns (B)
   const int nchunks = dm.dh / kWideChunk;
-  for (int p = blockIdx.x; p < total; p += gridDim.x) {
+  // Rounds of gridDim.x pairs; in each, XCD x (blockIdx % 8) takes a run of
+  // consecutive pairs, which mostly share their first block, so its L2
+  // serves that block's chunks to all of them.  A last partial round is
+  // split evenly over the XCDs.  (A grid that is not a multiple of 8 takes
+  // pairs in plain order.)
+  const bool by_xcd = gridDim.x % kXcds == 0;
+  for (int base = 0; base < total; base += gridDim.x) {
+    const int R = min((int)gridDim.x, total - base);
+    const int per = by_xcd ? (R + kXcds - 1) / kXcds : R;
+    const int k = by_xcd ? (int)blockIdx.x / kXcds : (int)blockIdx.x;
+    const int p = base + (by_xcd ? ((int)blockIdx.x % kXcds) * per : 0) + k;
+    if (k >= per || p >= base + R) continue;  // uniform over the workgroup
     // segment and block pair of p
     int q = 0;
     for (int lo = 0, hi = S - 1; lo < hi;) {
