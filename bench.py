@@ -30,16 +30,16 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-layer-6144": {
-        "sources_sha256": "04275c45c27241221a0ac274a87187296e9cc4fa345a16bd98dddf2f237795a0",
-        "lse_pass": 31187529, "colsum_pass": 32993402, "gram_pass": 15433890, "psi_topk": 818054, "gather_compact": 16887001,
+        "sources_sha256": "c4d6533d57b87d112b8ecf941048f3c127491957c653bd14de5dca96304291a1",
+        "lse_pass": 31186220, "colsum_pass": 32981324, "gram_pass": 15426726, "psi_topk": 818054, "gather_compact": 16886966,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "04275c45c27241221a0ac274a87187296e9cc4fa345a16bd98dddf2f237795a0",
-        "lse_pass": 611394974, "colsum_pass": 615848918, "gram_pass": 808967164, "psi_topk": 14596421, "gather_compact": 471770704,
+        "sources_sha256": "c4d6533d57b87d112b8ecf941048f3c127491957c653bd14de5dca96304291a1",
+        "lse_pass": 609988761, "colsum_pass": 615876283, "gram_pass": 805820510, "psi_topk": 14596168, "gather_compact": 471766999,
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "04275c45c27241221a0ac274a87187296e9cc4fa345a16bd98dddf2f237795a0",
-        "lse_pass": 31185590, "colsum_pass": 32991519, "gram_wide": 327765967, "psi_topk": 254395, "gather_compact": 16887659,
+        "sources_sha256": "c4d6533d57b87d112b8ecf941048f3c127491957c653bd14de5dca96304291a1",
+        "lse_pass": 31191157, "colsum_pass": 32971231, "gram_wide": 188147568, "psi_topk": 254395, "gather_compact": 16887551,
     },
 }
 
