@@ -70,7 +70,8 @@ typedef enum { OMNIMEM_SIM_MAX = 0, OMNIMEM_SIM_ADJ = 1 } omnimem_sim;
 /* Vectors the cosines of Eq. (7) are taken on.  Eq. (7) is printed on the
  * hidden states; Sec. 3.1 allows the value vectors instead, which keeps the
  * cache as it is.  Hidden states are per token, so one redundancy serves
- * every KV head of the layer; they are supported with SIM_ADJ only. */
+ * every KV head of the layer; both SIM_ADJ and SIM_MAX apply to them
+ * (SIM_MAX with hidden_dim a multiple of 64). */
 typedef enum { OMNIMEM_SRC_VALUES = 0, OMNIMEM_SRC_KEYS = 1, OMNIMEM_SRC_HIDDEN = 2 } omnimem_source;
 
 typedef struct {
@@ -182,8 +183,8 @@ omnimem_status omnimem_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, c
                                 const float* s, int64_t total_budget, int32_t* budgets,
                                 float* stats, hipStream_t stream);
 
-/* Offline budgets (end of Sec. 3.2: the layer budgets are determined offline
- * from a small calibration set).  The per-layer budgets B^(l) of Eq. (14)
+/* Offline budgets (end of Sec. 3.2: the layer budgets may be fixed ahead of
+ * time from a few calibration chunks).  The per-layer budgets B^(l) of Eq. (14)
  * are fixed in advance; every step then only splits them between the
  * modalities (Eqs. 11-12).
  *

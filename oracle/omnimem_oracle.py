@@ -17,8 +17,9 @@ in the paper's order and notation:
   * Eqs. (9), (10), (13)  normalised entropy x (1 - mean cosine)      -> avba_statistics
   * Eqs. (11), (12)  audio/visual proportions w_v, w_a                -> modality_weights
   * Eq. (14) + the [B_min, B_max] constraint of Sec. 3.2              -> layer_budgets
-  * "split according to w_v and w_a" (Sec. 3.2)                       -> split_budget
-  * budgets "determined offline ... on a small calibration set"
+  * the layer budget divided between the modalities by w_v and w_a
+    (Sec. 3.2, after Eqs. (11), (12))                                 -> split_budget
+  * layer budgets fixed in advance from calibration data
     (end of Sec. 3.2)                                                 -> calibration_budgets,
                                                                          fixed_split
   * Eqs. (4), (5) Select: top-M by psi per modality (Sec. 3.1)         -> select

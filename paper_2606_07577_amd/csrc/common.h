@@ -354,14 +354,24 @@ struct SwzTile {
 // any read it cannot prove disjoint, such as the other half of a
 // double-buffered array); the caller orders every read of the destination
 // after dma_wait() and a barrier.  Its own vector-memory waits stay correct:
-// copies it does not count only make them stricter.  The statement sets M0,
-// a register the compiler reserves and does not take as clobbered: use it
-// only in kernels where the compiler itself emits no M0 use (no builtin LDS
-// copies; on gfx950 ordinary LDS instructions do not read M0).
+// copies it does not count only make them stricter.  The copy takes its LDS
+// address from M0, a register the compiler reserves and never treats as
+// clobbered, so the statement saves M0 in a scratch SGPR of its own and
+// restores it after issuing the copy (the copy reads M0 when it issues):
+// whatever value the compiler keeps in M0 is unchanged across it.
 __device__ inline void dma16_opaque(const void* g, void* lds) {
   const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane(
       (int)(uintptr_t)(__attribute__((address_space(3))) void*)lds);
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(m0) : "memory");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(m0)
+      : "memory");
 }
 
 // A wave's DMA copies count as vector-memory loads; s_barrier does not wait

@@ -6,10 +6,10 @@
 //           segment of cos(u_k, u_j).  The segment's rows are first gathered
 //           into one contiguous block (visual rows, then audio rows, each in
 //           ascending order) with their fp32 inverse norms; the Gram matrix
-//           U U^T is then computed on MFMA over its upper triangle in
-//           256 x 64 tiles (raw bf16/fp32 inputs, fp32 accumulation),
-//           scaled by the inverse norms and reduced to row and column maxima
-//           in registers; maxima merge with atomicMax on an
+//           U U^T is then computed on MFMA, the whole matrix (both
+//           triangles) in 256 x 64 tiles (raw bf16/fp32 inputs, fp32
+//           accumulation), scaled by the inverse norms and reduced to row
+//           maxima in registers; maxima merge with atomicMax on an
 //           order-preserving int encoding.  The N x N matrix never leaves
 //           the chip.
 //  SIM_ADJ  Eq. (7) as printed: mean cosine with the previous and next row

@@ -1,5 +1,5 @@
-"""Pins of the oracle's offline budgets (end of Sec. 3.2: the budget is
-determined offline from a small calibration set) to facts other than the
+"""Pins of the oracle's offline budgets (end of Sec. 3.2: layer budgets fixed
+ahead of time from a few calibration chunks) to facts other than the
 oracle itself: averaging, softmax invariances, closed forms and the
 relation to the online step."""
 import math
