@@ -63,9 +63,14 @@ def measured_traffic(workload, kernel):
 def parse_args():
     p = argparse.ArgumentParser(description=__doc__)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--steps", type=int, default=None,
+                   help="timed steps (default: every chunk of a stream, 50 for a fixed working set)")
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="qwen7b-layer-6144")
+    p.add_argument("--workload", default="qwen7b-stream-64x28",
+                   help="a stream (default: 64 chunks through 28 layers) or a fixed working set")
+    p.add_argument("--out-of-place", action="store_true",
+                   help="streams: keep two cache buffers per layer and compact from one into the other "
+                        "instead of compacting in place")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--offline-budgets", action="store_true",
                    help="fix the layer budgets in advance from a calibration (end of Sec. 3.2): static "
@@ -116,7 +121,7 @@ def work_table(score, gram, topk, compact):
     """Per-launch algorithmic units of each counted kernel."""
     return {"lse_pass": ("mfma", score), "colsum_pass": ("mfma", score), "gram_pass": ("mfma", gram),
             "gram_wide": ("mfma", gram),
-            "gather_compact": ("hbm", compact), "psi_topk": ("hbm", topk)}
+            "gather_compact": ("hbm", compact), "gather_inplace": ("hbm", compact), "psi_topk": ("hbm", topk)}
 
 
 def static_work(layers, budgets, hidden_dim=0):
@@ -134,27 +139,87 @@ def static_work(layers, budgets, hidden_dim=0):
     return work_table(*tot)
 
 
-def cpu_baseline(layers, spec):
-    """The oracle, as it stands, on one layer of the same workload."""
-    import numpy as np
+def _host_cpu():
+    """Host threads available to this process and the CPU model."""
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cores, model
+
+
+def _time_oracle(layers, budget, threads, **kw):
     import threadpoolctl
 
     from oracle import omnimem_oracle as orc
-    lay = dict(layers[0])
-    for key in ("q", "k", "v", "h"):
-        if key in lay:
-            lay[key] = lay[key].astype(np.float64)
+    with threadpoolctl.threadpool_limits(limits=threads, user_api="blas"):
+        t0 = time.perf_counter()
+        orc.compression_step(layers, budget, **kw)
+        return time.perf_counter() - t0
+
+
+def cpu_baseline(layers, spec, sample_layers=1):
+    """The oracle, as it stands, on `sample_layers` layers of the same
+    working sets, with every host thread available to its BLAS and again
+    with one (on one layer)."""
+    import numpy as np
+
+    lays = []
+    for lay in layers[:sample_layers]:
+        x = dict(lay)
+        for key in ("q", "k", "v", "h"):
+            if key in x:
+                x[key] = x[key].astype(np.float64)
+        lays.append(x)
     per_layer_budget = spec["total_budget"] // spec["n_layers"]
     hidden = bool(spec.get("hidden_dim"))
-    t0 = time.perf_counter()
-    orc.compression_step([lay], per_layer_budget, mode="adj" if hidden else "max", shared_selection=hidden,
-                         use_hidden=hidden)
-    dt = time.perf_counter() - t0
-    threads = max([x["num_threads"] for x in threadpoolctl.threadpool_info() if x["user_api"] == "blas"] or [1])
-    n = lay["k"].shape[1]
-    return {"value": n / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"one layer ({n} tokens) of the same workload through the whole numpy fp64 oracle step, "
-                      f"{dt:.1f} s wall; BLAS threads as cores (exp/sort single-threaded)"}
+    kw = dict(mode="adj" if hidden else "max", shared_selection=hidden, use_hidden=hidden)
+    cores, model = _host_cpu()
+    dt = _time_oracle(lays, per_layer_budget * len(lays), cores, **kw)
+    dt1 = _time_oracle(lays[:1], per_layer_budget, 1, **kw)
+    n = sum(int(x["k"].shape[1]) for x in lays)
+    n1 = int(lays[0]["k"].shape[1])
+    return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu_model": model, "one_thread_value": n1 / dt1,
+            "sample": f"{len(lays)} layer(s) of {n // len(lays)} tokens of the same workload through the whole "
+                      f"numpy fp64 oracle step: {dt:.1f} s wall with its BLAS on {cores} threads "
+                      f"(exp, sort and the Python loops single-threaded); one layer on one thread: {dt1:.1f} s"}
+
+
+def stream_sample_layers(name, t=2, n_layers=2):
+    """Working sets of the first `n_layers` layers of a stream at chunk t
+    while every earlier row is still kept (true up to chunk 2 at the
+    headline's budget): the rows of chunks 0 .. t-1, visual rows then audio
+    rows in age order, followed by chunk t.  Host arrays (numpy generator)."""
+    import numpy as np
+
+    from paper_2606_07577_amd import synth
+    src = synth.StreamSource(name, n_layers=n_layers)
+    past = []
+    for c in range(t + 1):
+        ch = src.chunk(c)
+        if c < t:
+            past.append(ch)
+    out = []
+    for l in range(n_layers):
+        ks = np.concatenate([p[l]["k"] for p in past], axis=1) if past else ch[l]["k"][:, :0]
+        vs = np.concatenate([p[l]["v"] for p in past], axis=1) if past else ch[l]["v"][:, :0]
+        ms = np.concatenate([p[l]["modality"] for p in past]) if past else ch[l]["modality"][:0]
+        order = np.concatenate([np.flatnonzero(ms == 0), np.flatnonzero(ms == 1)])
+        out.append({"q": ch[l]["q"], "k": np.concatenate([ks[:, order], ch[l]["k"]], axis=1),
+                    "v": np.concatenate([vs[:, order], ch[l]["v"]], axis=1),
+                    "modality": np.concatenate([ms[order], ch[l]["modality"]]), "n_cache": len(order),
+                    "sm_scale": ch[l]["sm_scale"], "dtype": ch[l]["dtype"]})
+    return out
 
 
 def run_static(args, torch):
@@ -263,21 +328,23 @@ def run_static(args, torch):
 def run_stream(args, torch):
     """The step after each of K consecutive chunks of a stream, from empty
     caches.  All chunks are generated on the device before timing; the timed
-    region holds, per chunk, the append of its K/V behind the kept rows, the
-    four library calls and the read-back of the budgets."""
+    region holds, per chunk, the append of its K/V behind the kept rows
+    (Eq. 3), the four library calls and the read-back of the budgets (the
+    host waits for the budgets only; the compaction overlaps the next
+    step's preparation)."""
     from paper_2606_07577_amd import synth
     from paper_2606_07577_amd.step import StreamRunner
 
     spec = synth.STREAMS[args.workload]
-    steps = args.steps = min(args.steps, spec["n_chunks"])
+    steps = args.steps = min(args.steps or spec["n_chunks"], spec["n_chunks"])
     src = synth.StreamSource(args.workload, backend="torch")
     chunks = [src.chunk(t) for t in range(steps)]
     torch.cuda.synchronize()
 
-    def runner():
+    def runner(**kw):
         return StreamRunner(spec["n_layers"], spec["h_q"], spec["h_kv"], spec["d"], src.chunk_len,
-                            spec["total_budget"], dtype=spec["dtype"],
-                            shared_selection=int(args.shared_selection))
+                            spec["total_budget"], dtype=spec["dtype"], in_place=not args.out_of_place,
+                            shared_selection=int(args.shared_selection), **kw)
 
     print(f"[bench] stream {args.workload}: {steps} chunks resident, warmup {args.warmup} chunks",
           file=sys.stderr, flush=True)
@@ -300,6 +367,7 @@ def run_stream(args, torch):
             r.fixed = True
         return r
 
+    # Timed region: K steps of the stream, nothing else.
     run = fix(runner())
     stream = torch.cuda.current_stream()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -311,23 +379,32 @@ def run_stream(args, torch):
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / steps
     tokens = run.tokens / steps            # working-set rows per step, summed over layers
+    fallbacks = run.fallbacks
     run.close()
 
-    # The same stream again with per-kernel HIP events; per-step work from
-    # the shapes each step saw.
+    # The same stream again with events around the append and the four
+    # stages of every step.
+    run = fix(runner(timing=True))
+    for t in range(steps):
+        run.push(chunks[t], stream)
+    app_ms, abi_ms = run.timings()
+    run.close()
+
+    # And again with per-kernel HIP events; per-step work from the shapes
+    # each step saw.
     run = fix(runner())
     run.ctx.omnimem_profile(True)
     tot = [0, 0, 0, 0]
     elt = 2 if spec["dtype"] == "bf16" else 4
     for t in range(steps):
         n_cache = list(run.n_cache)
-        mods = [run.mbuf[run.cur][l][:n_cache[l]].cpu().numpy() for l in range(spec["n_layers"])]
+        k_a = [int((run.cache_modality(l) == 1).sum()) for l in range(spec["n_layers"])]
         budgets = run.push(chunks[t], stream)
         for l in range(spec["n_layers"]):
-            k_a = int(mods[l].sum()) + spec["n_frames"] * spec["frame_a"]
+            ka = k_a[l] + spec["n_frames"] * spec["frame_a"]
             n = n_cache[l] + src.chunk_len
             w = layer_work(spec["h_q"], src.chunk_len, n_cache[l], spec["h_kv"], n, spec["d"], elt,
-                           n - k_a, k_a, int(budgets[l].sum()))
+                           n - ka, ka, int(budgets[l].sum()))
             tot = [x + y for x, y in zip(tot, w)]
     torch.cuda.synchronize()
     kernels = run.ctx.omnimem_profile_report()
@@ -336,9 +413,19 @@ def run_stream(args, torch):
     config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "chunks": steps,
               "chunk": src.chunk_len, "budget": spec["total_budget"], "launch": "stream",
+              "compaction": "out of place (two buffers)" if args.out_of_place else "in place (one buffer)",
               "layer_budgets": "offline" if args.offline_budgets else "per step",
               "selection": "per layer" if args.shared_selection else "per KV head"}
-    return ms, tokens / (ms / 1e3), kernels, work, spec["dtype"], config, None
+    extra = {"append_ms_per_step": round(app_ms / steps, 5), "stages_ms_per_step": round(abi_ms / steps, 5),
+             "stages_tokens_per_s": round(tokens / (abi_ms / steps / 1e3), 1), "fallback_steps": fallbacks}
+    baseline = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        sample = stream_sample_layers(args.workload, t=2, n_layers=2)
+        baseline = cpu_baseline(sample, spec, sample_layers=2)
+        baseline["sample"] = ("the stream's working sets at chunk 2 (4096 kept rows + a 2048-row chunk) of layers "
+                              "0 and 1; " + baseline["sample"])
+    return ms, tokens / (ms / 1e3), kernels, work, spec["dtype"], config, baseline, extra
 
 
 def main():
@@ -357,9 +444,14 @@ def main():
     if args.lse_given and args.workload in synth.STREAMS:
         print("--lse-given applies to the fixed working sets, not to streams", file=sys.stderr)
         sys.exit(1)
+    extra = {}
     if args.workload in synth.STREAMS:
-        ms, value, kernels, work, dtype, config, base = run_stream(args, torch)
+        ms, value, kernels, work, dtype, config, base, extra = run_stream(args, torch)
     else:
+        if args.out_of_place:
+            print("--out-of-place applies to streams", file=sys.stderr)
+            sys.exit(1)
+        args.steps = args.steps or 50
         ms, value, kernels, work, dtype, config, base = run_static(args, torch)
     print(f"[bench] {ms:.4f} ms/step, {value:.4g} tokens/s", file=sys.stderr, flush=True)
     per_kernel = {}
@@ -384,14 +476,17 @@ def main():
                 "units_per_launch": work[dominant][1], "avg_launch_us": dk["avg_us"]}
 
     def stage_frac(names, peak_units, scale):
+        # time of every listed kernel that ran; units of those with algorithmic units (the
+        # in-place staging copy moves bytes beyond the out-of-place minimum: time only)
         t = sum(per_kernel[n]["avg_us"] for n in names if n in per_kernel) / 1e6
-        u = sum(work[n][1] for n in names if n in per_kernel)
+        u = sum(work[n][1] for n in names if n in per_kernel and n in work)
         return round(u / t / scale / peak_units, 4) if t > 0 else None
 
     fractions = {
         "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_pass", "gram_wide"],
                                            PEAK_MFMA_TFLOPS[dtype], 1e12),
-        "hbm_frac_topk_compact": stage_frac(["psi_topk", "gather_compact"], PEAK_HBM_GBS, 1e9),
+        "hbm_frac_topk_compact": stage_frac(["psi_topk", "gather_compact", "gather_inplace", "stage_moved_back"],
+                                            PEAK_HBM_GBS, 1e9),
     }
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -399,6 +494,7 @@ def main():
         "vs_baseline": None, "dtype": dtype, "data": "synthetic", "config": config,
         "roofline": roofline, "fractions": fractions, "kernels": per_kernel, "cpu_baseline": base,
     }
+    out.update(extra)
     print(json.dumps(out))
 
 

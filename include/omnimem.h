@@ -95,6 +95,11 @@ typedef struct {
   int64_t max_chunk;     /* capacity: largest n_chunk of a layer               */
   int32_t hidden_dim;    /* d_model of the hidden states (SRC_HIDDEN); rows of
                             whole 16-byte units                               */
+  int32_t inplace_stage_rows; /* in-place compaction (k_out == k): rows per
+                            (layer, KV head) reserved for kept rows that land
+                            behind their working-set row (audio rows behind a
+                            visual block that grew); 0: outputs may not alias
+                            the inputs.  See omnimem_select_compact.         */
 } omnimem_config;
 
 typedef struct {
@@ -122,7 +127,22 @@ typedef struct {
   void* hidden_out;         /* optional [M_l][hidden_dim] hidden states of the
                                kept rows (select_compact, shared selection)   */
   int64_t hidden_out_row_stride; /* elements                                 */
+  int64_t out_rows;         /* rows per KV head that k_out / v_out hold;
+                               0 -> N (select_compact)                        */
+  uint8_t* modality_out;    /* optional [out_rows] modality of the kept rows
+                               (select_compact); may equal `modality`         */
 } omnimem_layer;
+
+/* One layer's new chunk (Eq. 3): its K and V rows [H_kv][n_rows][d] and the
+ * modality of each row, in time order (input of omnimem_append). */
+typedef struct {
+  const void* k;
+  const void* v;
+  int64_t head_stride;      /* elements, shared by k and v                    */
+  int64_t row_stride;       /* elements, shared by k and v                    */
+  const uint8_t* modality;  /* [n_rows]: 0 visual, 1 audio                     */
+  int64_t n_rows;           /* must equal the layer descriptor's n_chunk      */
+} omnimem_chunk;
 
 typedef struct omnimem_ctx omnimem_ctx;
 
@@ -234,12 +254,51 @@ omnimem_status omnimem_allocate_fixed(omnimem_ctx* ctx, const omnimem_layer* lay
  * hidden).
  *   a, s     [L][H_kv][max_tokens] fp32; budgets [L][2] int32 (device).
  *   idx      optional [L][H_kv][max_tokens] int32 output of the kept rows.
- * k_out / v_out must not overlap k / v (ping-pong the cache buffers); the
- * caller sizes them for the budgets it passes.  Budgets are read on the
- * device and clamped to [0, K_mu]. */
+ * Budgets are read on the device and applied as M_v = min(max(budget_v, 0),
+ * K_v, out_rows) and M_a = min(max(budget_a, 0), K_a, out_rows - M_v): rows
+ * beyond a layer's output capacity are not kept, audio rows first.  A layer
+ * whose modality_out is given gets modality_out[i] = 0 for i < M_v and 1
+ * for M_v <= i < M_v + M_a (it may be the layer's own modality array).
+ *
+ * Outputs and inputs: k_out / v_out either do not overlap k, v or each
+ * other (out of place: the caller ping-pongs two caches), or they ARE k and
+ * v (same pointers and strides: in place, as the paper prunes each cache
+ * into its next self, Eqs. 2-5); any other overlap is INVALID_ARG.  In place
+ * needs cfg.inplace_stage_rows > 0 and gives bit for bit the out-of-place
+ * result.  Kept visual rows and most kept audio rows move toward the front
+ * and are moved in one ordered pass; kept audio rows that land behind their
+ * own row (when M_v exceeds the visual rows in front of them) are first
+ * copied to the context's staging rows.  If some (layer, KV head) needs more
+ * staging rows than cfg.inplace_stage_rows, the call moves no row of any
+ * layer (k, v and modality_out stay as they were; idx is written) and
+ * records the shortfall for omnimem_inplace_status.  The hidden states are
+ * never compacted in place: hidden_out must not overlap hidden. */
 omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* layers,
                                       const float* a, const float* s, const int32_t* budgets,
                                       int32_t* idx, hipStream_t stream);
+
+/* Status of the in-place compactions since the last query: OMNIMEM_OK, or
+ * OMNIMEM_ERR_CAPACITY when one of them needed more staging rows than the
+ * context reserves and so moved nothing (*rows_needed, if not null, gets
+ * the largest need; 0 when none), or OMNIMEM_ERR_HIP if an ordering wait of
+ * the in-place pass gave up (it waits only on work that has started, so
+ * this is not expected).  Synchronous: waits for the device, reads the
+ * context's record and clears it. */
+omnimem_status omnimem_inplace_status(omnimem_ctx* ctx, int64_t* rows_needed);
+
+/* Eq. (3): each layer's working set is its retained caches followed by the
+ * new chunk.  Copies chunks[l]'s K and V rows and modality to rows
+ * n_cache .. n_cache + n_chunk - 1 of layers[l].k, .v and .modality (the
+ * working-set buffers, written here: the caller owns them and they must be
+ * writable), for every layer, in one launch.  The retained rows 0 ..
+ * n_cache - 1 are not touched (after an in-place omnimem_select_compact
+ * with modality_out = modality they already hold the kept rows and their
+ * modality).  This is the write the model's prefill makes when it appends
+ * the chunk's K/V behind the cache.
+ * Errors: INVALID_ARG (null pointers, alignment, strides, n_rows differing
+ * from n_chunk, chunk rows overlapping the destination rows). */
+omnimem_status omnimem_append(omnimem_ctx* ctx, const omnimem_layer* layers, const omnimem_chunk* chunks,
+                              hipStream_t stream);
 
 /* Kernel timing for measurement.  While on, every kernel the context
  * launches is bracketed by two HIP events recorded on its launch stream

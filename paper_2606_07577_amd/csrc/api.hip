@@ -51,7 +51,8 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 
 static const char* kKernelNames[K_COUNT] = {
     "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact",
-    "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish", "layer_inputs"};
+    "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish", "layer_inputs",
+    "stage_moved_back", "gather_inplace", "append_chunk"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -105,6 +106,12 @@ bool overlaps(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a
 
 enum Need { NEED_Q = 1, NEED_K = 2, NEED_V = 4, NEED_OUT = 8 };
 
+// Compaction in place: the outputs are the working set itself.
+bool in_place(const omnimem_layer& L) {
+  return L.k_out == L.k && L.v_out == L.v && L.out_head_stride == L.kv_head_stride &&
+         L.out_row_stride == L.kv_row_stride;
+}
+
 omnimem_status validate(omnimem_ctx* ctx, const omnimem_layer* layers, int need) {
   if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
   if (!layers) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null layer array");
@@ -140,24 +147,43 @@ omnimem_status validate(omnimem_ctx* ctx, const omnimem_layer* layers, int need)
     }
     if (need & NEED_OUT) {
       if (!L.k_out || !L.v_out) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: null k_out or v_out", l);
-      if (!aligned16(L.k_out) || !aligned16(L.v_out) || (L.out_row_stride * esz) % 16 ||
-          (L.out_head_stride * esz) % 16)
-        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: outputs must be 16-byte aligned, strides of whole "
-                    "16-byte units", l);
+      if (L.out_rows < 0) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: out_rows < 0", l);
       const int64_t H = c.n_kv_heads;
-      const bool head_major = L.out_row_stride >= d && (H == 1 || L.out_head_stride >= n * L.out_row_stride);
-      const bool row_major = L.out_head_stride >= d && L.out_row_stride >= H * L.out_head_stride;
-      if (!head_major && !row_major)
-        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k_out/v_out must hold H_kv x N rows of d without "
-                    "overlap", l);
+      const int64_t cap = L.out_rows ? L.out_rows : n;
       uintptr_t k0, k1, v0, v1, o0, o1, p0, p1;
       extent(L.k, H, n, L.kv_head_stride, L.kv_row_stride, d, esz, &k0, &k1);
       extent(L.v, H, n, L.kv_head_stride, L.kv_row_stride, d, esz, &v0, &v1);
-      extent(L.k_out, H, n, L.out_head_stride, L.out_row_stride, d, esz, &o0, &o1);
-      extent(L.v_out, H, n, L.out_head_stride, L.out_row_stride, d, esz, &p0, &p1);
-      if (overlaps(o0, o1, k0, k1) || overlaps(o0, o1, v0, v1) || overlaps(p0, p1, k0, k1) ||
-          overlaps(p0, p1, v0, v1) || overlaps(o0, o1, p0, p1))
-        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k_out/v_out overlap k, v or each other", l);
+      if (in_place(L)) {
+        if (c.inplace_stage_rows <= 0)
+          return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k_out/v_out are k/v (in place), but the context "
+                      "reserves no staging rows (inplace_stage_rows = 0)", l);
+        if (overlaps(k0, k1, v0, v1))
+          return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: in place, k and v must not overlap", l);
+        o0 = k0; o1 = k1; p0 = v0; p1 = v1;
+      } else {
+        if (!aligned16(L.k_out) || !aligned16(L.v_out) || (L.out_row_stride * esz) % 16 ||
+            (L.out_head_stride * esz) % 16)
+          return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: outputs must be 16-byte aligned, strides of whole "
+                      "16-byte units", l);
+        const bool head_major = L.out_row_stride >= d && (H == 1 || L.out_head_stride >= cap * L.out_row_stride);
+        const bool row_major = L.out_head_stride >= d && L.out_row_stride >= H * L.out_head_stride;
+        if (!head_major && !row_major)
+          return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k_out/v_out must hold H_kv x out_rows rows of d "
+                      "without overlap", l);
+        extent(L.k_out, H, cap, L.out_head_stride, L.out_row_stride, d, esz, &o0, &o1);
+        extent(L.v_out, H, cap, L.out_head_stride, L.out_row_stride, d, esz, &p0, &p1);
+        if (overlaps(o0, o1, k0, k1) || overlaps(o0, o1, v0, v1) || overlaps(p0, p1, k0, k1) ||
+            overlaps(p0, p1, v0, v1) || overlaps(o0, o1, p0, p1))
+          return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k_out/v_out overlap k, v or each other without "
+                      "being k and v themselves", l);
+      }
+      if (L.modality_out) {
+        const uintptr_t m0 = reinterpret_cast<uintptr_t>(L.modality_out), m1 = m0 + (uintptr_t)cap;
+        const uintptr_t i0 = reinterpret_cast<uintptr_t>(L.modality), i1 = i0 + (uintptr_t)n;
+        if ((m0 != i0 && overlaps(m0, m1, i0, i1)) || overlaps(m0, m1, o0, o1) || overlaps(m0, m1, p0, p1))
+          return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: modality_out overlaps the outputs, or the input "
+                      "modality without being it", l);
+      }
     }
   }
   return OMNIMEM_OK;
@@ -194,8 +220,45 @@ omnimem_status validate_hidden(omnimem_ctx* ctx, const omnimem_layer* layers, bo
   return OMNIMEM_OK;
 }
 
+// New chunk rows of each layer (omnimem_append).
+omnimem_status validate_append(omnimem_ctx* ctx, const omnimem_layer* layers, const omnimem_chunk* chunks) {
+  if (!chunks) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null chunk array");
+  const omnimem_config& c = ctx->cfg;
+  const int64_t d = c.head_dim, H = c.n_kv_heads;
+  const size_t esz = elt_size(c);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const omnimem_layer& L = layers[l];
+    const omnimem_chunk& C = chunks[l];
+    if (C.n_rows != L.n_chunk)
+      return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: chunk has %lld rows, the descriptor's n_chunk is %lld", l,
+                  (long long)C.n_rows, (long long)L.n_chunk);
+    if (L.n_chunk == 0) continue;
+    if (!C.k || !C.v || !C.modality)
+      return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: null chunk k, v or modality", l);
+    if (!aligned16(C.k) || !aligned16(C.v) || C.row_stride < d || C.head_stride < 0 || (C.row_stride * esz) % 16 ||
+        (C.head_stride * esz) % 16)
+      return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: chunk k/v must be 16-byte aligned with row stride >= d "
+                  "and strides of whole 16-byte units", l);
+    const char* kd = static_cast<const char*>(L.k) + L.n_cache * L.kv_row_stride * (int64_t)esz;
+    const char* vd = static_cast<const char*>(L.v) + L.n_cache * L.kv_row_stride * (int64_t)esz;
+    uintptr_t a0, a1, b0, b1, x0, x1, y0, y1;
+    extent(kd, H, L.n_chunk, L.kv_head_stride, L.kv_row_stride, d, esz, &a0, &a1);
+    extent(vd, H, L.n_chunk, L.kv_head_stride, L.kv_row_stride, d, esz, &b0, &b1);
+    extent(C.k, H, L.n_chunk, C.head_stride, C.row_stride, d, esz, &x0, &x1);
+    extent(C.v, H, L.n_chunk, C.head_stride, C.row_stride, d, esz, &y0, &y1);
+    const uintptr_t m0 = reinterpret_cast<uintptr_t>(L.modality) + (uintptr_t)L.n_cache, m1 = m0 + L.n_chunk;
+    const uintptr_t c0 = reinterpret_cast<uintptr_t>(C.modality), c1 = c0 + L.n_chunk;
+    if (overlaps(a0, a1, b0, b1) || overlaps(a0, a1, x0, x1) || overlaps(a0, a1, y0, y1) ||
+        overlaps(b0, b1, x0, x1) || overlaps(b0, b1, y0, y1) || overlaps(m0, m1, c0, c1))
+      return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: the chunk rows overlap the rows they are copied to, or "
+                  "the destination k and v rows overlap", l);
+  }
+  return OMNIMEM_OK;
+}
+
 // Copy the descriptor table to the device unless it equals the last one.
-omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t st, const LayerDesc** dev) {
+omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t st, const LayerDesc** dev,
+                      const omnimem_chunk* chunks = nullptr) {
   const int L = ctx->cfg.n_layers;
   const double log2e = 1.4426950408889634;
   std::vector<LayerDesc> t(L);
@@ -213,6 +276,13 @@ omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t
       x.hidden_rs = s.hidden_row_stride; x.hidden_out_rs = s.hidden_out_row_stride;
     }
     x.n_cache = (int32_t)s.n_cache; x.n_chunk = (int32_t)s.n_chunk; x.n = (int32_t)(s.n_cache + s.n_chunk);
+    x.mod_out = s.modality_out;
+    x.out_cap = (int32_t)std::min<int64_t>(s.out_rows > 0 ? s.out_rows : x.n, x.n);
+    x.inplace = (s.k_out && in_place(s)) ? 1 : 0;
+    if (chunks) {
+      x.ck = chunks[l].k; x.cv = chunks[l].v; x.cmod = chunks[l].modality;
+      x.c_hs = chunks[l].head_stride; x.c_rs = chunks[l].row_stride;
+    }
     const double scale = s.sm_scale != 0.0f ? (double)s.sm_scale : 1.0 / std::sqrt((double)ctx->cfg.head_dim);
     x.scale_log2 = (float)(scale * log2e);
   }
@@ -316,6 +386,8 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "hidden_dim %d: the all-pairs maximum on hidden states takes "
                   "multiples of 64", c.hidden_dim);
   }
+  if (c.inplace_stage_rows < 0 || c.inplace_stage_rows > c.max_tokens)
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "inplace_stage_rows %d: need 0 .. max_tokens", c.inplace_stage_rows);
   if (!std::isfinite(c.lambda) || c.lambda < 0.0f || !(c.ratio_r > 0.0f) || !(c.temperature > 0.0f) ||
       !(c.b_min_frac >= 0.0f) || !(c.b_max_frac >= c.b_min_frac) || !std::isfinite(c.b_max_frac))
     return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "need lambda >= 0, r > 0, T > 0, 0 <= b_min_frac <= b_max_frac");
@@ -337,6 +409,7 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
   const size_t L = c.n_layers, Hq = c.n_q_heads, Hkv = c.n_kv_heads, T = c.max_tokens, Cm = dm.max_chunk;
   Workspace& ws = ctx->ws;
   ws.gram_grid = ctx->max_workgroups;
+  ws.stage_rows = c.inplace_stage_rows;
   const size_t elt = c.dtype == OMNIMEM_BF16 ? 2 : 4;
   if ((e = dalloc(ctx, &ws.desc, (size_t)kSlots * L)) != hipSuccess ||
       (e = dalloc(ctx, &ws.lse_part, L * Hq * (size_t)dm.qb * kMaxSeg * kScoreBlock)) != hipSuccess ||
@@ -353,7 +426,14 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.idx, L * Hkv * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.keys, L * Hkv * T)) != hipSuccess ||
-      (c.shared_selection && (e = dalloc(ctx, &ws.layer_as, 2 * L * T)) != hipSuccess)) {
+      (c.shared_selection && (e = dalloc(ctx, &ws.layer_as, 2 * L * T)) != hipSuccess) ||
+      (e = dalloc(ctx, &ws.ctl, 4)) != hipSuccess ||
+      (c.inplace_stage_rows > 0 &&
+       ((e = dalloc(ctx, reinterpret_cast<char**>(&ws.stage),
+                    2 * L * Hkv * (size_t)c.inplace_stage_rows * (size_t)c.head_dim * elt)) != hipSuccess ||
+        (e = dalloc(ctx, &ws.slot_of, L * Hkv * T)) != hipSuccess ||
+        (e = dalloc(ctx, &ws.read_flags, L * Hkv * (size_t)((T + 63) / 64))) != hipSuccess ||
+        (e = dalloc(ctx, &ws.tickets, L * Hkv * 32)) != hipSuccess))) {
     omnimem_destroy(ctx);
     return fail(nullptr, OMNIMEM_ERR_HIP, "workspace allocation: %s", hipGetErrorString(e));
   }
@@ -363,6 +443,10 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
     return fail(nullptr, OMNIMEM_ERR_HIP, "pinned descriptor ring: %s", hipGetErrorString(e));
   }
   ctx->pinned = static_cast<LayerDesc*>(pinned);
+  if ((e = hipMemset(ws.ctl, 0, 4 * sizeof(int))) != hipSuccess) {
+    omnimem_destroy(ctx);
+    return fail(nullptr, OMNIMEM_ERR_HIP, "control words: %s", hipGetErrorString(e));
+  }
   for (int i = 0; i < kSlots; ++i) {
     if ((e = hipEventCreateWithFlags(&ctx->ev[i], hipEventDisableTiming)) != hipSuccess) {
       omnimem_destroy(ctx);
@@ -506,12 +590,55 @@ omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* lay
     if ((st = validate_hidden(ctx, layers, true)) != OMNIMEM_OK) return st;
     for (int l = 0; l < ctx->cfg.n_layers; ++l) hidden = hidden || layers[l].hidden_out != nullptr;
   }
+  int n_inplace = 0;  // layers compacted in place
+  for (int l = 0; l < ctx->cfg.n_layers; ++l) n_inplace += in_place(layers[l]) ? 1 : 0;
+  const int inplace = n_inplace == 0 ? 0 : n_inplace == ctx->cfg.n_layers ? 2 : 1;
+  int64_t max_n = 1;
+  for (int l = 0; l < ctx->cfg.n_layers; ++l) max_n = std::max<int64_t>(max_n, layers[l].n_cache + layers[l].n_chunk);
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
   return finish(ctx, launch_select_compact(ctx->dm, ctx->cfg.dtype, ctx->cfg.lambda, ctx->cfg.shared_selection ? 1 : 0,
-                                           hidden, dev, ctx->ws, a, s, budgets, idx, stream),
+                                           hidden, inplace, (int)max_n, dev, ctx->ws, a, s, budgets, idx, stream),
                 stream, "omnimem_select_compact launch");
+}
+
+omnimem_status omnimem_inplace_status(omnimem_ctx* ctx, int64_t* rows_needed) {
+  if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
+  if (rows_needed) *rows_needed = 0;
+  omnimem_status st = set_device(ctx);
+  if (st != OMNIMEM_OK) return st;
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(ctx, e, "inplace status wait");
+  int words[4] = {0, 0, 0, 0};
+  if ((e = hipMemcpy(words, ctx->ws.ctl, sizeof words, hipMemcpyDeviceToHost)) != hipSuccess)
+    return hip_fail(ctx, e, "inplace status read");
+  const int zero[2] = {0, 0};
+  if ((e = hipMemcpy(ctx->ws.ctl + 2, zero, sizeof zero, hipMemcpyHostToDevice)) != hipSuccess)
+    return hip_fail(ctx, e, "inplace status clear");
+  if (rows_needed) *rows_needed = words[2];
+  if (words[3] != 0)
+    return fail(ctx, OMNIMEM_ERR_HIP, "%d ordering waits of the in-place pass gave up", words[3]);
+  if (words[2] != 0)
+    return fail(ctx, OMNIMEM_ERR_CAPACITY, "an in-place compaction needed %d staging rows per (layer, KV head); "
+                "the context reserves %d: that call moved no row", words[2], ctx->cfg.inplace_stage_rows);
+  ctx->err.clear();
+  return OMNIMEM_OK;
+}
+
+omnimem_status omnimem_append(omnimem_ctx* ctx, const omnimem_layer* layers, const omnimem_chunk* chunks,
+                              hipStream_t stream) {
+  omnimem_status st = validate(ctx, layers, NEED_K | NEED_V);
+  if (st != OMNIMEM_OK) return st;
+  if ((st = validate_append(ctx, layers, chunks)) != OMNIMEM_OK) return st;
+  int64_t max_rows = 0;
+  for (int l = 0; l < ctx->cfg.n_layers; ++l) max_rows = std::max<int64_t>(max_rows, layers[l].n_chunk);
+  if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
+  const LayerDesc* dev = nullptr;
+  if ((st = upload(ctx, layers, stream, &dev, chunks)) != OMNIMEM_OK) return st;
+  if (max_rows == 0) return finish(ctx, hipSuccess, stream, "omnimem_append");
+  return finish(ctx, launch_append(ctx->dm, ctx->cfg.dtype, dev, ctx->ws, max_rows, stream), stream,
+                "omnimem_append launch");
 }
 
 omnimem_status omnimem_profile(omnimem_ctx* ctx, int32_t on) {

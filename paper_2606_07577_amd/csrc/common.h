@@ -38,6 +38,14 @@ struct LayerDesc {
   const void* hidden;           // [N][dh] hidden states (redundancy source 2)
   void* hidden_out;             // kept rows' hidden states, or null
   int64_t hidden_rs, hidden_out_rs;
+  uint8_t* mod_out;             // modality of the kept rows, or null
+  int32_t out_cap;              // rows per head of k_out / v_out
+  int32_t inplace;              // 1: k_out, v_out are k, v (compaction in place)
+  // omnimem_append only: the layer's new chunk rows.
+  const void* ck;
+  const void* cv;
+  const uint8_t* cmod;
+  int64_t c_hs, c_rs;
 };
 
 // Sizes fixed for a context.
@@ -211,7 +219,8 @@ constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
 // ---------------------------------------------------------------------------
 enum KernelId {
   K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
-  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_LAYER_IN, K_COUNT
+  K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_LAYER_IN,
+  K_STAGE, K_GATHER_IP, K_APPEND, K_COUNT
 };
 struct Profiler;
 void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
@@ -245,6 +254,14 @@ struct Workspace {
   int* idx;               // [L][Hkv][max_tokens] fallback for the idx output
   uint32_t* keys;         // [L][Hkv][max_tokens]
   float* layer_as;        // [2][L][max_tokens] layer-shared selection inputs (null without it)
+  // In-place compaction (null / 0 unless the context reserves staging rows).
+  int stage_rows;         // staging rows per (layer, KV head)
+  void* stage;            // [2][L][Hkv][stage_rows][d] staged K, then V rows
+  int* slot_of;           // [L][Hkv][max_tokens] slot that reads row j (-1: dropped)
+  int* read_flags;        // [L][Hkv][tiles] 1 once a 64-slot tile has read its rows
+  int* ctl;               // [1] this call's staging need beyond the reserve (0: none), [2] largest need
+                          // and [3] wait time-outs since the last query ([0] unused)
+  int* tickets;           // [L * Hkv][32] tile tickets of the in-place gather, one 128-byte line each
   Profiler* prof;         // null unless timing is on
 };
 
@@ -269,9 +286,12 @@ hipError_t launch_calibration_budgets(const Dims& dm, const Workspace& ws, int64
 hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const float* a,
                                  const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
                                  float* stats, hipStream_t st);
-hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, const LayerDesc* desc,
-                                 const Workspace& ws, const float* a, const float* s,
-                                 const int32_t* budgets, int32_t* idx, hipStream_t st);
+hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, int inplace,
+                                 int max_n, const LayerDesc* desc, const Workspace& ws, const float* a,
+                                 const float* s, const int32_t* budgets, int32_t* idx,
+                                 hipStream_t st);  // inplace: 0 none, 1 some, 2 all; max_n: largest N
+hipError_t launch_append(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws, int64_t max_rows,
+                         hipStream_t st);
 
 // One LDS stage of kScoreTile rows of D elements, unpadded.  The 16-byte chunk c
 // of row r is stored at chunk position c ^ (r & XM): the 16 rows that a

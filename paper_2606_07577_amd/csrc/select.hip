@@ -79,7 +79,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
                                                         const float* __restrict__ a, const float* __restrict__ s,
                                                         const int32_t* __restrict__ budgets,
                                                         uint32_t* __restrict__ keys, int32_t* __restrict__ idx,
-                                                        int* __restrict__ eff) {
+                                                        int* __restrict__ eff, int* __restrict__ slot_of,
+                                                        int* __restrict__ ctl) {
   __shared__ uint32_t skey[kLdsKeys];
   __shared__ int hist[kBins];
   __shared__ int wave_tot[kSelWaves];
@@ -91,6 +92,10 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   const int mu = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
   const int N = layers[l].n;
   const uint8_t* mod = layers[l].mod;
+  const int cap = layers[l].out_cap;           // rows per head of the output
+  const bool want_slots = layers[l].inplace != 0 && slot_of != nullptr;
+  if (ctl != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0)
+    ctl[1] = 0;  // staging rows needed beyond the reserve, this call
   const int64_t off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
   const float* ag = a + (SHARED ? (int64_t)l * dm.max_tokens : off);
   const float* sg = s + (SHARED ? (int64_t)l * dm.max_tokens : off);
@@ -180,9 +185,11 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
       run += __popcll(bal);
     }
   }
-  const int M = min(max(bud_mu, 0), K);
+  // Budgets as applied: each modality's within its rows, visual first
+  // within the output capacity, audio in what remains.
   const int Kv = mu ? N - K : K;
-  const int Mv = mu ? min(max(bud_v, 0), Kv) : M;
+  const int Mv = min(min(max(bud_v, 0), Kv), cap);
+  const int M = mu ? min(min(max(bud_mu, 0), K), cap - Mv) : Mv;
   if (g == 0 && threadIdx.x == 0) eff[2 * l + mu] = M;
   const int out0 = mu ? Mv : 0;
 
@@ -349,7 +356,11 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   }
   int sel_tot;
   const int out_base = wave_scan(wsel, wt_sel, &sel_tot) + out0;
-  if (wsel == 0) return;
+  if (wsel == 0 && !want_slots) return;
+  // In place, every member row also records the slot that reads it (-1:
+  // dropped), for the ordering of the in-place gather.
+  int* so = want_slots ? slot_of + off : nullptr;
+  const int heads = SHARED ? dm.Hkv : 1;
   for (int i0 = 0, run = rank_base, eqr = eq_base, o = out_base; i0 < R; i0 += kGrp) {
     unsigned long long sb[kGrp];
     if (bits_ok) {
@@ -360,13 +371,15 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
     }
 #pragma unroll
     for (int u = 0; u < kGrp; ++u) {
+      const int row = wrow0 + (i0 + u) * 64 + lane;
       if ((sb[u] >> lane) & 1ull) {
-        const int slot = o + __popcll(sb[u] & lt), row = wrow0 + (i0 + u) * 64 + lane;
-        if constexpr (SHARED) {
-          for (int h = 0; h < dm.Hkv; ++h) ig[(int64_t)h * dm.max_tokens + slot] = row;
-        } else {
-          ig[slot] = row;
+        const int slot = o + __popcll(sb[u] & lt);
+        for (int h = 0; h < heads; ++h) {
+          ig[(int64_t)h * dm.max_tokens + slot] = row;
+          if (so) so[(int64_t)h * dm.max_tokens + row] = slot;
         }
+      } else if (so && i0 + u < R && row < N && member_at(i0 + u, row)) {
+        for (int h = 0; h < heads; ++h) so[(int64_t)h * dm.max_tokens + row] = -1;
       }
       o += __popcll(sb[u]);
     }
@@ -375,15 +388,19 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void gather_compact(const LayerDesc* __restrict__ layers, Dims dm,
-                                                      const int32_t* __restrict__ idx, const int* __restrict__ eff) {
+                                                      const int32_t* __restrict__ idx, const int* __restrict__ eff,
+                                                      const int* __restrict__ ctl) {
   constexpr int CPR = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
   constexpr int RPP = 256 / CPR;                // rows per pass
   constexpr int ROWS = 64;                      // rows per workgroup
   const int l = blockIdx.z, g = blockIdx.y;
   const LayerDesc Ld = layers[l];
-  const int M = eff[2 * l] + eff[2 * l + 1];
+  if (Ld.inplace || (ctl && ctl[1] != 0)) return;  // in-place layer, or a call that moves nothing
+  const int Mv = eff[2 * l], M = Mv + eff[2 * l + 1];
   const int i0 = blockIdx.x * ROWS;
   if (i0 >= M) return;
+  if (g == 0 && Ld.mod_out && threadIdx.x < ROWS && i0 + (int)threadIdx.x < M)
+    Ld.mod_out[i0 + threadIdx.x] = i0 + (int)threadIdx.x < Mv ? 0 : 1;
   const int32_t* ig = idx + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
   const T* k = reinterpret_cast<const T*>(Ld.k) + (int64_t)g * Ld.kv_hs;
   const T* v = reinterpret_cast<const T*>(Ld.v) + (int64_t)g * Ld.kv_hs;
@@ -439,10 +456,11 @@ __global__ __launch_bounds__(256) void layer_inputs(const LayerDesc* __restrict_
 // hidden_out[i] = hidden[idx[l][0][i]], one wave per row, 16 bytes a lane.
 template <typename T>
 __global__ __launch_bounds__(256) void gather_hidden(const LayerDesc* __restrict__ layers, Dims dm,
-                                                     const int32_t* __restrict__ idx, const int* __restrict__ eff) {
+                                                     const int32_t* __restrict__ idx, const int* __restrict__ eff,
+                                                     const int* __restrict__ ctl) {
   const int l = blockIdx.y;
   const LayerDesc Ld = layers[l];
-  if (!Ld.hidden_out) return;
+  if (!Ld.hidden_out || (ctl && ctl[1] != 0)) return;
   const int M = eff[2 * l] + eff[2 * l + 1];
   const int i = (int)blockIdx.x * 4 + wave_id(), lane = threadIdx.x & 63;
   if (i >= M) return;
@@ -453,18 +471,240 @@ __global__ __launch_bounds__(256) void gather_hidden(const LayerDesc* __restrict
   for (int c = lane; c < dm.dh / EPP; c += 64) *reinterpret_cast<uint4*>(dst + c * EPP) = gload16(src + c * EPP);
 }
 
+// ---------------------------------------------------------------------------
+// Compaction in place (k_out, v_out are k, v).  Slot i of (layer, KV head)
+// takes row p_i = idx[i].  Visual slots never take a row in front of them
+// (p_i >= i: the i-th kept visual row has at least i rows before it), and
+// neither do audio slots except a leading run of them, those whose row has
+// fewer than M_v visual rows in front of it (M_v + j - p_j does not grow
+// with j, so these are the first ones).  That run is copied out to the
+// staging rows first (stage_moved_back); every other slot is then filled
+// in one pass in which the 64-slot tile t writes its rows only after each
+// earlier tile that reads one of those rows has loaded it (flags set after
+// the loads).  The workgroups of one (layer, KV head) take its tiles as
+// tickets from a counter of their own, in their order of starting, and the
+// wait of a tile is only on tiles of the same (layer, KV head) with smaller
+// tickets, whose loading phase waits for nothing: every wait ends.  One
+// counter per (layer, KV head), each on a cache line of its own, keeps the
+// ticket atomics from queueing on one address.
+// ---------------------------------------------------------------------------
+constexpr int kGatherRows = 64;      // slots per workgroup of the gathers
+constexpr int kSpinLimit = 1 << 22;  // polls before a wait gives up (never reached when the order holds)
+constexpr int kTicketStride = 32;    // ints between two ticket counters (one 128-byte line each)
+
+// Rows of a tile, 16 bytes per lane: lane group `sub` of the row that
+// thread t handles in pass p is t / CPR + p * RPP.
 template <typename T, int D>
-void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const int32_t* idx, hipStream_t st) {
-  dim3 grid((unsigned)((dm.max_tokens + 63) / 64), dm.Hkv, dm.L);
-  OMNIMEM_LAUNCH(ws, K_GATHER, st, gather_compact<T, D><<<grid, 256, 0, st>>>(desc, dm, idx, ws.eff));
+struct RowCopy {
+  static constexpr int CPR = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
+  static constexpr int RPP = 256 / CPR;                // rows per pass
+  static constexpr int NP = kGatherRows / RPP;         // passes
+  static constexpr int EPC = 16 / (int)sizeof(T);
+};
+
+// Zero the read flags and ticket counters, and stage the slots that take a
+// row in front of them.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void stage_moved_back(const LayerDesc* __restrict__ layers, Dims dm,
+                                                        const int32_t* __restrict__ idx, const int* __restrict__ eff,
+                                                        Workspace ws) {
+  using RC = RowCopy<T, D>;
+  const int l = blockIdx.z, g = blockIdx.y, tile = blockIdx.x;
+  const int u = l * dm.Hkv + g;
+  const int tiles = (int)((dm.max_tokens + kGatherRows - 1) / kGatherRows);
+  if (threadIdx.x == 0) {
+    ws.read_flags[(int64_t)u * tiles + tile] = 0;
+    if (tile == 0) ws.tickets[u * kTicketStride] = 0;
+  }
+  const LayerDesc Ld = layers[l];
+  if (!Ld.inplace) return;
+  const int Mv = eff[2 * l], M = Mv + eff[2 * l + 1];
+  const int i0 = tile * kGatherRows;
+  if (i0 >= M || i0 + kGatherRows <= Mv) return;
+  const int32_t* ig = idx + (int64_t)u * dm.max_tokens;
+  const T* k = reinterpret_cast<const T*>(Ld.k) + (int64_t)g * Ld.kv_hs;
+  const T* v = reinterpret_cast<const T*>(Ld.v) + (int64_t)g * Ld.kv_hs;
+  const int64_t stage_len = (int64_t)dm.L * dm.Hkv * ws.stage_rows * D;
+  T* sk = reinterpret_cast<T*>(ws.stage) + (int64_t)u * ws.stage_rows * D;
+  T* sv = sk + stage_len;
+  const int sub = threadIdx.x % RC::CPR;
+#pragma unroll
+  for (int p = 0; p < RC::NP; ++p) {
+    const int i = i0 + (int)threadIdx.x / RC::CPR + p * RC::RPP;
+    if (i < Mv || i >= M) continue;
+    const int row = ig[i];
+    if (row >= i || row < 0) continue;  // moves to the front or stays
+    const int j = i - Mv;
+    if (j >= ws.stage_rows) {
+      if (sub == 0) atomicMax(&ws.ctl[1], j + 1);
+      continue;
+    }
+    const int64_t e = (int64_t)row * Ld.kv_rs + sub * RC::EPC;
+    const uint4 kx = gload16(k + e), vx = gload16(v + e);
+    *reinterpret_cast<uint4*>(sk + (int64_t)j * D + sub * RC::EPC) = kx;
+    *reinterpret_cast<uint4*>(sv + (int64_t)j * D + sub * RC::EPC) = vx;
+  }
+}
+
+// Grid: `active` workgroups per (layer, KV head), unit u = blockIdx.x % units;
+// `tiles` is the row stride of the flag array.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void gather_inplace(const LayerDesc* __restrict__ layers, Dims dm,
+                                                      const int32_t* __restrict__ idx, const int* __restrict__ eff,
+                                                      Workspace ws, int units, int tiles, int active) {
+  using RC = RowCopy<T, D>;
+  __shared__ int s_ticket;
+  const int u = (int)(blockIdx.x % (unsigned)units);
+  if (threadIdx.x == 0) s_ticket = atomicAdd(&ws.tickets[u * kTicketStride], 1);
+  __syncthreads();
+  const int tile = s_ticket;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && ws.ctl[1] > ws.ctl[2]) ws.ctl[2] = ws.ctl[1];  // largest shortfall
+  if (tile >= active) return;
+  const int l = u / dm.Hkv, g = u % dm.Hkv;
+  const LayerDesc Ld = layers[l];
+  if (!Ld.inplace || ws.ctl[1] != 0) return;
+  const int Mv = eff[2 * l], M = Mv + eff[2 * l + 1];
+  const int i0 = tile * kGatherRows;
+  if (i0 >= M) return;  // no slot here, and no later tile waits for this one
+  const int32_t* ig = idx + (int64_t)u * dm.max_tokens;
+  T* k = static_cast<T*>(Ld.k_out) + (int64_t)g * Ld.kv_hs;  // in place: k_out is k
+  T* v = static_cast<T*>(Ld.v_out) + (int64_t)g * Ld.kv_hs;
+  const int64_t stage_len = (int64_t)dm.L * dm.Hkv * ws.stage_rows * D;
+  const T* sk = reinterpret_cast<const T*>(ws.stage) + (int64_t)u * ws.stage_rows * D;
+  const T* sv = sk + stage_len;
+  const int sub = threadIdx.x % RC::CPR;
+
+  // Loading phase: each slot's row, from the working set (a row at or
+  // behind the slot) or from the staging rows.
+  int slot[RC::NP];
+  bool move[RC::NP];
+  uint4 kx[RC::NP], vx[RC::NP];
+#pragma unroll
+  for (int p = 0; p < RC::NP; ++p) {
+    const int i = i0 + (int)threadIdx.x / RC::CPR + p * RC::RPP;
+    slot[p] = i;
+    const int row = i < M ? ig[i] : i;
+    move[p] = false;
+    if (row > i && row < Ld.n) {
+      const int64_t e = (int64_t)row * Ld.kv_rs + sub * RC::EPC;
+      kx[p] = gload16(k + e);
+      vx[p] = gload16(v + e);
+      move[p] = true;
+    } else if (row < i && row >= 0 && i >= Mv && i - Mv < ws.stage_rows) {
+      const int64_t e = (int64_t)(i - Mv) * D + sub * RC::EPC;
+      kx[p] = gload16(sk + e);
+      vx[p] = gload16(sv + e);
+      move[p] = true;
+    }
+  }
+  dma_wait();        // this wave's loads have returned
+  __syncthreads();   // ... and every other wave's
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&ws.read_flags[(int64_t)u * tiles + tile], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // Each row this tile overwrites must have been loaded by the slot that
+  // takes it: by this tile (the barrier above), by a staging copy (a later
+  // slot), or by an earlier tile, whose flag is awaited here.
+  if (threadIdx.x < kGatherRows) {
+    const int i = i0 + (int)threadIdx.x;
+    int wait_tile = -1;
+    if (i < M && ig[i] != i) {
+      const int reader = ws.slot_of[(int64_t)u * dm.max_tokens + i];
+      if (reader >= 0 && reader < i0) wait_tile = reader / kGatherRows;
+    }
+    if (wait_tile >= 0) {
+      const int* f = &ws.read_flags[(int64_t)u * tiles + wait_tile];
+      int polls = 0;
+      while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+        __builtin_amdgcn_s_sleep(2);
+        if (++polls == kSpinLimit) {
+          atomicAdd(&ws.ctl[3], 1);
+          break;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // Writing phase.
+#pragma unroll
+  for (int p = 0; p < RC::NP; ++p) {
+    if (!move[p]) continue;
+    const int64_t e = (int64_t)slot[p] * Ld.kv_rs + sub * RC::EPC;
+    *reinterpret_cast<uint4*>(k + e) = kx[p];
+    *reinterpret_cast<uint4*>(v + e) = vx[p];
+  }
+  if (g == 0 && Ld.mod_out && threadIdx.x < kGatherRows && i0 + (int)threadIdx.x < M)
+    Ld.mod_out[i0 + threadIdx.x] = i0 + (int)threadIdx.x < Mv ? 0 : 1;
+}
+
+// Eq. (3): the chunk's K, V rows and modality behind each layer's retained
+// rows; 64 rows of one (layer, KV head) per workgroup.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void append_chunk(const LayerDesc* __restrict__ layers, Dims dm) {
+  using RC = RowCopy<T, D>;
+  const int l = blockIdx.z, g = blockIdx.y;
+  const LayerDesc Ld = layers[l];
+  const int i0 = blockIdx.x * kGatherRows;
+  if (i0 >= Ld.n_chunk) return;
+  const T* ck = reinterpret_cast<const T*>(Ld.ck) + (int64_t)g * Ld.c_hs;
+  const T* cv = reinterpret_cast<const T*>(Ld.cv) + (int64_t)g * Ld.c_hs;
+  T* k = const_cast<T*>(reinterpret_cast<const T*>(Ld.k)) + (int64_t)g * Ld.kv_hs;
+  T* v = const_cast<T*>(reinterpret_cast<const T*>(Ld.v)) + (int64_t)g * Ld.kv_hs;
+  const int sub = threadIdx.x % RC::CPR;
+  uint4 kx[RC::NP], vx[RC::NP];
+#pragma unroll
+  for (int p = 0; p < RC::NP; ++p) {
+    const int i = i0 + (int)threadIdx.x / RC::CPR + p * RC::RPP;
+    if (i < Ld.n_chunk) {
+      const int64_t e = (int64_t)i * Ld.c_rs + sub * RC::EPC;
+      kx[p] = gload16(ck + e);
+      vx[p] = gload16(cv + e);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < RC::NP; ++p) {
+    const int i = i0 + (int)threadIdx.x / RC::CPR + p * RC::RPP;
+    if (i < Ld.n_chunk) {
+      const int64_t e = (int64_t)(Ld.n_cache + i) * Ld.kv_rs + sub * RC::EPC;
+      *reinterpret_cast<uint4*>(k + e) = kx[p];
+      *reinterpret_cast<uint4*>(v + e) = vx[p];
+    }
+  }
+  if (g == 0 && threadIdx.x < kGatherRows && i0 + (int)threadIdx.x < Ld.n_chunk) {
+    uint8_t* mod = const_cast<uint8_t*>(Ld.mod);
+    mod[Ld.n_cache + i0 + threadIdx.x] = gload<uint8_t>(Ld.cmod + i0 + threadIdx.x) ? 1 : 0;
+  }
+}
+
+// inplace: 0 no layer in place, 1 some, 2 all.  max_n: the largest N of
+// the call's layers (no layer keeps more rows).
+template <typename T, int D>
+void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, const int32_t* idx, int inplace,
+                   int max_n, hipStream_t st) {
+  const int tiles = (int)((dm.max_tokens + kGatherRows - 1) / kGatherRows);
+  const int active = (max_n + kGatherRows - 1) / kGatherRows;
+  const dim3 grid((unsigned)active, dm.Hkv, dm.L);
+  const int* ctl = ws.stage_rows > 0 ? ws.ctl : nullptr;
+  if (inplace < 2)
+    OMNIMEM_LAUNCH(ws, K_GATHER, st, gather_compact<T, D><<<grid, 256, 0, st>>>(desc, dm, idx, ws.eff, ctl));
+  if (inplace > 0) {
+    const int units = dm.L * dm.Hkv;
+    OMNIMEM_LAUNCH(ws, K_STAGE, st, stage_moved_back<T, D><<<grid, 256, 0, st>>>(desc, dm, idx, ws.eff, ws));
+    OMNIMEM_LAUNCH(ws, K_GATHER_IP, st,
+                   gather_inplace<T, D><<<(unsigned)(units * active), 256, 0, st>>>(desc, dm, idx, ws.eff, ws,
+                                                                                     units, tiles, active));
+  }
 }
 
 }  // namespace
 
-hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, const LayerDesc* desc,
-                                 const Workspace& ws, const float* a, const float* s, const int32_t* budgets,
-                                 int32_t* idx, hipStream_t st) {
+hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, int inplace,
+                                 int max_n, const LayerDesc* desc, const Workspace& ws, const float* a,
+                                 const float* s, const int32_t* budgets, int32_t* idx, hipStream_t st) {
   int32_t* ix = idx ? idx : ws.idx;
+  int* slot_of = inplace ? ws.slot_of : nullptr;
+  int* ctl = ws.stage_rows > 0 ? ws.ctl : nullptr;
   if (shared) {
     float* la = ws.layer_as;
     float* ls = ws.layer_as + (size_t)dm.L * dm.max_tokens;
@@ -472,24 +712,37 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int sh
     OMNIMEM_LAUNCH(ws, K_LAYER_IN, st, layer_inputs<<<gtok, 256, 0, st>>>(desc, dm, a, s, la, ls));
     OMNIMEM_LAUNCH(ws, K_TOPK, st,
                    psi_topk<true><<<dim3(2, 1, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, la, ls, budgets, ws.keys,
-                                                                            ix, ws.eff));
+                                                                            ix, ws.eff, slot_of, ctl));
   } else
     OMNIMEM_LAUNCH(ws, K_TOPK, st,
                    psi_topk<false><<<dim3(2, dm.Hkv, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets,
-                                                                                  ws.keys, ix, ws.eff));
+                                                                                  ws.keys, ix, ws.eff, slot_of, ctl));
   if (dtype == 0) {
-    if (dm.d == 128) launch_gather<uint16_t, 128>(dm, desc, ws, ix, st);
-    else launch_gather<uint16_t, 64>(dm, desc, ws, ix, st);
+    if (dm.d == 128) launch_gather<uint16_t, 128>(dm, desc, ws, ix, inplace, max_n, st);
+    else launch_gather<uint16_t, 64>(dm, desc, ws, ix, inplace, max_n, st);
   } else {
-    if (dm.d == 128) launch_gather<float, 128>(dm, desc, ws, ix, st);
-    else launch_gather<float, 64>(dm, desc, ws, ix, st);
+    if (dm.d == 128) launch_gather<float, 128>(dm, desc, ws, ix, inplace, max_n, st);
+    else launch_gather<float, 64>(dm, desc, ws, ix, inplace, max_n, st);
   }
   if (hidden) {
     const dim3 grid((unsigned)((dm.max_tokens + 3) / 4), dm.L);
     if (dtype == 0)
-      OMNIMEM_LAUNCH(ws, K_GATHER_H, st, gather_hidden<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ix, ws.eff));
+      OMNIMEM_LAUNCH(ws, K_GATHER_H, st, gather_hidden<uint16_t><<<grid, 256, 0, st>>>(desc, dm, ix, ws.eff, ctl));
     else
-      OMNIMEM_LAUNCH(ws, K_GATHER_H, st, gather_hidden<float><<<grid, 256, 0, st>>>(desc, dm, ix, ws.eff));
+      OMNIMEM_LAUNCH(ws, K_GATHER_H, st, gather_hidden<float><<<grid, 256, 0, st>>>(desc, dm, ix, ws.eff, ctl));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws, int64_t max_rows,
+                         hipStream_t st) {
+  const dim3 grid((unsigned)((max_rows + kGatherRows - 1) / kGatherRows), dm.Hkv, dm.L);
+  if (dtype == 0) {
+    if (dm.d == 128) OMNIMEM_LAUNCH(ws, K_APPEND, st, append_chunk<uint16_t, 128><<<grid, 256, 0, st>>>(desc, dm));
+    else OMNIMEM_LAUNCH(ws, K_APPEND, st, append_chunk<uint16_t, 64><<<grid, 256, 0, st>>>(desc, dm));
+  } else {
+    if (dm.d == 128) OMNIMEM_LAUNCH(ws, K_APPEND, st, append_chunk<float, 128><<<grid, 256, 0, st>>>(desc, dm));
+    else OMNIMEM_LAUNCH(ws, K_APPEND, st, append_chunk<float, 64><<<grid, 256, 0, st>>>(desc, dm));
   }
   return hipGetLastError();
 }

@@ -25,7 +25,8 @@ EXPORTED = [
     "omnimem_config_default", "omnimem_create", "omnimem_destroy", "omnimem_last_error",
     "omnimem_score", "omnimem_redundancy", "omnimem_allocate", "omnimem_select_compact",
     "omnimem_calibrate", "omnimem_calibration_reset", "omnimem_calibration_budgets",
-    "omnimem_allocate_fixed", "omnimem_profile", "omnimem_profile_report",
+    "omnimem_allocate_fixed", "omnimem_profile", "omnimem_profile_report", "omnimem_inplace_status",
+    "omnimem_append",
 ]
 
 
@@ -42,7 +43,7 @@ class Config(ctypes.Structure):
         ("ratio_r", ctypes.c_float), ("temperature", ctypes.c_float), ("b_min_frac", ctypes.c_float),
         ("b_max_frac", ctypes.c_float), ("causal", ctypes.c_int32), ("sim", ctypes.c_int32),
         ("sim_source", ctypes.c_int32), ("shared_selection", ctypes.c_int32), ("max_tokens", ctypes.c_int64),
-        ("max_chunk", ctypes.c_int64), ("hidden_dim", ctypes.c_int32),
+        ("max_chunk", ctypes.c_int64), ("hidden_dim", ctypes.c_int32), ("inplace_stage_rows", ctypes.c_int32),
     ]
 
 
@@ -54,7 +55,15 @@ class Layer(ctypes.Structure):
         ("n_chunk", ctypes.c_int64), ("sm_scale", ctypes.c_float), ("lse", ctypes.c_void_p),
         ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p), ("out_head_stride", ctypes.c_int64),
         ("out_row_stride", ctypes.c_int64), ("hidden", ctypes.c_void_p), ("hidden_row_stride", ctypes.c_int64),
-        ("hidden_out", ctypes.c_void_p), ("hidden_out_row_stride", ctypes.c_int64),
+        ("hidden_out", ctypes.c_void_p), ("hidden_out_row_stride", ctypes.c_int64), ("out_rows", ctypes.c_int64),
+        ("modality_out", ctypes.c_void_p),
+    ]
+
+
+class Chunk(ctypes.Structure):
+    _fields_ = [
+        ("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("head_stride", ctypes.c_int64),
+        ("row_stride", ctypes.c_int64), ("modality", ctypes.c_void_p), ("n_rows", ctypes.c_int64),
     ]
 
 
@@ -98,6 +107,10 @@ def load_library(path=LIB_PATH):
     lib.omnimem_calibration_budgets.restype = i32
     lib.omnimem_allocate_fixed.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, vp, vp, vp, vp]
     lib.omnimem_allocate_fixed.restype = i32
+    lib.omnimem_inplace_status.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
+    lib.omnimem_inplace_status.restype = i32
+    lib.omnimem_append.argtypes = [vp, ctypes.POINTER(Layer), ctypes.POINTER(Chunk), vp]
+    lib.omnimem_append.restype = i32
     lib.omnimem_profile.argtypes = [vp, ctypes.c_int32]
     lib.omnimem_profile.restype = i32
     lib.omnimem_profile_report.argtypes = [vp, ctypes.POINTER(KernelTime), ctypes.c_int32,
@@ -121,12 +134,14 @@ def _stream(stream):
 
 
 def make_layer(q, k, v, modality, n_cache, sm_scale=0.0, lse=None, k_out=None, v_out=None, hidden=None,
-               hidden_out=None):
+               hidden_out=None, out_rows=0, modality_out=None, n=None):
     """Descriptor of one layer's working set from device tensors.
 
-    q [H_q, C, d]; k, v [H_kv, N, d]; modality uint8 [N]; optional lse
-    [H_q, C] fp32; optional k_out, v_out [H_kv, >=N, d] (same strides);
-    optional hidden [N, d_model] and hidden_out [>=M, d_model].
+    q [H_q, C, d]; k, v [H_kv, >=N, d] (the working set is their first N
+    rows, N = k.shape[1] unless given); modality uint8 [>=N]; optional lse
+    [H_q, C] fp32; optional k_out, v_out [H_kv, out_rows, d] (same strides;
+    k_out is k and v_out is v for compaction in place); optional hidden
+    [N, d_model] and hidden_out [>=M, d_model]; optional modality_out uint8.
     """
     if k.stride() != v.stride():
         raise ValueError("k and v must share strides")
@@ -134,7 +149,7 @@ def make_layer(q, k, v, modality, n_cache, sm_scale=0.0, lse=None, k_out=None, v
         raise ValueError("k_out and v_out must both be given with equal strides")
     if modality.dtype != torch.uint8:
         raise TypeError("modality must be uint8")
-    n = k.shape[1]
+    n = k.shape[1] if n is None else int(n)
     lay = Layer()
     lay.q = _ptr(q)
     lay.q_head_stride, lay.q_row_stride = (q.stride(0), q.stride(1)) if q is not None else (0, 0)
@@ -148,6 +163,11 @@ def make_layer(q, k, v, modality, n_cache, sm_scale=0.0, lse=None, k_out=None, v
     if k_out is not None:
         lay.k_out, lay.v_out = _ptr(k_out), _ptr(v_out)
         lay.out_head_stride, lay.out_row_stride = k_out.stride(0), k_out.stride(1)
+        lay.out_rows = int(out_rows)
+    if modality_out is not None:
+        if modality_out.dtype != torch.uint8:
+            raise TypeError("modality_out must be uint8")
+        lay.modality_out = _ptr(modality_out)
     if hidden is not None:
         lay.hidden, lay.hidden_row_stride = _ptr(hidden), hidden.stride(0)
     if hidden_out is not None:
@@ -189,8 +209,9 @@ class Context:
     def _layers(self, layers):
         if len(layers) != self.cfg.n_layers:
             raise ValueError(f"expected {self.cfg.n_layers} layer descriptors")
-        arr = (Layer * len(layers))(*layers)
-        return arr
+        if isinstance(layers, ctypes.Array) and layers._type_ is Layer:
+            return layers
+        return (Layer * len(layers))(*layers)
 
     def close(self):
         if self.handle:
@@ -237,6 +258,20 @@ class Context:
                                                      _stream(stream)))
 
 
+    def omnimem_inplace_status(self):
+        """Largest staging need of the in-place compactions since the last
+        query (0: none); raises OmnimemError when one moved nothing for lack
+        of staging rows or an ordering wait gave up.  Synchronous."""
+        need = ctypes.c_int64()
+        self._check(self._lib.omnimem_inplace_status(self.handle, ctypes.byref(need)))
+        return need.value
+
+    def omnimem_append(self, layers, chunks, stream=None):
+        if len(chunks) != self.cfg.n_layers:
+            raise ValueError(f"expected {self.cfg.n_layers} chunk descriptors")
+        arr = chunks if isinstance(chunks, ctypes.Array) else (Chunk * len(chunks))(*chunks)
+        self._check(self._lib.omnimem_append(self.handle, self._layers(layers), arr, _stream(stream)))
+
     def omnimem_profile(self, on):
         self._check(self._lib.omnimem_profile(self.handle, int(bool(on))))
 
@@ -246,6 +281,21 @@ class Context:
         n = ctypes.c_int32()
         self._check(self._lib.omnimem_profile_report(self.handle, buf, 32, ctypes.byref(n)))
         return {buf[i].name.decode(): (buf[i].launches, buf[i].total_ms) for i in range(n.value)}
+
+
+def make_chunk(k, v, modality):
+    """Descriptor of one layer's new chunk rows: k, v [H_kv, C, d] (equal
+    strides), modality uint8 [C] (device tensors)."""
+    if k.stride() != v.stride():
+        raise ValueError("chunk k and v must share strides")
+    if modality.dtype != torch.uint8:
+        raise TypeError("modality must be uint8")
+    ch = Chunk()
+    ch.k, ch.v = _ptr(k), _ptr(v)
+    ch.head_stride, ch.row_stride = k.stride(0), k.stride(1)
+    ch.modality = _ptr(modality)
+    ch.n_rows = k.shape[1]
+    return ch
 
 
 def default_scale(head_dim):

@@ -125,19 +125,30 @@ class DeviceStep:
 class StreamRunner:
     """The compression step after every chunk of a stream, on the GPU.
 
-    Each layer's cache lives in two ping-pong buffers [H_kv, cap, d]: the
-    working set of a step is the current buffer's first N = n_cache + C rows
-    (retained visual, retained audio, then the new chunk, Eq. 3), and
-    omnimem_select_compact writes the kept rows to the front of the other
-    buffer, which then receives the next chunk behind them.  Appending the
-    chunk stands in for the model's prefill writing its K/V; it is a device
-    copy outside the library.  After each step the budgets are read back (a
-    stream synchronisation): the host needs them to describe the next
-    working set.
+    Each layer's cache is one buffer [H_kv, cap, d] for K, one for V and a
+    modality buffer [cap].  A step's working set is the buffer's first
+    N = n_cache + C rows: omnimem_append writes the chunk's K/V and modality
+    behind the kept rows (Eq. 3), the four stages run, and
+    omnimem_select_compact moves the kept rows to the front of the same
+    buffers and rewrites their modality (in place, Eqs. 2-5).  With
+    in_place=False two buffers per layer alternate instead (out of place).
+
+    The host needs each layer's kept-row count to describe the next working
+    set: it copies the budgets back after the allocation stage and waits for
+    that copy only, so the compaction of one step overlaps the host's
+    preparation of the next.  The descriptors are ctypes arrays built once;
+    a step only updates the fields that change.
+
+    In place, kept audio rows that land behind their own row are staged in
+    the context's reserve of `stage_rows` rows per (layer, KV head); there
+    are never more of them than the layer's audio budget.  When a step's
+    audio budget exceeds the reserve, the runner asks the library whether
+    that step's compaction ran and, if it moved nothing for lack of staging
+    rows, compacts out of place into temporary buffers and copies back.
     """
 
     def __init__(self, n_layers, h_q, h_kv, d, chunk_len, total_budget, dtype="bf16", device="cuda",
-                 **options):
+                 in_place=True, stage_rows=None, keep_working_set=False, timing=False, **options):
         self.device = torch.device(device)
         self.L, self.h_q, self.h_kv, self.d, self.C = n_layers, h_q, h_kv, d, chunk_len
         self.total_budget = int(total_budget)
@@ -146,28 +157,52 @@ class StreamRunner:
         bmax = options.get("b_max_frac", cfg_probe.b_max_frac)
         self.cache_cap = int(bmax * total_budget / n_layers)   # no layer keeps more
         self.cap = self.cache_cap + chunk_len
+        self.in_place = bool(in_place)
+        self.stage_rows = int(stage_rows if stage_rows is not None else self.cache_cap // 2) if in_place else 0
         self.ctx = om.Context(n_layers, h_q, h_kv, d, self.cap, chunk_len,
-                              dtype=om.BF16 if dtype == "bf16" else om.F32, **options)
+                              dtype=om.BF16 if dtype == "bf16" else om.F32,
+                              inplace_stage_rows=self.stage_rows, **options)
         dev, td = self.device, self.tdtype
+        n_sets = 1 if self.in_place else 2
         self.kbuf = [[torch.zeros((h_kv, self.cap, d), device=dev, dtype=td) for _ in range(n_layers)]
-                     for _ in range(2)]
+                     for _ in range(n_sets)]
         self.vbuf = [[torch.zeros((h_kv, self.cap, d), device=dev, dtype=td) for _ in range(n_layers)]
-                     for _ in range(2)]
+                     for _ in range(n_sets)]
         self.mbuf = [[torch.zeros(self.cap, device=dev, dtype=torch.uint8) for _ in range(n_layers)]
-                     for _ in range(2)]
+                     for _ in range(n_sets)]
         shape = (n_layers, h_kv, self.cap)
         self.a = torch.zeros(shape, device=dev, dtype=torch.float32)
         self.s = torch.zeros(shape, device=dev, dtype=torch.float32)
         self.idx = torch.full(shape, -1, device=dev, dtype=torch.int32)
         self.budgets = torch.zeros((n_layers, 2), device=dev, dtype=torch.int32)
+        self.budgets_host = torch.zeros((n_layers, 2), dtype=torch.int32, pin_memory=True)
         self.stats = torch.zeros((n_layers, 10), device=dev, dtype=torch.float32)
         self.layer_budgets = torch.zeros(n_layers, device=dev, dtype=torch.int32)
         self.calibrating = False   # each step also adds its C^(l) to the calibration
         self.fixed = False         # steps split self.layer_budgets instead of Eq. (14)
-        self.cur = 0
+        self.cur = 0               # buffer set holding the cache (out of place: alternates)
         self.n_cache = [0] * n_layers
         self.steps = 0
-        self.tokens = 0          # sum over steps and layers of the working-set size
+        self.tokens = 0            # sum over steps and layers of the working-set size
+        self.fallbacks = 0         # steps compacted out of place for lack of staging rows
+        self.keep_working_set = keep_working_set
+        self.working_set = None    # [L] of (k, v, modality) copies of the last step's working set
+        self._layers = (om.Layer * n_layers)()
+        self._chunks = (om.Chunk * n_layers)()
+        self._budget_ready = torch.cuda.Event()
+        self.timing = timing       # per step: events before the append, before score, after select_compact
+        self.events = []
+
+    # buffers ------------------------------------------------------------
+    def cache_k(self, l):
+        """Device view of layer l's kept keys [H_kv, n_cache, d]."""
+        return self.kbuf[self.cur][l][:, : self.n_cache[l]]
+
+    def cache_v(self, l):
+        return self.vbuf[self.cur][l][:, : self.n_cache[l]]
+
+    def cache_modality(self, l):
+        return self.mbuf[self.cur][l][: self.n_cache[l]]
 
     def set_cache(self, l, k, v, m_v, m_a):
         """Replace layer l's retained cache: k, v [H_kv, m_v + m_a, d] (host or
@@ -182,50 +217,127 @@ class StreamRunner:
         mb[m_v:m] = 1
         self.n_cache[l] = m
 
-    def working_set(self, l):
-        """Device views of layer l's current working set (k, v, modality)."""
-        n = self.n_cache[l] + self.C
-        return (self.kbuf[self.cur][l][:, :n], self.vbuf[self.cur][l][:, :n], self.mbuf[self.cur][l][:n])
+    # one step ----------------------------------------------------------
+    def _describe(self, chunk, qs):
+        """Fill the persistent descriptor arrays for this step's working sets."""
+        other = self.cur if self.in_place else 1 - self.cur
+        for l, ch in enumerate(chunk):
+            kb, vb, mb = self.kbuf[self.cur][l], self.vbuf[self.cur][l], self.mbuf[self.cur][l]
+            ko, vo, mo = self.kbuf[other][l], self.vbuf[other][l], self.mbuf[other][l]
+            lay = self._layers[l]
+            q = qs[l]
+            lay.q, lay.q_head_stride, lay.q_row_stride = q.data_ptr(), q.stride(0), q.stride(1)
+            lay.k, lay.v = kb.data_ptr(), vb.data_ptr()
+            lay.kv_head_stride, lay.kv_row_stride = kb.stride(0), kb.stride(1)
+            lay.modality = mb.data_ptr()
+            lay.n_cache, lay.n_chunk = self.n_cache[l], self.C
+            lay.sm_scale = float(ch["sm_scale"])
+            lay.k_out, lay.v_out = ko.data_ptr(), vo.data_ptr()
+            lay.out_head_stride, lay.out_row_stride = ko.stride(0), ko.stride(1)
+            lay.out_rows = self.cap
+            lay.modality_out = mo.data_ptr()
+            c = self._chunks[l]
+            ck, cv, cm = ch["k"], ch["v"], ch["modality"]
+            c.k, c.v, c.modality = ck.data_ptr(), cv.data_ptr(), cm.data_ptr()
+            c.head_stride, c.row_stride, c.n_rows = ck.stride(0), ck.stride(1), ck.shape[1]
+
+    def _on_device(self, chunk):
+        dev, td = self.device, self.tdtype
+        out = []
+        for ch in chunk:
+            x = dict(ch)
+            for key in ("q", "k", "v"):
+                t = torch.as_tensor(ch[key]).to(dev, td)
+                x[key] = t if t.is_contiguous() else t.contiguous()
+            x["modality"] = torch.as_tensor(ch["modality"]).to(dev, torch.uint8)
+            out.append(x)
+        return out
 
     def push(self, chunk, stream=None):
-        """Append one chunk (list of per-layer dicts from synth.StreamSource)
-        and run the step.  Returns the budgets [L, 2] as a host array."""
-        dev, td = self.device, self.tdtype
-        descs, qs = [], []
-        other = 1 - self.cur
-        for l, ch in enumerate(chunk):
-            n0 = self.n_cache[l]
-            n = n0 + self.C
-            kb, vb, mb = self.kbuf[self.cur][l], self.vbuf[self.cur][l], self.mbuf[self.cur][l]
-            kb[:, n0:n] = torch.as_tensor(ch["k"]).to(dev, td)
-            vb[:, n0:n] = torch.as_tensor(ch["v"]).to(dev, td)
-            mb[n0:n] = torch.as_tensor(ch["modality"]).to(dev)
-            q = torch.as_tensor(ch["q"]).to(dev, td).contiguous()
-            qs.append(q)
-            descs.append(om.make_layer(q, kb[:, :n], vb[:, :n], mb[:n], n0, ch["sm_scale"], None,
-                                       self.kbuf[other][l], self.vbuf[other][l]))
-            self.tokens += n
-        self._descs, self._qs = descs, qs
-        self.ctx.omnimem_score(descs, self.a, None, stream)
-        self.ctx.omnimem_redundancy(descs, self.s, stream)
+        """Append one chunk (list of per-layer dicts from synth.StreamSource:
+        q [H_q, C, d], k, v [H_kv, C, d], modality [C], sm_scale) and run the
+        step.  Returns the budgets [L, 2] as a host array; the compaction may
+        still be running on the stream when it returns."""
+        stream = stream if stream is not None else torch.cuda.current_stream()
+        chunk = self._on_device(chunk)
+        self._chunk_refs = chunk   # keep the inputs alive while the stream uses them
+        self._describe(chunk, [ch["q"] for ch in chunk])
+        ctx, lays = self.ctx, self._layers
+        ev = None
+        if self.timing:
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            ev[0].record(stream)
+        ctx.omnimem_append(lays, self._chunks, stream)
+        if self.keep_working_set:
+            with torch.cuda.stream(stream):
+                self.working_set = [(self.kbuf[self.cur][l][:, : self.n_cache[l] + self.C].clone(),
+                                     self.vbuf[self.cur][l][:, : self.n_cache[l] + self.C].clone(),
+                                     self.mbuf[self.cur][l][: self.n_cache[l] + self.C].clone())
+                                    for l in range(self.L)]
+        if ev:
+            ev[1].record(stream)
+        ctx.omnimem_score(lays, self.a, None, stream)
+        ctx.omnimem_redundancy(lays, self.s, stream)
         if self.calibrating:
-            self.ctx.omnimem_calibrate(descs, self.a, self.s, None, stream)
+            ctx.omnimem_calibrate(lays, self.a, self.s, None, stream)
         if self.fixed:
-            self.ctx.omnimem_allocate_fixed(descs, self.a, self.s, self.layer_budgets, self.budgets, self.stats,
-                                            stream)
+            ctx.omnimem_allocate_fixed(lays, self.a, self.s, self.layer_budgets, self.budgets, self.stats, stream)
         else:
-            self.ctx.omnimem_allocate(descs, self.a, self.s, self.total_budget, self.budgets, self.stats, stream)
-        self.ctx.omnimem_select_compact(descs, self.a, self.s, self.budgets, self.idx, stream)
-        budgets = self.budgets.cpu().numpy()
+            ctx.omnimem_allocate(lays, self.a, self.s, self.total_budget, self.budgets, self.stats, stream)
+        with torch.cuda.stream(stream):
+            self.budgets_host.copy_(self.budgets, non_blocking=True)
+            self._budget_ready.record(stream)
+        ctx.omnimem_select_compact(lays, self.a, self.s, self.budgets, self.idx, stream)
+        if ev:
+            ev[2].record(stream)
+            self.events.append(ev)
         for l in range(self.L):
-            m_v, m_a = int(budgets[l, 0]), int(budgets[l, 1])
-            mb = self.mbuf[other][l]
-            mb[:m_v] = 0
-            mb[m_v:m_v + m_a] = 1
-            self.n_cache[l] = m_v + m_a
-        self.cur = other
+            self.tokens += self.n_cache[l] + self.C
+        self._budget_ready.synchronize()
+        budgets = self.budgets_host.numpy().copy()
+        if self.in_place and int(budgets[:, 1].max()) > self.stage_rows:
+            self._check_staging(stream)
+        for l in range(self.L):
+            self.n_cache[l] = int(budgets[l, 0]) + int(budgets[l, 1])
+        if not self.in_place:
+            self.cur = 1 - self.cur
         self.steps += 1
         return budgets
+
+    def _check_staging(self, stream):
+        """A step whose audio budget exceeds the staging reserve: if its
+        in-place compaction moved nothing, compact out of place into
+        temporaries and copy the kept rows back."""
+        stream.synchronize()
+        try:
+            self.ctx.omnimem_inplace_status()
+            return
+        except om.OmnimemError as e:
+            if e.status != om.ERR_CAPACITY:
+                raise
+        self.fallbacks += 1
+        tmp = []
+        lays = (om.Layer * self.L)()
+        for l in range(self.L):
+            lay = om.Layer.from_buffer_copy(self._layers[l])
+            ko = torch.empty_like(self.kbuf[self.cur][l])
+            vo = torch.empty_like(self.vbuf[self.cur][l])
+            lay.k_out, lay.v_out = ko.data_ptr(), vo.data_ptr()
+            tmp.append((ko, vo))
+            lays[l] = lay
+        self.ctx.omnimem_select_compact(lays, self.a, self.s, self.budgets, self.idx, stream)
+        with torch.cuda.stream(stream):
+            for l, (ko, vo) in enumerate(tmp):
+                self.kbuf[self.cur][l].copy_(ko)
+                self.vbuf[self.cur][l].copy_(vo)
+        stream.synchronize()
+
+    def timings(self):
+        """Summed milliseconds over the timed steps: (appends, four stages)."""
+        torch.cuda.synchronize()
+        app = sum(e[0].elapsed_time(e[1]) for e in self.events)
+        abi = sum(e[1].elapsed_time(e[2]) for e in self.events)
+        return app, abi
 
     def freeze_budgets(self, stream=None):
         """Layer budgets from the steps calibrated so far; later steps split them."""
