@@ -256,35 +256,40 @@ omnimem_status validate_append(omnimem_ctx* ctx, const omnimem_layer* layers, co
   return OMNIMEM_OK;
 }
 
+// Device descriptor of one layer (the score-pass plan fields are filled by
+// plan_score).
+void describe(const omnimem_config& cfg, const omnimem_layer& s, const omnimem_chunk* chunk, LayerDesc* out) {
+  LayerDesc& x = *out;
+  std::memset(&x, 0, sizeof x);
+  x.q = s.q; x.k = s.k; x.v = s.v; x.mod = s.modality; x.lse_in = s.lse;
+  x.k_out = s.k_out; x.v_out = s.v_out;
+  x.q_hs = s.q_head_stride; x.q_rs = s.q_row_stride;
+  x.kv_hs = s.kv_head_stride; x.kv_rs = s.kv_row_stride;
+  x.out_hs = s.out_head_stride; x.out_rs = s.out_row_stride;
+  if (cfg.sim_source == OMNIMEM_SRC_HIDDEN) {
+    x.hidden = s.hidden; x.hidden_out = s.hidden_out;
+    x.hidden_rs = s.hidden_row_stride; x.hidden_out_rs = s.hidden_out_row_stride;
+  }
+  x.n_cache = (int32_t)s.n_cache; x.n_chunk = (int32_t)s.n_chunk; x.n = (int32_t)(s.n_cache + s.n_chunk);
+  x.mod_out = s.modality_out;
+  x.out_cap = (int32_t)std::min<int64_t>(s.out_rows > 0 ? s.out_rows : x.n, x.n);
+  x.inplace = (s.k_out && in_place(s)) ? 1 : 0;
+  if (chunk) {
+    x.ck = chunk->k; x.cv = chunk->v; x.cmod = chunk->modality;
+    x.c_hs = chunk->head_stride; x.c_rs = chunk->row_stride;
+  }
+  const double log2e = 1.4426950408889634;
+  const double scale = s.sm_scale != 0.0f ? (double)s.sm_scale : 1.0 / std::sqrt((double)cfg.head_dim);
+  x.scale_log2 = (float)(scale * log2e);
+}
+
 // Copy the descriptor table to the device unless it equals the last one.
 omnimem_status upload(omnimem_ctx* ctx, const omnimem_layer* layers, hipStream_t st, const LayerDesc** dev,
                       const omnimem_chunk* chunks = nullptr) {
   const int L = ctx->cfg.n_layers;
-  const double log2e = 1.4426950408889634;
   std::vector<LayerDesc> t(L);
   for (int l = 0; l < L; ++l) {
-    const omnimem_layer& s = layers[l];
-    LayerDesc& x = t[l];
-    std::memset(&x, 0, sizeof x);
-    x.q = s.q; x.k = s.k; x.v = s.v; x.mod = s.modality; x.lse_in = s.lse;
-    x.k_out = s.k_out; x.v_out = s.v_out;
-    x.q_hs = s.q_head_stride; x.q_rs = s.q_row_stride;
-    x.kv_hs = s.kv_head_stride; x.kv_rs = s.kv_row_stride;
-    x.out_hs = s.out_head_stride; x.out_rs = s.out_row_stride;
-    if (ctx->cfg.sim_source == OMNIMEM_SRC_HIDDEN) {
-      x.hidden = s.hidden; x.hidden_out = s.hidden_out;
-      x.hidden_rs = s.hidden_row_stride; x.hidden_out_rs = s.hidden_out_row_stride;
-    }
-    x.n_cache = (int32_t)s.n_cache; x.n_chunk = (int32_t)s.n_chunk; x.n = (int32_t)(s.n_cache + s.n_chunk);
-    x.mod_out = s.modality_out;
-    x.out_cap = (int32_t)std::min<int64_t>(s.out_rows > 0 ? s.out_rows : x.n, x.n);
-    x.inplace = (s.k_out && in_place(s)) ? 1 : 0;
-    if (chunks) {
-      x.ck = chunks[l].k; x.cv = chunks[l].v; x.cmod = chunks[l].modality;
-      x.c_hs = chunks[l].head_stride; x.c_rs = chunks[l].row_stride;
-    }
-    const double scale = s.sm_scale != 0.0f ? (double)s.sm_scale : 1.0 / std::sqrt((double)ctx->cfg.head_dim);
-    x.scale_log2 = (float)(scale * log2e);
+    describe(ctx->cfg, layers[l], chunks ? &chunks[l] : nullptr, &t[l]);
   }
   plan_score(ctx->dm, t.data(), ctx->max_workgroups, &ctx->lse_plan, &ctx->cs_plan);
   if (ctx->last_slot >= 0 && ctx->last_table.size() == t.size() &&
@@ -328,6 +333,52 @@ omnimem_status set_device(omnimem_ctx* ctx) {
   return OMNIMEM_OK;
 }
 
+// Sizes and options of a configuration, checked without touching the device.
+omnimem_status check_config(const omnimem_config& c) {
+  if (c.n_layers < 1 || c.n_layers > kMaxLayers || c.n_q_heads < 1 || c.n_kv_heads < 1 ||
+      c.n_q_heads % c.n_kv_heads != 0 || c.max_tokens < 1 || c.max_chunk < 0 || c.max_chunk > c.max_tokens ||
+      c.max_tokens > (int64_t)1 << 30)
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "bad sizes: need 1 <= n_layers <= %d, H_kv | H_q, "
+                "0 <= max_chunk <= max_tokens <= 2^30", kMaxLayers);
+  if ((int64_t)c.n_layers * c.n_kv_heads > 256)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "n_layers * n_kv_heads = %d: at most 256 supported",
+                c.n_layers * c.n_kv_heads);
+  if (c.head_dim != 64 && c.head_dim != 128)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "head_dim %d: supported 64 and 128", c.head_dim);
+  if (c.dtype != OMNIMEM_BF16 && c.dtype != OMNIMEM_F32)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "dtype %d", c.dtype);
+  if (c.sim != OMNIMEM_SIM_MAX && c.sim != OMNIMEM_SIM_ADJ)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "sim %d", c.sim);
+  if (c.sim_source < OMNIMEM_SRC_VALUES || c.sim_source > OMNIMEM_SRC_HIDDEN)
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "sim_source %d", c.sim_source);
+  if (c.sim_source == OMNIMEM_SRC_HIDDEN) {
+    const int64_t esz = c.dtype == OMNIMEM_BF16 ? 2 : 4;
+    if (c.hidden_dim < 1 || c.hidden_dim > 65536 || (c.hidden_dim * esz) % 16)
+      return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "hidden_dim %d: need 1..65536 and rows of whole 16-byte units",
+                  c.hidden_dim);
+    if (c.sim == OMNIMEM_SIM_MAX && c.hidden_dim % 64)
+      return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "hidden_dim %d: the all-pairs maximum on hidden states takes "
+                  "multiples of 64", c.hidden_dim);
+  }
+  if (c.inplace_stage_rows < 0 || c.inplace_stage_rows > c.max_tokens)
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "inplace_stage_rows %d: need 0 .. max_tokens", c.inplace_stage_rows);
+  if (!std::isfinite(c.lambda) || c.lambda < 0.0f || !(c.ratio_r > 0.0f) || !(c.temperature > 0.0f) ||
+      !(c.b_min_frac >= 0.0f) || !(c.b_max_frac >= c.b_min_frac) || !std::isfinite(c.b_max_frac))
+    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "need lambda >= 0, r > 0, T > 0, 0 <= b_min_frac <= b_max_frac");
+  return OMNIMEM_OK;
+}
+
+Dims make_dims(const omnimem_config& c) {
+  Dims dm;
+  dm.L = c.n_layers; dm.Hq = c.n_q_heads; dm.Hkv = c.n_kv_heads; dm.G = c.n_q_heads / c.n_kv_heads;
+  dm.d = c.head_dim; dm.max_tokens = c.max_tokens; dm.max_chunk = std::max<int64_t>(c.max_chunk, 1);
+  dm.causal = c.causal ? 1 : 0;
+  dm.qb = (int)((dm.max_chunk + kScoreBlock - 1) / kScoreBlock);
+  dm.kb = (int)((dm.max_tokens + kScoreBlock - 1) / kScoreBlock);
+  dm.dh = c.sim_source == OMNIMEM_SRC_HIDDEN ? c.hidden_dim : 0;
+  return dm;
+}
+
 template <typename T>
 hipError_t dalloc(omnimem_ctx* ctx, T** p, size_t count) {
   void* q = nullptr;
@@ -361,48 +412,15 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
   if (!cfg || !out) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null argument");
   *out = nullptr;
   const omnimem_config& c = *cfg;
-  if (c.n_layers < 1 || c.n_layers > kMaxLayers || c.n_q_heads < 1 || c.n_kv_heads < 1 ||
-      c.n_q_heads % c.n_kv_heads != 0 || c.max_tokens < 1 || c.max_chunk < 0 || c.max_chunk > c.max_tokens ||
-      c.max_tokens > (int64_t)1 << 30)
-    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "bad sizes: need 1 <= n_layers <= %d, H_kv | H_q, "
-                "0 <= max_chunk <= max_tokens <= 2^30", kMaxLayers);
-  if ((int64_t)c.n_layers * c.n_kv_heads > 256)
-    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "n_layers * n_kv_heads = %d: at most 256 supported",
-                c.n_layers * c.n_kv_heads);
-  if (c.head_dim != 64 && c.head_dim != 128)
-    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "head_dim %d: supported 64 and 128", c.head_dim);
-  if (c.dtype != OMNIMEM_BF16 && c.dtype != OMNIMEM_F32)
-    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "dtype %d", c.dtype);
-  if (c.sim != OMNIMEM_SIM_MAX && c.sim != OMNIMEM_SIM_ADJ)
-    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "sim %d", c.sim);
-  if (c.sim_source < OMNIMEM_SRC_VALUES || c.sim_source > OMNIMEM_SRC_HIDDEN)
-    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "sim_source %d", c.sim_source);
-  if (c.sim_source == OMNIMEM_SRC_HIDDEN) {
-    const int64_t esz = c.dtype == OMNIMEM_BF16 ? 2 : 4;
-    if (c.hidden_dim < 1 || c.hidden_dim > 65536 || (c.hidden_dim * esz) % 16)
-      return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "hidden_dim %d: need 1..65536 and rows of whole 16-byte units",
-                  c.hidden_dim);
-    if (c.sim == OMNIMEM_SIM_MAX && c.hidden_dim % 64)
-      return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "hidden_dim %d: the all-pairs maximum on hidden states takes "
-                  "multiples of 64", c.hidden_dim);
-  }
-  if (c.inplace_stage_rows < 0 || c.inplace_stage_rows > c.max_tokens)
-    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "inplace_stage_rows %d: need 0 .. max_tokens", c.inplace_stage_rows);
-  if (!std::isfinite(c.lambda) || c.lambda < 0.0f || !(c.ratio_r > 0.0f) || !(c.temperature > 0.0f) ||
-      !(c.b_min_frac >= 0.0f) || !(c.b_max_frac >= c.b_min_frac) || !std::isfinite(c.b_max_frac))
-    return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "need lambda >= 0, r > 0, T > 0, 0 <= b_min_frac <= b_max_frac");
+  omnimem_status cst = check_config(c);
+  if (cst != OMNIMEM_OK) return cst;
 
   omnimem_ctx* ctx = new omnimem_ctx();
   ctx->cfg = c;
   hipError_t e = hipGetDevice(&ctx->device);
   if (e != hipSuccess) { delete ctx; return fail(nullptr, OMNIMEM_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e)); }
   Dims& dm = ctx->dm;
-  dm.L = c.n_layers; dm.Hq = c.n_q_heads; dm.Hkv = c.n_kv_heads; dm.G = c.n_q_heads / c.n_kv_heads;
-  dm.d = c.head_dim; dm.max_tokens = c.max_tokens; dm.max_chunk = std::max<int64_t>(c.max_chunk, 1);
-  dm.causal = c.causal ? 1 : 0;
-  dm.qb = (int)((dm.max_chunk + kScoreBlock - 1) / kScoreBlock);
-  dm.kb = (int)((dm.max_tokens + kScoreBlock - 1) / kScoreBlock);
-  dm.dh = c.sim_source == OMNIMEM_SRC_HIDDEN ? c.hidden_dim : 0;
+  dm = make_dims(c);
   int cus = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ctx->device) == hipSuccess && cus > 0)
     ctx->max_workgroups = 2 * cus;
