@@ -203,6 +203,24 @@ omnimem_status omnimem_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, c
                                 const float* s, int64_t total_budget, int32_t* budgets,
                                 float* stats, hipStream_t stream);
 
+/* omnimem_allocate for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): no context, and no device allocation by this call or by the
+ * library on its behalf.  Same arguments and results as omnimem_allocate,
+ * with the configuration passed directly (its sizes and options checked as
+ * by omnimem_create).  Its scratch (the layer table and the per-chunk
+ * partial sums) is a fixed 4 MiB device array of the library, one per GPU,
+ * held until the process ends; the call needs under 256 bytes per layer
+ * for the table plus L * H_kv * ceil(max_tokens / 512) * 64 bytes of
+ * partial sums, and fails with OMNIMEM_ERR_CAPACITY beyond 4 MiB, before
+ * any launch (the 28-layer, 4-KV-head, 10240-token stream needs 150 KB).  Every call on a GPU
+ * uses the same array: calls that overlap in time on one GPU (on different
+ * streams, or from different threads) race and must not be made.  Errors
+ * and their text as omnimem_allocate (text from omnimem_last_error(NULL)). */
+omnimem_status omnimem_allocate_noalloc(const omnimem_config* cfg, const omnimem_layer* layers, const float* a,
+                                        const float* s, int64_t total_budget, int32_t* budgets, float* stats,
+                                        hipStream_t stream);
+
 /* Offline budgets (end of Sec. 3.2: the layer budgets may be fixed ahead of
  * time from a few calibration chunks).  The per-layer budgets B^(l) of Eq. (14)
  * are fixed in advance; every step then only splits them between the

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -23,6 +24,10 @@ constexpr int kMaxLayers = 1024;  // bound of the allocation kernel's tables
 std::string g_create_error;
 
 }  // namespace
+
+// Scratch of omnimem_allocate_noalloc (see there).
+constexpr size_t kScratchBytes = (size_t)4 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace omnimem {
 // Launch timing: an event pool and the (kernel, begin event) of each launch.
@@ -379,6 +384,67 @@ Dims make_dims(const omnimem_config& c) {
   return dm;
 }
 
+// Arguments of the allocation stage (Eqs. 9-14), including the host-side
+// feasibility of the per-layer minimum budgets.
+omnimem_status check_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,
+                              int64_t total_budget, const int32_t* budgets) {
+  omnimem_status st = validate(ctx, layers, 0);
+  if (st != OMNIMEM_OK) return st;
+  if (!a || !s || !budgets) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a, s or budgets");
+  const omnimem_config& c = ctx->cfg;
+  if (total_budget < 0 || total_budget > ((int64_t)1 << 40))
+    return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "total budget %lld out of range", (long long)total_budget);
+  const int64_t lo_base = (int64_t)std::ceil(((double)c.b_min_frac * (double)total_budget) / c.n_layers);
+  int64_t sum_lo = 0;
+  for (int l = 0; l < c.n_layers; ++l) sum_lo += std::min<int64_t>(lo_base, layers[l].n_cache + layers[l].n_chunk);
+  if (sum_lo > total_budget)
+    return fail(ctx, OMNIMEM_ERR_INFEASIBLE, "per-layer minimum budgets sum to %lld > total %lld",
+                (long long)sum_lo, (long long)total_budget);
+  return OMNIMEM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The allocation stage without a context and without any device allocation
+// (omnimem_allocate_noalloc).  Its scratch -- the layer table and the fp64
+// partial sums of Eqs. 9-10 and 13 -- lives in `scratch`, a fixed device
+// array of kScratchBytes that every GPU the library runs on holds until the
+// process ends.  Host code never uses the array's name as an address: the
+// first call on a device asks the runtime for the array's address on that
+// device (hipGetSymbolAddress, with the device current) and keeps it.
+// ---------------------------------------------------------------------------
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+omnimem_status scratch_address(int device, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (device < 0 || device >= kMaxDevices)
+    return fail(nullptr, OMNIMEM_ERR_UNSUPPORTED, "device %d: at most %d devices", device, kMaxDevices);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(nullptr, OMNIMEM_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[device] = p;
+  }
+  *out = g_scratch_ptr[device];
+  return OMNIMEM_OK;
+}
+
+// Layer descriptors passed by value and stored into the scratch table.
+constexpr int kDescPerStore = 8;
+struct DescBlock {
+  LayerDesc d[kDescPerStore];
+};
+static_assert(sizeof(DescBlock) <= 3072, "kernel argument block too large");
+
+__global__ void store_descs(LayerDesc* __restrict__ dst, DescBlock blk, int count) {
+  if (threadIdx.x != 0) return;
+#pragma unroll
+  for (int i = 0; i < kDescPerStore; ++i)
+    if (i < count) dst[i] = blk.d[i];
+}
+
 template <typename T>
 hipError_t dalloc(omnimem_ctx* ctx, T** p, size_t count) {
   void* q = nullptr;
@@ -522,24 +588,57 @@ omnimem_status omnimem_redundancy(omnimem_ctx* ctx, const omnimem_layer* layers,
 
 omnimem_status omnimem_allocate(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,
                                 int64_t total_budget, int32_t* budgets, float* stats, hipStream_t stream) {
-  omnimem_status st = validate(ctx, layers, 0);
+  omnimem_status st = check_allocate(ctx, layers, a, s, total_budget, budgets);
   if (st != OMNIMEM_OK) return st;
-  if (!a || !s || !budgets) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "null a, s or budgets");
   const omnimem_config& c = ctx->cfg;
-  if (total_budget < 0 || total_budget > ((int64_t)1 << 40))
-    return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "total budget %lld out of range", (long long)total_budget);
-  const int64_t lo_base = (int64_t)std::ceil(((double)c.b_min_frac * (double)total_budget) / c.n_layers);
-  int64_t sum_lo = 0;
-  for (int l = 0; l < c.n_layers; ++l) sum_lo += std::min<int64_t>(lo_base, layers[l].n_cache + layers[l].n_chunk);
-  if (sum_lo > total_budget)
-    return fail(ctx, OMNIMEM_ERR_INFEASIBLE, "per-layer minimum budgets sum to %lld > total %lld",
-                (long long)sum_lo, (long long)total_budget);
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
   return finish(ctx, launch_allocate(ctx->dm, dev, ctx->ws, a, s, total_budget, c.ratio_r, c.temperature,
                                      c.b_min_frac, c.b_max_frac, budgets, stats, stream),
                 stream, "omnimem_allocate launch");
+}
+
+omnimem_status omnimem_allocate_noalloc(const omnimem_config* cfg, const omnimem_layer* layers, const float* a,
+                                        const float* s, int64_t total_budget, int32_t* budgets, float* stats,
+                                        hipStream_t stream) {
+  if (!cfg) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null config");
+  omnimem_status st = check_config(*cfg);
+  if (st != OMNIMEM_OK) return st;
+  const Dims dm = make_dims(*cfg);
+  const size_t desc_bytes = ((size_t)cfg->n_layers * sizeof(LayerDesc) + 255) / 256 * 256;
+  const size_t part_bytes = (size_t)cfg->n_layers * cfg->n_kv_heads * allocate_part_chunks(dm) * 2 * 4 * sizeof(double);
+  if (desc_bytes + part_bytes > kScratchBytes)
+    return fail(nullptr, OMNIMEM_ERR_CAPACITY, "scratch of %zu bytes needed (layer table %zu + partial sums %zu); "
+                "the fixed scratch holds %zu", desc_bytes + part_bytes, desc_bytes, part_bytes, kScratchBytes);
+  omnimem_ctx check;  // host-only: argument checks and their message
+  check.cfg = *cfg;
+  if ((st = check_allocate(&check, layers, a, s, total_budget, budgets)) != OMNIMEM_OK) {
+    g_create_error = check.err;
+    return st;
+  }
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  if (e != hipSuccess) return fail(nullptr, OMNIMEM_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if ((e = hipGetLastError()) != hipSuccess)
+    return fail(nullptr, OMNIMEM_ERR_HIP, "earlier device error: %s", hipGetErrorString(e));
+  void* base = nullptr;
+  if ((st = scratch_address(device, &base)) != OMNIMEM_OK) return st;
+  LayerDesc* table = static_cast<LayerDesc*>(base);
+  Workspace ws{};
+  ws.stat_part = reinterpret_cast<double*>(static_cast<char*>(base) + desc_bytes);
+  for (int l0 = 0; l0 < cfg->n_layers; l0 += kDescPerStore) {
+    DescBlock blk;
+    std::memset(&blk, 0, sizeof blk);
+    const int count = std::min(kDescPerStore, cfg->n_layers - l0);
+    for (int i = 0; i < count; ++i) describe(*cfg, layers[l0 + i], nullptr, &blk.d[i]);
+    store_descs<<<1, 64, 0, stream>>>(table + l0, blk, count);
+  }
+  e = launch_allocate(dm, table, ws, a, s, total_budget, cfg->ratio_r, cfg->temperature, cfg->b_min_frac,
+                      cfg->b_max_frac, budgets, stats, stream);
+  if (e != hipSuccess) return fail(nullptr, OMNIMEM_ERR_HIP, "omnimem_allocate_noalloc launch: %s", hipGetErrorString(e));
+  g_create_error.clear();
+  return OMNIMEM_OK;
 }
 
 omnimem_status omnimem_calibrate(omnimem_ctx* ctx, const omnimem_layer* layers, const float* a, const float* s,

@@ -26,7 +26,7 @@ EXPORTED = [
     "omnimem_score", "omnimem_redundancy", "omnimem_allocate", "omnimem_select_compact",
     "omnimem_calibrate", "omnimem_calibration_reset", "omnimem_calibration_budgets",
     "omnimem_allocate_fixed", "omnimem_profile", "omnimem_profile_report", "omnimem_inplace_status",
-    "omnimem_append",
+    "omnimem_append", "omnimem_allocate_noalloc",
 ]
 
 
@@ -107,6 +107,8 @@ def load_library(path=LIB_PATH):
     lib.omnimem_calibration_budgets.restype = i32
     lib.omnimem_allocate_fixed.argtypes = [vp, ctypes.POINTER(Layer), vp, vp, vp, vp, vp, vp]
     lib.omnimem_allocate_fixed.restype = i32
+    lib.omnimem_allocate_noalloc.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Layer), vp, vp, i64, vp, vp, vp]
+    lib.omnimem_allocate_noalloc.restype = i32
     lib.omnimem_inplace_status.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
     lib.omnimem_inplace_status.restype = i32
     lib.omnimem_append.argtypes = [vp, ctypes.POINTER(Layer), ctypes.POINTER(Chunk), vp]
@@ -281,6 +283,17 @@ class Context:
         n = ctypes.c_int32()
         self._check(self._lib.omnimem_profile_report(self.handle, buf, 32, ctypes.byref(n)))
         return {buf[i].name.decode(): (buf[i].launches, buf[i].total_ms) for i in range(n.value)}
+
+
+def allocate_noalloc(cfg, layers, a, s, total_budget, budgets, stats=None, stream=None):
+    """omnimem_allocate_noalloc: the allocation stage with no context and no
+    device allocation (cfg is a Config; layers a list of Layer)."""
+    lib = load_library()
+    arr = layers if isinstance(layers, ctypes.Array) else (Layer * len(layers))(*layers)
+    st = lib.omnimem_allocate_noalloc(ctypes.byref(cfg), arr, _ptr(a), _ptr(s), int(total_budget), _ptr(budgets),
+                                      _ptr(stats), _stream(stream))
+    if st != OK:
+        raise OmnimemError(st, lib.omnimem_last_error(None).decode())
 
 
 def make_chunk(k, v, modality):
