@@ -726,3 +726,75 @@ def test_validation_errors():
     assert e.value.status == omnimem.ERR_INFEASIBLE
     tight.close()
     st.close()
+
+
+# ---------------------------------------------------------------------------
+# The LSE pass's redo path and redundancy on key vectors
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d", [128, 64])
+def test_lse_redo_when_later_keys_dominate(d):
+    # The bf16 LSE pass takes each query's exponent reference from the first
+    # 32 keys of its key range and redoes a range whose sums leave the fp32
+    # headroom.  Keys 1000 times larger than the rest, at offsets 40..47 of
+    # every 64-key tile (never among the first 32 keys of a range), give
+    # later scores far above that reference; lse and a (Eq. 6) must still
+    # match the oracle.
+    layers = ragged_layers(seed=110, d=d, caches=((300, 100),), frames=(3, 70, 20))
+    lay = layers[0]
+    n = lay["k"].shape[1]
+    planted = np.flatnonzero((np.arange(n) % 64 >= 40) & (np.arange(n) % 64 < 48))
+    lay["k"][:, planted] = synth.round_to_bf16(lay["k"][:, planted] * 1000.0)
+    step = DeviceStep(layers, 300)
+    step.score(lse_out=True)
+    _sync()
+    x = P.as_f64(lay)
+    lse = om.attention_lse(x["q"], x["k"], x["n_cache"], x["sm_scale"], True)
+    # the planted keys lift lse far above what the first 32 keys give (ln 2^100 = 69.3)
+    import scipy.special
+    group = x["q"].shape[0] // x["k"].shape[0]
+    first = np.stack([scipy.special.logsumexp(x["sm_scale"] * x["q"][h] @ x["k"][h // group, :32].T, axis=1)
+                      for h in range(x["q"].shape[0])])
+    assert (lse - first > 80).mean() > 0.5
+    P.assert_close_a(step.host("lse", 0), lse, "lse")
+    a = om.attention_importance(x["q"], x["k"], x["n_cache"], x["sm_scale"], True, lse=lse)
+    P.assert_close_a(step.host("a", 0), a, "a")
+    assert np.isfinite(step.host("a", 0)).all()
+    step.close()
+
+
+@pytest.mark.parametrize("sim", [omnimem.SIM_MAX, omnimem.SIM_ADJ])
+def test_redundancy_on_keys(sim):
+    # Eq. (7) on the key vectors (Sec. 3.1 allows the cache's own vectors):
+    # s from k instead of v, then the whole step against the oracle's step
+    # run on keys.
+    mode = "max" if sim == omnimem.SIM_MAX else "adj"
+    layers = ragged_layers(2, seed=111, caches=((200, 77), (150, 60)))
+    c = Case(layers, 2 * 250, sim=sim, sim_source=omnimem.SRC_KEYS)
+    ref = om.compression_step(c.layers64, c.budget, lam=P.LAMBDA, temperature=P.TEMPERATURE, r=P.RATIO,
+                              mode=mode, use_keys=True)
+    for l, lay in enumerate(c.layers64):
+        P.assert_close_s(c.s[l], om.redundancy(lay["k"], lay["modality"], mode), f"s on keys, layer {l}")
+        assert not np.allclose(c.s[l], om.redundancy(lay["v"], lay["modality"], mode), atol=1e-3)
+    assert c.budgets.sum() == np.array(ref["budgets"]).sum()
+    assert np.abs(c.budgets - np.array(ref["budgets"])).max() <= 1
+    for l, lay in enumerate(c.layers):
+        mv, ma = c.budgets[l]
+        psi = om.retention_score(ref["a"][l], ref["s"][l], P.LAMBDA)
+        for g in range(c.step.h_kv):
+            row = c.idx[l][g, : mv + ma]
+            P.check_selection(row, psi[g], lay["modality"], mv, ma, rel=5e-3)
+            np.testing.assert_array_equal(c.k_out[l][g, : mv + ma], lay["k"][g, row])
+    c.step.close()
+
+
+def test_redundancy_on_keys_full_size():
+    layers = synth.make_workload("qwen7b-layer-6144")
+    step = DeviceStep(layers, 4096, sim_source=omnimem.SRC_KEYS)
+    step.redundancy()
+    _sync()
+    lay = P.as_f64(layers[0])
+    rows = np.sort(np.random.default_rng(5).choice(lay["k"].shape[1], size=128, replace=False))
+    P.assert_close_s(step.host("s", 0)[:, rows], om.redundancy(lay["k"], lay["modality"], "max", rows=rows),
+                     "s on keys (sampled rows)")
+    step.close()
