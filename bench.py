@@ -88,6 +88,11 @@ def parse_args():
     p.add_argument("--lse-given", action="store_true",
                    help="take each layer's log-sum-exp as an input, as the model's chunk prefill attention "
                         "produces it (Eq. 1): the step then runs without the LSE pass")
+    p.add_argument("--roof-probe", action="store_true",
+                   help="only measure the instruction-mix ceiling of the score passes (MFMA alone, exp2 alone, "
+                        "the passes' MFMA/exp2/FMA/add mix with and without LDS fragment reads) and exit")
+    p.add_argument("--no-roof-probe", action="store_true",
+                   help="leave the instruction-mix ceiling out of the bench line")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run 5 device-to-device copies of MIB MiB each (reference kernel for "
                         "scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -104,6 +109,60 @@ def copy_calibration(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
+
+
+def roof_probe(torch):
+    """Throughput of the score passes' instruction mix on this GPU, from the
+    probe kernels of libomnimem_probe.so (registers only, plus LDS reads in
+    one of them).  Returns MFMA-flop rates as fractions of the bf16 peak:
+    MFMA alone, and the per-MFMA mix of the passes (one 32x32x16 bf16 MFMA,
+    two exp2, two FMA, two adds) with and without its LDS fragment reads;
+    the mix is the ceiling of a pass that does this work per MFMA."""
+    import ctypes
+
+    from paper_2606_07577_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.omnimem_probe_run.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                      ctypes.c_void_p]
+    lib.omnimem_probe_run.restype = ctypes.c_int
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    out = torch.zeros(1, device="cuda")
+    stream = torch.cuda.current_stream()
+    mfma_flop = 32 * 32 * 16 * 2
+
+    def best_ms(kind, blocks, iters, reps=5):
+        best = float("inf")
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            rc = lib.omnimem_probe_run(kind, blocks, iters, ctypes.c_void_p(out.data_ptr()), 0,
+                                       ctypes.c_void_p(stream.cuda_stream))
+            b.record(stream)
+            if rc != 0:
+                raise RuntimeError(f"probe {kind}: hip error {rc}")
+            torch.cuda.synchronize()
+            best = min(best, a.elapsed_time(b))
+        return best
+
+    res = {"cus": cus}
+    for waves in (2, 4):                       # waves per SIMD (workgroups of 4 waves per compute unit)
+        blocks = cus * waves
+        ms = best_ms(0, blocks, 20000)
+        res[f"mfma_only_{waves}w"] = blocks * 4 * 4 * 20000 * mfma_flop / (ms / 1e3) / 1e12
+        ms = best_ms(1, blocks, 20000)
+        res[f"exp2_per_ns_{waves}w"] = blocks * 4 * 64 * 16 * 20000 / (ms * 1e6)
+    for kind, name in ((2, "mix"), (3, "mix_lds")):
+        blocks = cus * 2                        # the passes' occupancy: two 4-wave workgroups per compute unit
+        ms = best_ms(kind, blocks, 2500)
+        res[name] = blocks * 4 * 32 * 2500 * mfma_flop / (ms / 1e3) / 1e12
+    peak = PEAK_MFMA_TFLOPS["bf16"]
+    out_d = {"unit": "TFLOP/s of MFMA work", "peak": peak,
+             "mfma_only": round(max(res["mfma_only_2w"], res["mfma_only_4w"]), 1),
+             "mix": round(res["mix"], 1), "mix_lds": round(res["mix_lds"], 1),
+             "exp2_per_ns": round(max(res["exp2_per_ns_2w"], res["exp2_per_ns_4w"]), 1)}
+    for k in ("mfma_only", "mix", "mix_lds"):
+        out_d[k + "_frac"] = round(out_d[k] / peak, 4)
+    return out_d
 
 
 def layer_work(h_q, c, n_cache, h_kv, n, d, elt, k_v, k_a, m, causal=True):
@@ -440,6 +499,10 @@ def main():
         return
     import torch
 
+    if args.roof_probe:
+        print(json.dumps({"score_pass_ceiling": roof_probe(torch)}))
+        return
+
     from paper_2606_07577_amd import synth
     if args.lse_given and args.workload in synth.STREAMS:
         print("--lse-given applies to the fixed working sets, not to streams", file=sys.stderr)
@@ -495,6 +558,12 @@ def main():
         "roofline": roofline, "fractions": fractions, "kernels": per_kernel, "cpu_baseline": base,
     }
     out.update(extra)
+    if not args.no_roof_probe:
+        ceiling = roof_probe(torch)
+        for name in ("lse_pass", "colsum_pass"):
+            if name in per_kernel and "frac" in per_kernel[name]:
+                ceiling[name + "_vs_mix"] = round(per_kernel[name]["frac"] / ceiling["mix_frac"], 4)
+        out["score_pass_ceiling"] = ceiling
     print(json.dumps(out))
 
 

@@ -14,6 +14,10 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libomnimem.so")
 SOURCES = ["api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip"]
+# Throughput probes of the score passes' instruction mix (measurement only,
+# a library of their own: nothing of the product links them).
+PROBE_SOURCES = ["probe.hip"]
+PROBE_LIB = os.path.join(HERE, "libomnimem_probe.so")
 ARCH = "gfx950"
 
 FLAGS = [
@@ -42,19 +46,25 @@ def _compile(src):
     return obj, err
 
 
-def build(verbose=True):
-    os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        results = list(ex.map(_compile, SOURCES))
-    for (obj, err) in results:
-        if err.strip() and verbose:
-            print(err, file=sys.stderr)
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + [o for o, _ in results]
+def _link(objs, lib):
+    tmp = lib + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("link failed:\n" + res.stderr)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose=True):
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        results = dict(zip(srcs, ex.map(_compile, srcs)))
+    for obj, err in results.values():
+        if err.strip() and verbose:
+            print(err, file=sys.stderr)
+    _link([results[s][0] for s in SOURCES], LIB)
+    _link([results[s][0] for s in PROBE_SOURCES], PROBE_LIB)
     return LIB
 
 
