@@ -151,7 +151,7 @@ def roof_probe(torch):
         res[f"mfma_only_{waves}w"] = blocks * 4 * 4 * 20000 * mfma_flop / (ms / 1e3) / 1e12
         ms = best_ms(1, blocks, 20000)
         res[f"exp2_per_ns_{waves}w"] = blocks * 4 * 64 * 16 * 20000 / (ms * 1e6)
-    for kind, name in ((2, "mix"), (3, "mix_lds")):
+    for kind, name in ((2, "mix"), (3, "mix_lds"), (4, "mix_lds_barrier")):
         blocks = cus * 2                        # the passes' occupancy: two 4-wave workgroups per compute unit
         ms = best_ms(kind, blocks, 2500)
         res[name] = blocks * 4 * 32 * 2500 * mfma_flop / (ms / 1e3) / 1e12
@@ -159,8 +159,9 @@ def roof_probe(torch):
     out_d = {"unit": "TFLOP/s of MFMA work", "peak": peak,
              "mfma_only": round(max(res["mfma_only_2w"], res["mfma_only_4w"]), 1),
              "mix": round(res["mix"], 1), "mix_lds": round(res["mix_lds"], 1),
+             "mix_lds_barrier": round(res["mix_lds_barrier"], 1),
              "exp2_per_ns": round(max(res["exp2_per_ns_2w"], res["exp2_per_ns_4w"]), 1)}
-    for k in ("mfma_only", "mix", "mix_lds"):
+    for k in ("mfma_only", "mix", "mix_lds", "mix_lds_barrier"):
         out_d[k + "_frac"] = round(out_d[k] / peak, 4)
     return out_d
 

@@ -13,6 +13,8 @@
 //                   MFMA), software-pipelined as in the pass
 //   probe_mix_lds   the same, with the MFMA's key fragments read from LDS
 //                   (one ds_read_b128 per k-step and phase), as in the pass
+//   probe_mix_bar   probe_mix_lds with one workgroup barrier every two
+//                   phases (one per 64-key tile, as in the pass)
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -110,7 +112,7 @@ __device__ inline void mix_phase(floatx16 (&o)[2], const floatx16 (&in)[2], bf16
   lsum[1] += s[1][0] + s[1][1];
 }
 
-template <bool LDS>
+template <bool LDS, bool BAR = false>
 __global__ __launch_bounds__(256, 2) void probe_mix(int iters, float* out, int flag) {
   __shared__ bf16x8 tile[512];  // 8 KB of key fragments
   const int lane = threadIdx.x & 63;
@@ -130,6 +132,7 @@ __global__ __launch_bounds__(256, 2) void probe_mix(int iters, float* out, int f
   const float sl2 = 0.1275f, neg = -1.0f;
   for (int it = 0; it < iters; ++it) {
     mix_phase<LDS>(acc0, acc1, f, qf, sl2, neg, lsum, tile, lane);
+    if (BAR) __syncthreads();  // the passes hand each tile to the workgroup's waves with one barrier
     mix_phase<LDS>(acc1, acc0, f, qf, sl2, neg, lsum, tile, lane);
   }
   if (flag) out[blockIdx.x * blockDim.x + threadIdx.x] = lsum[0] + lsum[1] + acc0[0][0] + acc1[1][1];
@@ -139,18 +142,20 @@ __global__ __launch_bounds__(256, 2) void probe_mix(int iters, float* out, int f
 
 extern "C" {
 
-// Launch probe `kind` (0 MFMA, 1 exp2, 2 mix, 3 mix with LDS fragments) on
+// Launch probe `kind` (0 MFMA, 1 exp2, 2 mix, 3 mix with LDS fragments, 4 the
+// same with a barrier per tile) on
 // `blocks` workgroups of 256 threads for `iters` iterations on `stream`.
 // Work per launch, per wave: kind 0: 4 * iters MFMAs; kind 1: 16 * iters
-// exp2; kinds 2, 3: 32 * iters MFMAs and 64 * iters exp2.  `out` receives
+// exp2; kinds 2-4: 32 * iters MFMAs and 64 * iters exp2.  `out` receives
 // nothing unless `flag` is set.  Returns a hipError_t.
 int omnimem_probe_run(int kind, int blocks, int iters, float* out, int flag, hipStream_t stream) {
-  if (blocks < 1 || iters < 1 || kind < 0 || kind > 3) return (int)hipErrorInvalidValue;
+  if (blocks < 1 || iters < 1 || kind < 0 || kind > 4) return (int)hipErrorInvalidValue;
   switch (kind) {
     case 0: probe_mfma<<<blocks, 256, 0, stream>>>(iters, out, flag); break;
     case 1: probe_exp<<<blocks, 256, 0, stream>>>(iters, out, flag); break;
     case 2: probe_mix<false><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
-    default: probe_mix<true><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
+    case 3: probe_mix<true><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
+    default: probe_mix<true, true><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
   }
   return (int)hipGetLastError();
 }
