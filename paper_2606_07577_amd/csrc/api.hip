@@ -504,7 +504,8 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       (e = dalloc(ctx, &ws.counts, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.inv_norm, L * Hkv * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.best, L * Hkv * T)) != hipSuccess ||
-      (e = dalloc(ctx, reinterpret_cast<char**>(&ws.perm), L * Hkv * T * (size_t)c.head_dim * elt)) != hipSuccess ||
+      (c.dtype != OMNIMEM_BF16 &&  // fp32 rows are copied in segment order for the Gram pass
+       (e = dalloc(ctx, reinterpret_cast<char**>(&ws.perm), L * Hkv * T * (size_t)c.head_dim * elt)) != hipSuccess) ||
       (e = dalloc(ctx, &ws.stat_part, L * Hkv * (size_t)allocate_part_chunks(dm) * 2 * 4)) != hipSuccess ||
       (e = dalloc(ctx, &ws.calib, L)) != hipSuccess ||
       (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||

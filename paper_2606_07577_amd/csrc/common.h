@@ -246,7 +246,7 @@ struct Workspace {
   int* counts;            // [L][2]           K_v, K_a
   float* inv_norm;        // [L][Hkv][max_tokens] inverse norms, segment order
   int* best;              // [L][Hkv][max_tokens] ord_f32 of the best cosine, segment order
-  void* perm;             // [L][Hkv][max_tokens][d] rows in segment order (visual, then audio)
+  void* perm;             // fp32 only: [L][Hkv][max_tokens][d] rows in segment order (visual, then audio)
   int gram_grid;          // persistent Gram workgroups
   double* stat_part;      // [L][Hkv][chunks][2][4]
   double* calib;          // [L] sums of C^(l) over the calibration steps
@@ -391,6 +391,24 @@ __device__ inline void dma16_opaque(const void* g, void* lds) {
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
       : "v"(g), "s"(m0)
+      : "memory");
+}
+
+// dma16_opaque with the global address split into a wave-uniform base (in
+// scalar registers) and a 32-bit per-lane byte offset, so that no 64-bit
+// address arithmetic runs per lane.
+__device__ inline void dma16_opaque_s(const void* base, uint32_t off, void* lds) {
+  const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane(
+      (int)(uintptr_t)(__attribute__((address_space(3))) void*)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"(m0)
       : "memory");
 }
 

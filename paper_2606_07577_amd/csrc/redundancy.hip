@@ -116,7 +116,7 @@ struct GatherShape {
 // counts) for the later kernels.
 constexpr int kListRows = 128;
 
-template <typename T, int D>
+template <typename T, int D, bool PERM>
 __global__ __launch_bounds__(256) void lists_norms(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
                                                    int* __restrict__ pos, int* __restrict__ rank,
                                                    int* __restrict__ counts, T* __restrict__ perm,
@@ -216,7 +216,7 @@ __global__ __launch_bounds__(256) void lists_norms(const LayerDesc* __restrict__
     int64_t o = 0;
     if (in) {
       o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + dst[r];
-      *reinterpret_cast<uint4*>(perm + o * D + sub * EPL) = v[p];
+      if (PERM) *reinterpret_cast<uint4*>(perm + o * D + sub * EPL) = v[p];
       const uint32_t w[4] = {v[p].x, v[p].y, v[p].z, v[p].w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -817,6 +817,341 @@ __global__ void hidden_finish(const LayerDesc* __restrict__ layers, Dims dm, con
   for (int g = 0; g < dm.Hkv; ++g) s[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = v;
 }
 
+// --- Gram max, each pair once (bf16 keys or values) -----------------------------
+// Work layout: a "row" is one block I of 256 segment rows (4 waves x 64)
+// held in registers as MFMA A operands; its tiles are the 64-row tiles
+// t >= 4I of the same segment (the block's own rows and every later row),
+// copied by DMA through the segment's row list straight from the key or
+// value rows into LDS, where they are B operands.  So each pair of rows
+// (i, j) with block(i) <= block(j) is computed once: by the register block of
+// i against the tile of j.  A product becomes a cosine, (dot * inv_j) * inv_i,
+// which enters two maxima: the register row's (a running maximum per lane
+// over the tile rows the lane holds, reduced across lanes once per row of
+// work) and the tile row's (over the lane's 32 register rows in-lane, then
+// over lane halves and waves through LDS, merged into best once per tile).
+// Inside a wave, the MFMAs of one 32-row column block of a tile run while
+// the previous column block's products become cosines, across the per-tile
+// barrier (the score passes' software pipeline).  Register rows and tile
+// rows past the segment carry NaN inverse norms, and a row's pair with itself
+// is set to NaN; fmaxf ignores both.
+constexpr int kSymBlock = 256;
+
+// Tiles of a segment of K rows: register block I sees tiles 4I .. kt-1.
+__device__ inline int64_t sym_seg_tiles(int K) {
+  const int64_t kt = (K + kScoreTile - 1) / kScoreTile, nb = (K + kSymBlock - 1) / kSymBlock;
+  return nb * kt - 2 * nb * (nb - 1);
+}
+
+__device__ inline void gatomic_max(int* p, int v) {
+  typedef __attribute__((address_space(1))) int global_int;
+  __hip_atomic_fetch_max((global_int*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// v_max_f32 / v_max3_f32 written out: a running maximum carried across loop
+// iterations is not known to be canonical, so fmaxf would first quiet it with
+// an extra v_max_f32 per use.  In IEEE mode these return the other operand
+// for a quiet NaN input, the only NaN that reaches them here.
+__device__ inline float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ inline float vmax3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// One phase of gram_sym in a wave: with MMA, the MFMAs (k-steps x the two
+// register row blocks) of the 32 tile rows from LDS row `brow` into `out`;
+// with EPI, interleaved with them (32 / (2 NKS) per MFMA), the products of
+// the previous column block `in` become cosines and enter the row maxima
+// `rmax` and the column maximum `cm`.  LDS fragments are requested two
+// k-steps ahead of their MFMAs.
+template <int NKS, bool MMA, bool EPI>
+__device__ inline void sym_phase(floatx16 (&out)[2], bf16x8 (&a)[2][NKS], const uint16_t* lds, int brow, int half,
+                                 floatx16 (&in)[2], float invj, float (&iv)[2][16], float (&rmax)[2][16],
+                                 float& cm) {
+  using M = Mfma<uint16_t>;
+  using Tl = SwzTile<uint16_t, NKS * 16>;
+  constexpr int NG = 2 * NKS;     // groups, one MFMA each
+  constexpr int PER = 32 / NG;    // cosines per group
+  static_assert(PER * NG == 32 && PER >= 1, "products per lane of a column block");
+  // LDS address of row brow's k-step-ks fragment in the swizzled tile: piece
+  // (2 ks + half) ^ (brow & XM) of the row, that is base ^ (ks << 5) with
+  // base the k-step-0 address (the tile starts on a ROWB boundary and the
+  // row's own offset has no bits below ROWB).  The base is rebuilt per
+  // phase rather than held across the tile loop.
+  static_assert(Tl::ROWB >= 32 * NKS, "k-step bits stay inside a row");
+  typedef __attribute__((address_space(3))) const bf16x8 lds_frag;
+  uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds + brow * Tl::ROWB +
+                  ((half ^ (brow & Tl::XM)) << 4);
+  pin(base);
+  auto frag = [&](int ks) { return *(lds_frag*)(uintptr_t)(base ^ (uint32_t)(ks << 5)); };
+  bf16x8 f[NKS];
+  if (MMA) {
+    f[0] = frag(0);
+    if (NKS > 1) f[1] = frag(1);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int ks = g >> 1, rb = g & 1;
+    if (MMA) {
+      if (rb == 0 && ks + 2 < NKS) f[ks + 2] = frag(ks + 2);
+      pin(a[rb][ks]);
+      out[rb] = M::mma(a[rb][ks], f[ks], ks ? out[rb] : floatx16{});
+    }
+    if (EPI) {
+      float c[PER];
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int e = g * PER + i, erb = e >> 4, r = e & 15;
+        c[i] = in[erb][r] * invj * iv[erb][r];
+        rmax[erb][r] = vmax(rmax[erb][r], c[i]);
+        pin(rmax[erb][r]);
+      }
+#pragma unroll
+      for (int i = 0; i < PER; i += 2) cm = vmax3(cm, c[i], c[i + 1]);
+      pin(cm);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int D, bool BY_XCD>
+__global__ __launch_bounds__(256, 2) void gram_sym(const LayerDesc* __restrict__ layers, Dims dm, int on_keys,
+                                                   const int* __restrict__ counts, const int* __restrict__ pos,
+                                                   const float* __restrict__ inv, int* __restrict__ best) {
+  using T = uint16_t;
+  using M = Mfma<T>;
+  using Tl = SwzTile<T, D>;
+  constexpr int NKS = D / M::KSTEP;
+  constexpr int IPW = Tl::INSTR_PER_WAVE;  // DMA copies per wave and tile
+  constexpr int kMaxL = 1024;
+  constexpr int kSlots = 4;  // column maxima of tiles t - 1 (being merged) .. t + 2 (being written)
+  __shared__ __attribute__((aligned(256))) T jt[2][Tl::ELEMS];  // stages start on row boundaries
+  __shared__ float cmx[kSlots][4][2][kScoreTile];  // [tile][wave][lane half][tile row]
+  __shared__ int64_t lbase[kMaxL + 1];  // first tile of each layer
+  __shared__ int64_t sc[2];             // total tiles, longest row
+
+  if (threadIdx.x == 0) {
+    int64_t w = 0;
+    int tmax = 0;
+    for (int l = 0; l < dm.L; ++l) {
+      lbase[l] = w;
+      const int kv = counts[2 * l], ka = counts[2 * l + 1];
+      w += (int64_t)dm.Hkv * (sym_seg_tiles(kv) + sym_seg_tiles(ka));
+      tmax = max(tmax, (max(kv, ka) + kScoreTile - 1) / kScoreTile);
+    }
+    lbase[dm.L] = w;
+    sc[0] = w;
+    sc[1] = tmax;
+  }
+  __syncthreads();
+  const int64_t W = sc[0];
+  const int i = gridDim.x % kXcds == 0 ? xcd_swizzle(blockIdx.x, gridDim.x) : (int)blockIdx.x;
+  const int wave = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
+  // This lane's DMA pieces of a tile: copy j moves piece (slot % CPR) of
+  // tile row slot / CPR (slot = (wave * IPW + j) * 64 + lane) to its
+  // swizzled place; the rows come through the row list.  (Recomputed where
+  // used: cheaper than registers held across the tile loop.)
+  auto trow = [&](int j, int ln) { return (int)(((uint32_t)(wave * IPW + j) * 64u + (uint32_t)ln) / Tl::CPR); };
+  auto tcol = [&](int j, int ln) {
+    const uint32_t slot = (uint32_t)(wave * IPW + j) * 64u + (uint32_t)ln;
+    return (int)(((slot % Tl::CPR) ^ ((slot / Tl::CPR) & Tl::XM)) * Tl::EPC);
+  };
+  bool first = true;
+
+  auto run_range = [&](int64_t gt, const int64_t gend) {
+    while (gt < gend) {
+      // the row holding tile gt: layer, KV head, modality, register block
+      int l = 0;
+      for (int lo = 0, hi = dm.L - 1; lo < hi;) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (lbase[mid] <= gt) lo = mid; else hi = mid - 1;
+        l = lo;
+      }
+      const int kv = counts[2 * l], ka = counts[2 * l + 1];
+      const int64_t tv = sym_seg_tiles(kv), tav = sym_seg_tiles(ka);
+      int64_t rem = gt - lbase[l];
+      const int g = (int)(rem / (tv + tav));
+      rem -= g * (tv + tav);
+      const int mu = rem >= tv ? 1 : 0;
+      if (mu) rem -= tv;
+      const int K = mu ? ka : kv;
+      const int kt = (K + kScoreTile - 1) / kScoreTile;
+      int I = 0;
+      while (rem >= kt - 4 * I) { rem -= kt - 4 * I; ++I; }
+      const int t0 = 4 * I + (int)rem;
+      const int t1 = (int)min((int64_t)kt, t0 + (gend - gt));
+      gt += t1 - t0;
+
+      const LayerDesc& Ld = layers[l];
+      const T* U = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
+      const int64_t rs = Ld.kv_rs;
+      const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
+      const int64_t seg_off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + (mu ? kv : 0);
+      const float* invs = inv + seg_off;
+      int* bst = best + seg_off;
+      if (!first) __syncthreads();  // every wave is done with the previous row's stages and maxima
+      first = false;
+
+      int pr[IPW];  // source rows of this lane's pieces of the next tile to copy
+      // (byte offsets of rows in one head fit 31 bits, which the entry points check)
+      const uint32_t rs_b = (uint32_t)(rs * (int64_t)sizeof(T));
+      auto rows_of = [&](int t) {
+        int ln = lane;
+        pin(ln);
+#pragma unroll
+        for (int j = 0; j < IPW; ++j) pr[j] = gload<int>(P + (uint32_t)min(t * kScoreTile + trow(j, ln), K - 1));
+      };
+      auto copy = [&](int buf) {
+        int ln = lane;
+        pin(ln);
+#pragma unroll
+        for (int j = 0; j < IPW; ++j)
+          dma16_opaque_s(U, (uint32_t)pr[j] * rs_b + (uint32_t)tcol(j, ln) * (uint32_t)sizeof(T),
+                         &jt[buf][(wave * IPW + j) * 64 * Tl::EPC]);
+      };
+      auto invj_of = [&](int t, int cb) {  // inverse norm of tile row t*64 + cb*32 + lane%32 (NaN past K)
+        const int row = t * kScoreTile + cb * 32 + (lane & 31);
+        const float v = gload<float>(invs + (uint32_t)min(row, K - 1));
+        return row < K ? v : __builtin_nanf("");
+      };
+      rows_of(t0);
+      copy(0);
+      if (t0 + 1 < t1) { rows_of(t0 + 1); copy(1); }
+      if (t0 + 2 < t1) rows_of(t0 + 2);
+      // this wave's 64 register rows (two 32-row blocks of the output)
+      const int c0 = I * kSymBlock + wave * 64;
+      bf16x8 a[2][NKS];
+      float iv[2][16], rmax[2][16];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const int src = gload<int>(P + (uint32_t)min(c0 + rb * 32 + (lane & 31), K - 1));
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+          a[rb][ks] = M::gload(U + ((uint32_t)src * (uint32_t)rs + ks * M::KSTEP + half * M::PER_LANE));
+        int ln = lane;
+        pin(ln);  // the rows below are recomputed per row of work, not held across the loop
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = c0 + rb * 32 + acc_row(r, ln);
+          const float v = gload<float>(invs + (uint32_t)min(row, K - 1));
+          iv[rb][r] = row < K ? v : __builtin_nanf("");
+          rmax[rb][r] = -INFINITY;
+        }
+      }
+      float ij[2] = {invj_of(t0, 0), invj_of(t0, 1)}, ijn[2] = {0.0f, 0.0f};
+      // a column block of tile t that holds the register rows of block rb: the pairs (i, i) are dropped
+      // (lane's column m = lane % 32 is row acc_row(r) for r = 4 (q / 8) + q % 4, q = m - 4 half, if q >= 0
+      // and q % 8 < 4; the register index is computed where it is used, not held across the loop)
+      auto mask_diag = [&](floatx16 (&acc)[2], int t, int cb) {
+        const int col0 = t * kScoreTile + cb * 32;
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+          if (col0 == c0 + rb * 32) {
+            int q = (lane & 31) - half * 4;
+            pin(q);
+            const int rd = q >= 0 && (q & 4) == 0 ? ((q >> 3) << 2) | (q & 3) : -1;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[rb][r] = r == rd ? __builtin_nanf("") : acc[rb][r];
+          }
+      };
+      auto merge = [&](int t) {  // tile t's row maxima over the register block into best
+        if (lane < 16) {
+          const int col = wave * 16 + lane;
+          float m = -INFINITY;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) m = fmaxf(m, fmaxf(cmx[t & 3][w][0][col], cmx[t & 3][w][1][col]));
+          const int row = t * kScoreTile + col;
+          if (row < K && m > -INFINITY) gatomic_max(bst + row, ord_f32(fminf(1.0f, fmaxf(-1.0f, m))));
+        }
+      };
+      floatx16 acc0[2], acc1[2];
+      float cm = -INFINITY;
+      dma_wait();
+      __syncthreads();  // tiles t0 and t0+1 landed
+      sym_phase<NKS, true, false>(acc0, a, jt[0], lane & 31, half, acc1, 0.0f, iv, rmax, cm);
+      // phase A of tile t: MFMAs of its tile rows 32..63 || cosines of its rows 0..31
+      auto phase_a = [&](int t) {
+        mask_diag(acc0, t, 0);
+        cm = -INFINITY;
+        sym_phase<NKS, true, true>(acc1, a, jt[(t - t0) & 1], 32 + (lane & 31), half, acc0, ij[0], iv, rmax, cm);
+        cmx[t & 3][wave][half][lane & 31] = cm;
+      };
+      for (int t = t0; t + 1 < t1; ++t) {
+        const int st = (t - t0) & 1;
+        ijn[0] = invj_of(t + 1, 0);
+        ijn[1] = invj_of(t + 1, 1);
+        phase_a(t);
+        dma_wait();
+        __syncthreads();  // tile t+1 landed; every wave is done with tile t's stage
+        pin(ijn[0]);
+        pin(ijn[1]);
+        if (t + 2 < t1) {
+          copy(st);
+          if (t + 3 < t1) rows_of(t + 3);
+        }
+        if (t > t0) merge(t - 1);
+        // phase B: MFMAs of tile rows 0..31 of tile t+1 || cosines of rows 32..63 of tile t
+        mask_diag(acc1, t, 1);
+        cm = -INFINITY;
+        sym_phase<NKS, true, true>(acc0, a, jt[st ^ 1], lane & 31, half, acc1, ij[1], iv, rmax, cm);
+        cmx[t & 3][wave][half][32 + (lane & 31)] = cm;
+        ij[0] = ijn[0];
+        ij[1] = ijn[1];
+      }
+      {  // the last tile: its phase B has no MFMAs
+        const int t = t1 - 1;
+        phase_a(t);
+        __syncthreads();
+        if (t > t0) merge(t - 1);
+        mask_diag(acc1, t, 1);
+        cm = -INFINITY;
+        sym_phase<NKS, false, true>(acc0, a, jt[0], 0, half, acc1, ij[1], iv, rmax, cm);
+        cmx[t & 3][wave][half][32 + (lane & 31)] = cm;
+      }
+      __syncthreads();  // the last tile's maxima are in LDS
+      merge(t1 - 1);
+      // the register rows' maxima: over the 32 lanes of each half
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        half_wave_max16(rmax[rb], lane);
+        const int row = c0 + rb * 32 + acc_row((lane >> 1) & 15, lane);
+        if ((lane & 1) == 0 && row < K && rmax[rb][0] > -INFINITY)
+          gatomic_max(bst + row, ord_f32(fminf(1.0f, fmaxf(-1.0f, rmax[rb][0]))));
+      }
+    }
+  };
+  // Unit u = (layer, KV head) goes to XCD u % 8 (with BY_XCD; otherwise the
+  // whole grid is one group), whose workgroups take its units k at a time
+  // and split their tiles evenly, so that an XCD's L2 holds the rows of k
+  // units at a time.  One call site of run_range keeps one copy of its code.
+  constexpr int kX = BY_XCD ? kXcds : 1;
+  const int units = dm.L * dm.Hkv;
+  const int px = (int)gridDim.x / kX, x = i / px, ix = i % px;
+  const int64_t per0 = max((int64_t)1, W / max(units, 1));
+  const int k = (int)max((int64_t)1, min((int64_t)8, (sc[1] * px + per0 - 1) / per0));
+  for (int u0 = x; u0 < units; u0 += k * kX) {
+    int64_t tot = 0;
+    for (int jj = 0; jj < k && u0 + jj * kX < units; ++jj) {
+      const int l = (u0 + jj * kX) / dm.Hkv;
+      tot += sym_seg_tiles(counts[2 * l]) + sym_seg_tiles(counts[2 * l + 1]);
+    }
+    const int64_t cu = (tot + px - 1) / px, ga = ix * cu, gb = min(tot, ga + cu);
+    int64_t off = 0;
+    for (int jj = 0; jj < k && u0 + jj * kX < units && off < gb; ++jj) {
+      const int u = u0 + jj * kX, l = u / dm.Hkv, g = u % dm.Hkv;
+      const int64_t per = sym_seg_tiles(counts[2 * l]) + sym_seg_tiles(counts[2 * l + 1]);
+      const int64_t lo = max(ga, off), hi = min(gb, off + per);
+      if (lo < hi) run_range(lbase[l] + g * per + (lo - off), lbase[l] + g * per + (hi - off));
+      off += per;
+    }
+  }
+}
+
 template <typename T, int D>
 void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, const Workspace& ws, float* s,
                   hipStream_t st) {
@@ -827,10 +1162,26 @@ void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, c
   }
   const dim3 glist((unsigned)((dm.max_tokens + kListRows - 1) / kListRows), dm.Hkv, dm.L);
   T* perm = reinterpret_cast<T*>(ws.perm);
+  const bool by_xcd = dm.L * dm.Hkv >= 2 * kXcds && ws.gram_grid % kXcds == 0;
+  if constexpr (sizeof(T) == 2) {  // bf16: each pair once, rows gathered through the row lists
+    OMNIMEM_LAUNCH(ws, K_NORMS, st,
+                   lists_norms<T, D, false><<<glist, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts,
+                                                                   perm, ws.inv_norm, ws.best));
+    if (by_xcd)
+      OMNIMEM_LAUNCH(ws, K_GRAM, st,
+                     gram_sym<D, true><<<ws.gram_grid, 256, 0, st>>>(desc, dm, on_keys, ws.counts, ws.pos,
+                                                                      ws.inv_norm, ws.best));
+    else
+      OMNIMEM_LAUNCH(ws, K_GRAM, st,
+                     gram_sym<D, false><<<ws.gram_grid, 256, 0, st>>>(desc, dm, on_keys, ws.counts, ws.pos,
+                                                                       ws.inv_norm, ws.best));
+    OMNIMEM_LAUNCH(ws, K_GRAM_FINISH, st, gram_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.pos, ws.counts, ws.best, s));
+    return;
+  }
   OMNIMEM_LAUNCH(ws, K_NORMS, st,
-                 lists_norms<T, D><<<glist, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts, perm,
-                                                          ws.inv_norm, ws.best));
-  if (dm.L * dm.Hkv >= 2 * kXcds && ws.gram_grid % kXcds == 0)
+                 lists_norms<T, D, true><<<glist, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts, perm,
+                                                                ws.inv_norm, ws.best));
+  if (by_xcd)
     OMNIMEM_LAUNCH(ws, K_GRAM, st,
                    gram_pass<T, D, true><<<ws.gram_grid, 256, 0, st>>>(desc, dm, ws.counts, perm, ws.inv_norm, ws.best));
   else
