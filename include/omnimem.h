@@ -109,7 +109,10 @@ typedef struct {
   const void* k;            /* [H_kv][N][d] working-set keys (Eq. 3)           */
   const void* v;            /* [H_kv][N][d] working-set values                 */
   int64_t kv_head_stride;   /* elements, shared by k and v                    */
-  int64_t kv_row_stride;    /* elements, shared by k and v                    */
+  int64_t kv_row_stride;    /* elements, shared by k and v; with bf16, below
+                               2^24 bytes and times max_tokens below 2^31
+                               bytes (rows are addressed by 32-bit byte
+                               offsets from a head's base)                  */
   const uint8_t* modality;  /* [N]: 0 visual, 1 audio                         */
   int64_t n_cache;          /* retained rows at the front of the working set  */
   int64_t n_chunk;          /* chunk rows (and chunk queries) at the back     */

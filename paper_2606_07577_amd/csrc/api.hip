@@ -149,6 +149,11 @@ omnimem_status validate(omnimem_ctx* ctx, const omnimem_layer* layers, int need)
           (L.kv_row_stride * esz) % 16 || (L.kv_head_stride * esz) % 16)
         return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: k/v must be 16-byte aligned with row stride >= d and "
                     "strides of whole 16-byte units", l);
+      // bf16 rows are addressed by 32-bit byte offsets from a head's base
+      const int64_t rs_b = L.kv_row_stride * (int64_t)esz;
+      if (c.dtype == OMNIMEM_BF16 && (rs_b >= (int64_t{1} << 24) || rs_b * c.max_tokens >= (int64_t{1} << 31)))
+        return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: bf16 k/v need a row stride below 16 MiB and row "
+                    "stride x max_tokens below 2 GiB", l);
     }
     if (need & NEED_OUT) {
       if (!L.k_out || !L.v_out) return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "layer %d: null k_out or v_out", l);
@@ -499,7 +504,7 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       (e = dalloc(ctx, &ws.lse_part, L * Hq * (size_t)dm.qb * kMaxSeg * kScoreBlock)) != hipSuccess ||
       (e = dalloc(ctx, &ws.lse2, L * Hq * Cm)) != hipSuccess ||
       (e = dalloc(ctx, &ws.part, L * Hq * (size_t)dm.kb * kMaxSeg * kScoreBlock)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.pos, L * 2 * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.pos, L * 2 * (size_t)list_stride(T))) != hipSuccess ||
       (e = dalloc(ctx, &ws.rank, L * T)) != hipSuccess ||
       (e = dalloc(ctx, &ws.counts, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.inv_norm, L * Hkv * T)) != hipSuccess ||

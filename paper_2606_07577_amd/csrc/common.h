@@ -214,6 +214,12 @@ __device__ inline float unord_f32(int i) { return __int_as_float(i ^ ((i >> 31) 
 
 constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
 
+// The modality row lists hold max_tokens entries plus kListPad more after
+// each list's end, set to the list's last row: a 64-row tile or a 256-row
+// register block that runs past a segment's end reads valid rows.
+constexpr int kListPad = 256;
+__host__ __device__ inline int64_t list_stride(int64_t max_tokens) { return max_tokens + kListPad; }
+
 // ---------------------------------------------------------------------------
 // Optional launch timing (see omnimem_profile).
 // ---------------------------------------------------------------------------
@@ -241,7 +247,7 @@ struct Workspace {
   float2* lse_part;       // [L][Hq][qb][kMaxSeg][256] partial (reference, sum) in log2 units
   float* lse2;            // [L][Hq][max_chunk] merged normaliser, log2 units
   float* part;            // [L][Hq][kb][kMaxSeg][256] partial column sums per query head
-  int* pos;               // [L][2][max_tokens] visual rows, audio rows (ascending)
+  int* pos;               // [L][2][max_tokens + kListPad] visual rows, audio rows (ascending)
   int* rank;              // [L][max_tokens]  rank of row j inside its modality
   int* counts;            // [L][2]           K_v, K_a
   float* inv_norm;        // [L][Hkv][max_tokens] inverse norms, segment order

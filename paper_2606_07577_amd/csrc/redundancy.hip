@@ -36,8 +36,8 @@ __global__ __launch_bounds__(1024) void modality_lists(const LayerDesc* __restri
   __shared__ int wave_tot[16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
   const unsigned long long lt = (1ull << lane) - 1ull;
-  int* Pv = pos + (int64_t)(2 * l) * dm.max_tokens;
-  int* Pa = Pv + dm.max_tokens;
+  int* Pv = pos + (int64_t)(2 * l) * list_stride(dm.max_tokens);
+  int* Pa = Pv + list_stride(dm.max_tokens);
   int* R = rank + (int64_t)l * dm.max_tokens;
   // Wave w owns rows [w * 64S, (w + 1) * 64S); step i covers the 64
   // consecutive rows w * 64S + 64 i + lane, so reads and writes coalesce.
@@ -188,6 +188,7 @@ __global__ __launch_bounds__(256) void lists_norms(const LayerDesc* __restrict__
   const int kv = wv_total[0] + wv_total[1] + wv_total[2] + wv_total[3];
   if (wave == 0) {  // the 64-row steps of the workgroup's rows, in order
     int vb = wv_before[0] + wv_before[1] + wv_before[2] + wv_before[3];
+    int last[2] = {-1, -1};  // the last row of each list, if this workgroup holds it
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int j = j0 + q * 64 + lane;
@@ -199,13 +200,25 @@ __global__ __launch_bounds__(256) void lists_norms(const LayerDesc* __restrict__
       if (in) {
         dst[q * 64 + lane] = vis ? r : kv + r;
         if (g == 0) {
-          pos[(int64_t)(2 * l + (vis ? 0 : 1)) * dm.max_tokens + r] = j;
+          pos[(int64_t)(2 * l + (vis ? 0 : 1)) * list_stride(dm.max_tokens) + r] = j;
           rank[(int64_t)l * dm.max_tokens + j] = r;
         }
+        if (r == (vis ? kv : N - kv) - 1) last[vis ? 0 : 1] = j;
       }
       vb += __popcll(bal);
     }
     if (g == 0 && blockIdx.x == 0 && lane == 0) { counts[2 * l] = kv; counts[2 * l + 1] = N - kv; }
+    if (g == 0) {  // each list's padding repeats its last row
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const unsigned long long has = __ballot(last[m] >= 0);
+        if (has) {
+          const int jl = __shfl(last[m], __ffsll((long long)has) - 1, 64);
+          int* pad = pos + (int64_t)(2 * l + m) * list_stride(dm.max_tokens) + (m ? N - kv : kv);
+          for (int e = lane; e < kListPad; e += 64) pad[e] = jl;
+        }
+      }
+    }
   }
   __syncthreads();
 #pragma unroll
@@ -444,7 +457,8 @@ __global__ void gram_finish(const LayerDesc* __restrict__ layers, Dims dm, const
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= N) return;
   const int kv = counts[2 * l];
-  const int row = k < kv ? pos[(int64_t)(2 * l) * dm.max_tokens + k] : pos[(int64_t)(2 * l + 1) * dm.max_tokens + k - kv];
+  const int64_t ls = list_stride(dm.max_tokens);
+  const int row = k < kv ? pos[(int64_t)(2 * l) * ls + k] : pos[(int64_t)(2 * l + 1) * ls + k - kv];
   const int64_t o = ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
   const int b = best[o + k];
   s[o + row] = b == kNoPartner ? 0.0f : fminf(1.0f, fmaxf(-1.0f, unord_f32(b)));
@@ -475,7 +489,7 @@ __global__ void adjacent_cos(const LayerDesc* __restrict__ layers, Dims dm, int 
   if (j >= N) return;
   const int mu = Ld.mod[j] ? 1 : 0;
   const int K = counts[2 * l + mu];
-  const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
+  const int* P = pos + (int64_t)(2 * l + mu) * list_stride(dm.max_tokens);
   const int t = rank[(int64_t)l * dm.max_tokens + j];
   const T* u = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
   const T* x = u + (int64_t)j * Ld.kv_rs;
@@ -517,7 +531,7 @@ __global__ __launch_bounds__(256) void adjacent_cos_hidden(const LayerDesc* __re
   if (j >= N) return;  // the whole wave leaves
   const int mu = Ld.mod[j] ? 1 : 0;
   const int K = counts[2 * l + mu];
-  const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
+  const int* P = pos + (int64_t)(2 * l + mu) * list_stride(dm.max_tokens);
   const int t = rank[(int64_t)l * dm.max_tokens + j];
   const int jp = t > 0 ? P[t - 1] : -1, jn = t + 1 < K ? P[t + 1] : -1;
   const T* H = reinterpret_cast<const T*>(Ld.hidden);
@@ -698,7 +712,7 @@ __global__ __launch_bounds__(wide_threads<T>(), 2) void gram_wide(
     while (r >= nb - bi) { r -= nb - bi; ++bi; }
     const int bj = bi + r;
     const LayerDesc Ld = layers[l];
-    const int* P = pos + (int64_t)q * dm.max_tokens;
+    const int* P = pos + (int64_t)q * list_stride(dm.max_tokens);
     __syncthreads();  // every wave is done with the previous pair's LDS
     for (int t = threadIdx.x; t < 2 * BR; t += blockDim.x) {
       const int side = t / BR, k = t % BR;
@@ -889,6 +903,7 @@ __device__ inline void sym_phase(floatx16 (&out)[2], bf16x8 (&a)[2][NKS], const 
   pin(base);
   auto frag = [&](int ks) { return *(lds_frag*)(uintptr_t)(base ^ (uint32_t)(ks << 5)); };
   bf16x8 f[NKS];
+  if (MMA) __builtin_amdgcn_s_setprio(1);  // a wave in its MFMA stream issues ahead of one in the tile bookkeeping
   if (MMA) {
     f[0] = frag(0);
     if (NKS > 1) f[1] = frag(1);
@@ -917,6 +932,7 @@ __device__ inline void sym_phase(floatx16 (&out)[2], bf16x8 (&a)[2][NKS], const 
     }
     __builtin_amdgcn_sched_barrier(0);
   }
+  if (MMA) __builtin_amdgcn_s_setprio(0);
 }
 
 template <int D, bool BY_XCD>
@@ -952,15 +968,15 @@ __global__ __launch_bounds__(256, 2) void gram_sym(const LayerDesc* __restrict__
   const int64_t W = sc[0];
   const int i = gridDim.x % kXcds == 0 ? xcd_swizzle(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const int wave = wave_id(), lane = threadIdx.x & 63, half = lane >> 5;
-  // This lane's DMA pieces of a tile: copy j moves piece (slot % CPR) of
-  // tile row slot / CPR (slot = (wave * IPW + j) * 64 + lane) to its
-  // swizzled place; the rows come through the row list.  (Recomputed where
-  // used: cheaper than registers held across the tile loop.)
-  auto trow = [&](int j, int ln) { return (int)(((uint32_t)(wave * IPW + j) * 64u + (uint32_t)ln) / Tl::CPR); };
-  auto tcol = [&](int j, int ln) {
-    const uint32_t slot = (uint32_t)(wave * IPW + j) * 64u + (uint32_t)ln;
-    return (int)(((slot % Tl::CPR) ^ ((slot / Tl::CPR) & Tl::XM)) * Tl::EPC);
-  };
+  // This lane's DMA pieces of a tile: copy j moves piece ln % CPR of tile
+  // row (wave * IPW + j) * RPI + ln / CPR (RPI rows per copy) to its
+  // swizzled place, piece (ln % CPR) ^ (row & XM); the rows come through the
+  // row list.  As wave * IPW * RPI is a multiple of XM + 1, the swizzle is
+  // the lane's own, ((ln % CPR) ^ (ln / CPR)) << 4 bytes, xor the copy's
+  // ((j * RPI) & XM) << 4.  (Recomputed where used: cheaper than registers
+  // held across the tile loop.)
+  constexpr int RPI = 64 / Tl::CPR;
+  static_assert((IPW * RPI) % (Tl::XM + 1) == 0 && RPI <= Tl::XM + 1, "copy swizzle is per lane");
   bool first = true;
 
   auto run_range = [&](int64_t gt, const int64_t gend) {
@@ -990,7 +1006,7 @@ __global__ __launch_bounds__(256, 2) void gram_sym(const LayerDesc* __restrict__
       const LayerDesc& Ld = layers[l];
       const T* U = reinterpret_cast<const T*>(on_keys ? Ld.k : Ld.v) + (int64_t)g * Ld.kv_hs;
       const int64_t rs = Ld.kv_rs;
-      const int* P = pos + (int64_t)(2 * l + mu) * dm.max_tokens;
+      const int* P = pos + (int64_t)(2 * l + mu) * list_stride(dm.max_tokens);
       const int64_t seg_off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens + (mu ? kv : 0);
       const float* invs = inv + seg_off;
       int* bst = best + seg_off;
@@ -1000,18 +1016,21 @@ __global__ __launch_bounds__(256, 2) void gram_sym(const LayerDesc* __restrict__
       int pr[IPW];  // source rows of this lane's pieces of the next tile to copy
       // (byte offsets of rows in one head fit 31 bits, which the entry points check)
       const uint32_t rs_b = (uint32_t)(rs * (int64_t)sizeof(T));
+      // (rows past the segment come from the list's padding, which repeats its last row)
       auto rows_of = [&](int t) {
         int ln = lane;
         pin(ln);
+        const int* Pt = P + (t * kScoreTile + wave * IPW * RPI);
 #pragma unroll
-        for (int j = 0; j < IPW; ++j) pr[j] = gload<int>(P + (uint32_t)min(t * kScoreTile + trow(j, ln), K - 1));
+        for (int j = 0; j < IPW; ++j) pr[j] = gload<int>(Pt + ((uint32_t)ln / Tl::CPR + j * RPI));
       };
       auto copy = [&](int buf) {
         int ln = lane;
         pin(ln);
+        const uint32_t colb = (((uint32_t)ln % Tl::CPR) ^ ((uint32_t)ln / Tl::CPR)) << 4;
 #pragma unroll
         for (int j = 0; j < IPW; ++j)
-          dma16_opaque_s(U, (uint32_t)pr[j] * rs_b + (uint32_t)tcol(j, ln) * (uint32_t)sizeof(T),
+          dma16_opaque_s(U, __umul24((uint32_t)pr[j], rs_b) + (colb ^ (uint32_t)(((j * RPI) & Tl::XM) << 4)),
                          &jt[buf][(wave * IPW + j) * 64 * Tl::EPC]);
       };
       auto invj_of = [&](int t, int cb) {  // inverse norm of tile row t*64 + cb*32 + lane%32 (NaN past K)
@@ -1029,7 +1048,7 @@ __global__ __launch_bounds__(256, 2) void gram_sym(const LayerDesc* __restrict__
       float iv[2][16], rmax[2][16];
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb) {
-        const int src = gload<int>(P + (uint32_t)min(c0 + rb * 32 + (lane & 31), K - 1));
+        const int src = gload<int>(P + (uint32_t)(c0 + rb * 32 + (lane & 31)));
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
           a[rb][ks] = M::gload(U + ((uint32_t)src * (uint32_t)rs + ks * M::KSTEP + half * M::PER_LANE));
@@ -1059,13 +1078,12 @@ __global__ __launch_bounds__(256, 2) void gram_sym(const LayerDesc* __restrict__
             for (int r = 0; r < 16; ++r) acc[rb][r] = r == rd ? __builtin_nanf("") : acc[rb][r];
           }
       };
-      auto merge = [&](int t) {  // tile t's row maxima over the register block into best
-        if (lane < 16) {
-          const int col = wave * 16 + lane;
+      auto merge = [&](int t) {  // tile t's row maxima over the register block into best, by wave t % 4
+        if (wave == (t & 3)) {
           float m = -INFINITY;
 #pragma unroll
-          for (int w = 0; w < 4; ++w) m = fmaxf(m, fmaxf(cmx[t & 3][w][0][col], cmx[t & 3][w][1][col]));
-          const int row = t * kScoreTile + col;
+          for (int w = 0; w < 4; ++w) m = fmaxf(m, fmaxf(cmx[t & 3][w][0][lane], cmx[t & 3][w][1][lane]));
+          const int row = t * kScoreTile + lane;
           if (row < K && m > -INFINITY) gatomic_max(bst + row, ord_f32(fminf(1.0f, fmaxf(-1.0f, m))));
         }
       };
