@@ -29,17 +29,31 @@ PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}       # dense MFMA
 KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f in (
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
-    "qwen7b-layer-6144": {
-        "sources_sha256": "c4d6533d57b87d112b8ecf941048f3c127491957c653bd14de5dca96304291a1",
-        "lse_pass": 31186220, "colsum_pass": 32981324, "gram_pass": 15426726, "psi_topk": 818054, "gather_compact": 16886966,
+    "qwen7b-stream-64x28": {
+        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "append_chunk": 235255686, "lse_pass": 604414862, "lse_merge": 19381020, "colsum_pass": 622617905,
+        "head_sum": 21741403, "lists_norms": 181331651, "gram_sym": 816381184, "gram_finish": 6206193,
+        "avba_partials": 6040922, "avba_allocate": 180771, "psi_topk": 17178582, "stage_moved_back": 15209435,
+        "gather_inplace": 417910033,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "c4d6533d57b87d112b8ecf941048f3c127491957c653bd14de5dca96304291a1",
-        "lse_pass": 609988761, "colsum_pass": 615876283, "gram_pass": 805820510, "psi_topk": 14596168, "gather_compact": 471766999,
+        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "lse_pass": 608607492, "lse_merge": 19381168, "colsum_pass": 613155300, "head_sum": 22114184,
+        "lists_norms": 184701051, "gram_sym": 822267402, "gram_finish": 6248421, "avba_partials": 6078432,
+        "avba_allocate": 123709, "psi_topk": 14666015, "gather_compact": 471798186,
+    },
+    "qwen7b-layer-6144": {
+        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "lse_pass": 31059193, "lse_merge": 1738838, "colsum_pass": 33068509, "head_sum": 1292309,
+        "lists_norms": 6740159, "gram_sym": 14033861, "gram_finish": 245756, "avba_partials": 300160,
+        "avba_allocate": 36063, "psi_topk": 861627, "gather_compact": 16889831,
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "c4d6533d57b87d112b8ecf941048f3c127491957c653bd14de5dca96304291a1",
-        "lse_pass": 31191157, "colsum_pass": 32971231, "gram_wide": 188147568, "psi_topk": 254395, "gather_compact": 16887551,
+        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "lse_pass": 31060948, "lse_merge": 1738710, "colsum_pass": 33071501, "head_sum": 1292280,
+        "modality_lists": 65787, "hidden_norms": 44175419, "gram_wide": 188161894, "hidden_finish": 138273,
+        "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 265346, "psi_topk": 271034,
+        "gather_compact": 16889947, "gather_hidden": 58879344,
     },
 }
 
@@ -180,6 +194,7 @@ def layer_work(h_q, c, n_cache, h_kv, n, d, elt, k_v, k_a, m, causal=True):
 def work_table(score, gram, topk, compact):
     """Per-launch algorithmic units of each counted kernel."""
     return {"lse_pass": ("mfma", score), "colsum_pass": ("mfma", score), "gram_pass": ("mfma", gram),
+            "gram_sym": ("mfma", gram),
             "gram_wide": ("mfma", gram),
             "gather_compact": ("hbm", compact), "gather_inplace": ("hbm", compact), "psi_topk": ("hbm", topk)}
 
@@ -450,25 +465,35 @@ def run_stream(args, torch):
     app_ms, abi_ms = run.timings()
     run.close()
 
-    # And again with per-kernel HIP events; per-step work from the shapes
-    # each step saw.
+    # The shapes each step saw (kept rows, audio rows, budgets), read back in
+    # a pass of their own (the stream is deterministic: every pass sees the
+    # same), then the stream again with per-kernel HIP events and no
+    # read-back beyond the budgets push itself waits for.
     run = fix(runner())
-    run.ctx.omnimem_profile(True)
-    tot = [0, 0, 0, 0]
-    elt = 2 if spec["dtype"] == "bf16" else 4
+    shapes = []
     for t in range(steps):
         n_cache = list(run.n_cache)
         k_a = [int((run.cache_modality(l) == 1).sum()) for l in range(spec["n_layers"])]
         budgets = run.push(chunks[t], stream)
+        shapes.append((n_cache, k_a, [int(budgets[l].sum()) for l in range(spec["n_layers"])]))
+    torch.cuda.synchronize()
+    run.close()
+    run = fix(runner())
+    run.ctx.omnimem_profile(True)
+    for t in range(steps):
+        run.push(chunks[t], stream)
+    torch.cuda.synchronize()
+    kernels = run.ctx.omnimem_profile_report()
+    run.close()
+    tot = [0, 0, 0, 0]
+    elt = 2 if spec["dtype"] == "bf16" else 4
+    for n_cache, k_a, kept in shapes:
         for l in range(spec["n_layers"]):
             ka = k_a[l] + spec["n_frames"] * spec["frame_a"]
             n = n_cache[l] + src.chunk_len
             w = layer_work(spec["h_q"], src.chunk_len, n_cache[l], spec["h_kv"], n, spec["d"], elt,
-                           n - ka, ka, int(budgets[l].sum()))
+                           n - ka, ka, kept[l])
             tot = [x + y for x, y in zip(tot, w)]
-    torch.cuda.synchronize()
-    kernels = run.ctx.omnimem_profile_report()
-    run.close()
     work = work_table(*[x / steps for x in tot])
     config = {"workload": args.workload, "layers": spec["n_layers"], "q_heads": spec["h_q"],
               "kv_heads": spec["h_kv"], "head_dim": spec["d"], "chunks": steps,
@@ -547,7 +572,7 @@ def main():
         return round(u / t / scale / peak_units, 4) if t > 0 else None
 
     fractions = {
-        "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_pass", "gram_wide"],
+        "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_pass", "gram_sym", "gram_wide"],
                                            PEAK_MFMA_TFLOPS[dtype], 1e12),
         "hbm_frac_topk_compact": stage_frac(["psi_topk", "gather_compact", "gather_inplace", "stage_moved_back"],
                                             PEAK_HBM_GBS, 1e9),

@@ -57,7 +57,7 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 static const char* kKernelNames[K_COUNT] = {
     "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact",
     "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish", "layer_inputs",
-    "stage_moved_back", "gather_inplace", "append_chunk"};
+    "stage_moved_back", "gather_inplace", "append_chunk", "gram_sym"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -771,7 +771,9 @@ omnimem_status omnimem_profile(omnimem_ctx* ctx, int32_t on) {
   if (on && ctx->prof.pool.empty()) {
     ctx->prof.pool.resize(kProfEvents);
     for (auto& e : ctx->prof.pool) {
-      hipError_t err = hipEventCreate(&e);
+      // timing only: no system-scope fence (cache writeback and invalidation) at each record,
+      // which would slow the kernel that follows it
+      hipError_t err = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
       if (err != hipSuccess) return hip_fail(ctx, err, "profiling events");
     }
   }

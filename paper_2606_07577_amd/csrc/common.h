@@ -226,7 +226,7 @@ __host__ __device__ inline int64_t list_stride(int64_t max_tokens) { return max_
 enum KernelId {
   K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
   K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_LAYER_IN,
-  K_STAGE, K_GATHER_IP, K_APPEND, K_COUNT
+  K_STAGE, K_GATHER_IP, K_APPEND, K_GRAM_SYM, K_COUNT
 };
 struct Profiler;
 void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);

@@ -1186,11 +1186,11 @@ void launch_typed(const Dims& dm, int sim, int on_keys, const LayerDesc* desc, c
                    lists_norms<T, D, false><<<glist, 256, 0, st>>>(desc, dm, on_keys, ws.pos, ws.rank, ws.counts,
                                                                    perm, ws.inv_norm, ws.best));
     if (by_xcd)
-      OMNIMEM_LAUNCH(ws, K_GRAM, st,
+      OMNIMEM_LAUNCH(ws, K_GRAM_SYM, st,
                      gram_sym<D, true><<<ws.gram_grid, 256, 0, st>>>(desc, dm, on_keys, ws.counts, ws.pos,
                                                                       ws.inv_norm, ws.best));
     else
-      OMNIMEM_LAUNCH(ws, K_GRAM, st,
+      OMNIMEM_LAUNCH(ws, K_GRAM_SYM, st,
                      gram_sym<D, false><<<ws.gram_grid, 256, 0, st>>>(desc, dm, on_keys, ws.counts, ws.pos,
                                                                        ws.inv_norm, ws.best));
     OMNIMEM_LAUNCH(ws, K_GRAM_FINISH, st, gram_finish<<<gtok, 256, 0, st>>>(desc, dm, ws.pos, ws.counts, ws.best, s));
