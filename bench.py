@@ -24,32 +24,33 @@ PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}       # dense MFMA
 # HBM bytes per launch from two rocprofv3 counter passes (FETCH_SIZE, then
 # WRITE_SIZE, KiB per dispatch), each divided by what that counter reads for a
 # plain 1 GiB device-to-device copy (FETCH_SIZE 0.5x, WRITE_SIZE 1.0x), with
-# the SHA-256 of the library sources the counters were taken on.  A source
-# change makes the figures stale: the roofline then reports traffic null.
+# the SHA-256 of the code of the library sources the counters were taken on
+# (comments and blank lines left out).  A code change makes the figures
+# stale: the roofline then reports traffic null.
 KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f in (
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
-        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
         "append_chunk": 235255686, "lse_pass": 604414862, "lse_merge": 19381020, "colsum_pass": 622617905,
         "head_sum": 21741403, "lists_norms": 181331651, "gram_sym": 816381184, "gram_finish": 6206193,
         "avba_partials": 6040922, "avba_allocate": 180771, "psi_topk": 17178582, "stage_moved_back": 15209435,
         "gather_inplace": 417910033,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
         "lse_pass": 608607492, "lse_merge": 19381168, "colsum_pass": 613155300, "head_sum": 22114184,
         "lists_norms": 184701051, "gram_sym": 822267402, "gram_finish": 6248421, "avba_partials": 6078432,
         "avba_allocate": 123709, "psi_topk": 14666015, "gather_compact": 471798186,
     },
     "qwen7b-layer-6144": {
-        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
         "lse_pass": 31059193, "lse_merge": 1738838, "colsum_pass": 33068509, "head_sum": 1292309,
         "lists_norms": 6740159, "gram_sym": 14033861, "gram_finish": 245756, "avba_partials": 300160,
         "avba_allocate": 36063, "psi_topk": 861627, "gather_compact": 16889831,
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "01797c7e171723fa580b484c19497e1f2928508b59c80e4e12f00a4d0380f95b",
+        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
         "lse_pass": 31060948, "lse_merge": 1738710, "colsum_pass": 33071501, "head_sum": 1292280,
         "modality_lists": 65787, "hidden_norms": 44175419, "gram_wide": 188161894, "hidden_finish": 138273,
         "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 265346, "psi_topk": 271034,
@@ -58,12 +59,44 @@ MEASURED_TRAFFIC = {
 }
 
 
+def _code_only(text):
+    """The source without its comments and blank lines: what the counters
+    depend on is the code, so a comment edit does not make them stale."""
+    out, i, n, quote = [], 0, len(text), None
+    while i < n:
+        c = text[i]
+        if quote:
+            out.append(c)
+            if c == "\\" and i + 1 < n:
+                out.append(text[i + 1])
+                i += 2
+                continue
+            if c == quote:
+                quote = None
+            i += 1
+        elif c in "\"'":
+            quote = c
+            out.append(c)
+            i += 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return "\n".join(line.rstrip() for line in "".join(out).split("\n") if line.strip())
+
+
 def sources_sha256():
     import hashlib
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 

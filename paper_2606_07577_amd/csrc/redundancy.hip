@@ -3,15 +3,15 @@
 //
 // Two modes:
 //  SIM_MAX  s_k = max over the other rows j of k's (KV head, modality)
-//           segment of cos(u_k, u_j).  The segment's rows are first gathered
-//           into one contiguous block (visual rows, then audio rows, each in
-//           ascending order) with their fp32 inverse norms; the Gram matrix
-//           U U^T is then computed on MFMA, the whole matrix (both
-//           triangles) in 256 x 64 tiles (raw bf16/fp32 inputs, fp32
-//           accumulation), scaled by the inverse norms and reduced to row
-//           maxima in registers; maxima merge with atomicMax on an
-//           order-preserving int encoding.  The N x N matrix never leaves
-//           the chip.
+//           segment of cos(u_k, u_j).  lists_norms builds the segment's row
+//           list (visual rows, then audio rows, each ascending) and fp32
+//           inverse norms.  The Gram matrix U U^T is computed on MFMA in
+//           256 x 64 tiles with fp32 accumulation and never leaves the chip:
+//           for bf16 rows (gram_sym) each pair once, rows gathered through
+//           the list by DMA, each product scaled into a cosine that enters
+//           both rows' maxima; for fp32 rows (gram_pass) the whole matrix
+//           over a copy of the rows in list order.  Maxima merge with
+//           atomicMax on an order-preserving int encoding.
 //  SIM_ADJ  Eq. (7) as printed: mean cosine with the previous and next row
 //           of the same modality, in fp64.
 #include "common.h"
