@@ -8,6 +8,8 @@ index sets are bit-exact where the oracle's psi margin at the M-th boundary
 exceeds 1e-3 relative; otherwise every kept row must have psi >= psi_(M)
 (1 - 1e-3) and every dropped row psi <= psi_(M) (1 + 1e-3).
 """
+import math
+
 import numpy as np
 
 from oracle import omnimem_oracle as om
@@ -118,3 +120,28 @@ def as_f64(layer):
     for key in ("q", "k", "v"):
         out[key] = np.asarray(layer[key], dtype=np.float64)
     return out
+
+
+def free_running_budget_bounds(gpu_stats, ref_stats, shares, ref_budgets, temperature=TEMPERATURE):
+    """Per-layer bounds on |M_v - M_v_ref| and |M_a - M_a_ref| when the
+    budgets come from the GPU's own a and s, derived from the measured
+    differences of the statistics (Eqs. 13, 14 and readings R16-R18):
+
+    x_l = clamp(kappa B_tot p_l, lo_l, hi_l), p = softmax(C / T).  If every
+    C_l moves by at most dC, each p_l moves by a factor within exp(+-2 dC/T),
+    kappa (fixed by sum x = B_tot) by at most the same, and the clamp does not
+    amplify: |dx_l| <= x_l (exp(4 dC/T) - 1).  The integer budgets (R17) add
+    at most one unit (a floor crossing or a change in the remainder order):
+    |dB_l| <= ceil(|dx_l|) + 1.  The split M_v = floor(w_v B_l + 1/2), clamped
+    (R18), moves by at most |dB_l| + B_l |dw_v| + 1, and M_a = B_l - M_v by
+    at most |dB_l| + |dM_v|.
+    """
+    d_c = max(abs(float(g[8]) - float(r["C_l"])) for g, r in zip(gpu_stats, ref_stats))
+    grow = math.expm1(4.0 * d_c / temperature)
+    out = []
+    for l, (g, r) in enumerate(zip(gpu_stats, ref_stats)):
+        d_b = math.ceil(float(shares[l]) * grow) + 1
+        b_l = int(ref_budgets[l].sum())
+        d_mv = d_b + math.ceil(b_l * abs(float(g[9]) - float(r["w_v"]))) + 1
+        out.append((d_mv, d_b + d_mv))
+    return np.array(out, dtype=np.int64)

@@ -191,17 +191,20 @@ def test_select_compact_teacher_forced(name):
 
 @pytest.mark.parametrize("name", FULL_CASES)
 def test_chain_free_running(name):
-    # The GPU's own a, s -> budgets -> kept rows; budgets close to the
-    # oracle's, the kept rows a valid top-M of the oracle's psi under the
-    # GPU's budgets, and the compacted caches exactly the kept rows.
+    # The GPU's own a, s -> budgets -> kept rows; budgets within the bounds
+    # that the measured differences of the statistics imply, the kept rows a
+    # valid top-M of the oracle's psi under the GPU's budgets, and the
+    # compacted caches exactly the kept rows.
     c = get_case(name)
     a_o, s_o = [], []
     for lay in c.layers64:
         a_o.append(om.attention_importance(lay["q"], lay["k"], lay["n_cache"], lay["sm_scale"], c.causal))
         s_o.append(om.redundancy(lay["v"], lay["modality"], c.mode))
-    _, _, ref_budgets = P.oracle_allocation(a_o, s_o, c.layers, c.budget)
+    ref_stats, shares, ref_budgets = P.oracle_allocation(a_o, s_o, c.layers, c.budget)
     assert c.budgets.sum() == ref_budgets.sum()
-    assert np.abs(c.budgets - ref_budgets).max() <= max(1, int(2e-3 * ref_budgets.max()))
+    bounds = P.free_running_budget_bounds(c.stats, ref_stats, shares, ref_budgets)
+    print(f"{name}: budget differences {np.abs(c.budgets - ref_budgets).max()} within bounds up to {bounds.max()}")
+    assert (np.abs(c.budgets - ref_budgets) <= bounds).all(), (c.budgets, ref_budgets, bounds)
     for l, lay in enumerate(c.layers):
         mv, ma = c.budgets[l]
         psi = om.retention_score(a_o[l], s_o[l], P.LAMBDA)

@@ -259,11 +259,13 @@ def test_post_eviction_working_sets_full_size(t):
         P.assert_close_s(run.s[l, :, :n].cpu().numpy(), s, f"s chunk {t} layer {l}")
         a_ref.append(a)
         s_ref.append(s)
-    _, _, ref_budgets = P.oracle_allocation(a_ref, s_ref, layers, L * 4096)
+    ref_stats, shares, ref_budgets = P.oracle_allocation(a_ref, s_ref, layers, L * 4096)
     print(f"chunk {t}: N {[len(x['modality']) for x in layers]} budgets gpu {budgets.tolist()} "
           f"oracle {ref_budgets.tolist()}", flush=True)
     assert budgets.sum() == ref_budgets.sum()
-    assert np.abs(budgets - ref_budgets).max() <= max(1, int(2e-3 * ref_budgets.max()))
+    bounds = P.free_running_budget_bounds(run.stats.cpu().numpy(), ref_stats, shares, ref_budgets)
+    print(f"chunk {t}: budget differences {np.abs(budgets - ref_budgets).max()} within bounds up to {bounds.max()}")
+    assert (np.abs(budgets - ref_budgets) <= bounds).all(), (budgets, ref_budgets, bounds)
     for l, lay in enumerate(layers):
         mv, ma = budgets[l]
         psi = om.retention_score(a_ref[l], s_ref[l], P.LAMBDA)
