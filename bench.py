@@ -215,25 +215,29 @@ def roof_probe(torch):
 
 def layer_work(h_q, c, n_cache, h_kv, n, d, elt, k_v, k_a, m, causal=True):
     """Algorithmic units of one layer in one step: score flops (per pass),
-    Gram flops, top-k bytes, compaction bytes."""
+    Gram flops, top-k bytes read (a, s, modality) and written (idx),
+    compaction bytes."""
     pairs = c * n_cache + c * (c + 1) // 2 if causal else c * n
     score = 2 * d * h_q * pairs
     gram = h_kv * (k_v * (k_v - 1) + k_a * (k_a - 1)) * d   # K(K-1)/2 pairs x 2d per segment
-    topk = h_kv * n * (4 + 4) + n + 4 * h_kv * m             # a, s, modality in; idx out
+    topk_in = h_kv * n * (4 + 4) + n                         # a, s, modality in
+    topk_out = 4 * h_kv * m                                   # idx out
     compact = 2 * 2 * h_kv * m * d * elt                      # K and V rows, read + write
-    return score, gram, topk, compact
+    return score, gram, topk_in, topk_out, compact
 
 
-def work_table(score, gram, topk, compact):
-    """Per-launch algorithmic units of each counted kernel."""
+def work_table(score, gram, topk_in, topk_out, compact):
+    """Per-launch algorithmic units of each counted kernel (the split top-k's
+    inputs are read by topk_hist and its output written by topk_emit)."""
     return {"lse_pass": ("mfma", score), "colsum_pass": ("mfma", score), "gram_pass": ("mfma", gram),
             "gram_sym": ("mfma", gram),
             "gram_wide": ("mfma", gram),
-            "gather_compact": ("hbm", compact), "gather_inplace": ("hbm", compact), "psi_topk": ("hbm", topk)}
+            "gather_compact": ("hbm", compact), "gather_inplace": ("hbm", compact),
+            "psi_topk": ("hbm", topk_in + topk_out), "topk_hist": ("hbm", topk_in), "topk_emit": ("hbm", topk_out)}
 
 
 def static_work(layers, budgets, hidden_dim=0):
-    tot = [0, 0, 0, 0]
+    tot = [0, 0, 0, 0, 0]
     for lay, (mv, ma) in zip(layers, budgets):
         h_q, c, d = lay["q"].shape
         h_kv, n, _ = lay["k"].shape
@@ -242,7 +246,7 @@ def static_work(layers, budgets, hidden_dim=0):
         w = layer_work(h_q, c, lay["n_cache"], h_kv, n, d, 2 if lay["dtype"] == "bf16" else 4,
                        k_v, k_a, int(mv) + int(ma))
         if hidden_dim:  # the Gram on the layer's hidden states: one per layer, d_model wide
-            w = (w[0], (k_v * (k_v - 1) + k_a * (k_a - 1)) * hidden_dim, w[2], w[3])
+            w = (w[0], (k_v * (k_v - 1) + k_a * (k_a - 1)) * hidden_dim) + tuple(w[2:])
         tot = [x + y for x, y in zip(tot, w)]
     return work_table(*tot)
 
@@ -518,7 +522,7 @@ def run_stream(args, torch):
     torch.cuda.synchronize()
     kernels = run.ctx.omnimem_profile_report()
     run.close()
-    tot = [0, 0, 0, 0]
+    tot = [0, 0, 0, 0, 0]
     elt = 2 if spec["dtype"] == "bf16" else 4
     for n_cache, k_a, kept in shapes:
         for l in range(spec["n_layers"]):
@@ -607,8 +611,8 @@ def main():
     fractions = {
         "mfma_frac_score_gram": stage_frac(["lse_pass", "colsum_pass", "gram_pass", "gram_sym", "gram_wide"],
                                            PEAK_MFMA_TFLOPS[dtype], 1e12),
-        "hbm_frac_topk_compact": stage_frac(["psi_topk", "gather_compact", "gather_inplace", "stage_moved_back"],
-                                            PEAK_HBM_GBS, 1e9),
+        "hbm_frac_topk_compact": stage_frac(["psi_topk", "topk_hist", "topk_bin", "topk_emit", "gather_compact",
+                                             "gather_inplace", "stage_moved_back"], PEAK_HBM_GBS, 1e9),
     }
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,

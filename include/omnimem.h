@@ -321,6 +321,19 @@ omnimem_status omnimem_inplace_status(omnimem_ctx* ctx, int64_t* rows_needed);
 omnimem_status omnimem_append(omnimem_ctx* ctx, const omnimem_layer* layers, const omnimem_chunk* chunks,
                               hipStream_t stream);
 
+/* How omnimem_select_compact ranks (Eq. 8 keys, top-M per modality): a
+ * call whose longest working set has more than `rows` rows splits each
+ * (layer, KV head) over several workgroups (2048-row slices: keys and a
+ * global first-digit histogram, then the threshold bin's keys ranked
+ * exactly; three launches); shorter ones take one workgroup per (layer, KV
+ * head, modality) in one launch.  0: always split; negative: never.  Both
+ * give the same kept rows (top M by psi, ties to the lower row).  Default
+ * 16384: below it the one launch is faster.  Working sets of more than 256
+ * slices (524288 rows) always take the one-workgroup ranking.  The setting
+ * applies to later calls on the context.
+ * Errors: INVALID_ARG (null context). */
+omnimem_status omnimem_set_topk_split(omnimem_ctx* ctx, int64_t rows);
+
 /* Kernel timing for measurement.  While on, every kernel the context
  * launches is bracketed by two HIP events recorded on its launch stream
  * (up to 16384 launches are kept; later ones are not recorded). */

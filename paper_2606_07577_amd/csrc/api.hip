@@ -18,6 +18,7 @@ using namespace omnimem;
 namespace {
 
 constexpr int kSlots = 16;        // descriptor ring depth
+constexpr int64_t kDefaultTopkSplitRows = 16384;  // longest working set still ranked by one workgroup
 constexpr int kProfEvents = 2 * 16384;
 constexpr int kMaxLayers = 1024;  // bound of the allocation kernel's tables
 
@@ -57,7 +58,7 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 static const char* kKernelNames[K_COUNT] = {
     "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact",
     "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish", "layer_inputs",
-    "stage_moved_back", "gather_inplace", "append_chunk", "gram_sym"};
+    "stage_moved_back", "gather_inplace", "append_chunk", "gram_sym", "topk_hist", "topk_bin", "topk_emit"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -73,6 +74,7 @@ struct omnimem_ctx {
   PassPlan lse_plan{0, 0}, cs_plan{0, 0};  // score-pass plans of the last table
   int max_workgroups = 512;               // persistent score-pass grid: 2 per compute unit
   int calib_steps = 0;                    // steps in the calibration sums since the last reset
+  int64_t topk_split_rows = kDefaultTopkSplitRows;  // split top-k when some working set is longer
   std::string err;
   std::vector<void*> allocations;
   Profiler prof;
@@ -515,7 +517,12 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
       (e = dalloc(ctx, &ws.calib, L)) != hipSuccess ||
       (e = dalloc(ctx, &ws.eff, L * 2)) != hipSuccess ||
       (e = dalloc(ctx, &ws.idx, L * Hkv * T)) != hipSuccess ||
-      (e = dalloc(ctx, &ws.keys, L * Hkv * T)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.keys, L * Hkv * (size_t)topk_stride(T))) != hipSuccess ||
+      (e = dalloc(ctx, &ws.tk_hist, L * Hkv * 2 * (size_t)kTopkBins)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.tk_seg, L * Hkv * 2 * 8)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.tk_slice, L * Hkv * (size_t)kTopkMaxSlices * 2)) != hipSuccess ||
+      (e = dalloc(ctx, &ws.tk_cand, L * Hkv * (size_t)topk_stride(T))) != hipSuccess ||
+      (e = dalloc(ctx, &ws.tk_ccount, L * Hkv * 2)) != hipSuccess ||
       (c.shared_selection && (e = dalloc(ctx, &ws.layer_as, 2 * L * T)) != hipSuccess) ||
       (e = dalloc(ctx, &ws.ctl, 4)) != hipSuccess ||
       (c.inplace_stage_rows > 0 &&
@@ -533,7 +540,8 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
     return fail(nullptr, OMNIMEM_ERR_HIP, "pinned descriptor ring: %s", hipGetErrorString(e));
   }
   ctx->pinned = static_cast<LayerDesc*>(pinned);
-  if ((e = hipMemset(ws.ctl, 0, 4 * sizeof(int))) != hipSuccess) {
+  if ((e = hipMemset(ws.ctl, 0, 4 * sizeof(int))) != hipSuccess ||
+      (e = hipMemset(ws.tk_hist, 0, L * Hkv * 2 * (size_t)kTopkBins * sizeof(int))) != hipSuccess) {
     omnimem_destroy(ctx);
     return fail(nullptr, OMNIMEM_ERR_HIP, "control words: %s", hipGetErrorString(e));
   }
@@ -721,8 +729,11 @@ omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* lay
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
+  const bool split = ctx->topk_split_rows >= 0 && max_n > ctx->topk_split_rows &&
+                     (max_n + kTopkSlice - 1) / kTopkSlice <= kTopkMaxSlices;
   return finish(ctx, launch_select_compact(ctx->dm, ctx->cfg.dtype, ctx->cfg.lambda, ctx->cfg.shared_selection ? 1 : 0,
-                                           hidden, inplace, (int)max_n, dev, ctx->ws, a, s, budgets, idx, stream),
+                                           hidden, inplace, (int)max_n, split, dev, ctx->ws, a, s, budgets, idx,
+                                           stream),
                 stream, "omnimem_select_compact launch");
 }
 
@@ -762,6 +773,12 @@ omnimem_status omnimem_append(omnimem_ctx* ctx, const omnimem_layer* layers, con
   if (max_rows == 0) return finish(ctx, hipSuccess, stream, "omnimem_append");
   return finish(ctx, launch_append(ctx->dm, ctx->cfg.dtype, dev, ctx->ws, max_rows, stream), stream,
                 "omnimem_append launch");
+}
+
+omnimem_status omnimem_set_topk_split(omnimem_ctx* ctx, int64_t rows) {
+  if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
+  ctx->topk_split_rows = rows < 0 ? -1 : rows;
+  return OMNIMEM_OK;
 }
 
 omnimem_status omnimem_profile(omnimem_ctx* ctx, int32_t on) {

@@ -220,13 +220,24 @@ constexpr int kNoPartner = (int)0x80000000;  // below ord_f32 of every float
 constexpr int kListPad = 256;
 __host__ __device__ inline int64_t list_stride(int64_t max_tokens) { return max_tokens + kListPad; }
 
+// Top-k split over several workgroups per (layer, KV head): rows are taken
+// in slices of kTopkSlice; the keys and candidate arrays of a (layer, KV
+// head) are max_tokens rounded up to whole slices; at most kTopkMaxSlices
+// slices per working set (larger contexts use the one-workgroup top-k).
+constexpr int kTopkSlice = 2048;
+constexpr int kTopkMaxSlices = 256;
+constexpr int kTopkBins = 4096;   // bins of the first two radix digits
+__host__ __device__ inline int64_t topk_stride(int64_t max_tokens) {
+  return (max_tokens + kTopkSlice - 1) / kTopkSlice * kTopkSlice;
+}
+
 // ---------------------------------------------------------------------------
 // Optional launch timing (see omnimem_profile).
 // ---------------------------------------------------------------------------
 enum KernelId {
   K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
   K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_LAYER_IN,
-  K_STAGE, K_GATHER_IP, K_APPEND, K_GRAM_SYM, K_COUNT
+  K_STAGE, K_GATHER_IP, K_APPEND, K_GRAM_SYM, K_TOPK_HIST, K_TOPK_BIN, K_TOPK_EMIT, K_COUNT
 };
 struct Profiler;
 void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
@@ -258,7 +269,14 @@ struct Workspace {
   double* calib;          // [L] sums of C^(l) over the calibration steps
   int* eff;               // [L][2] budgets as applied by select
   int* idx;               // [L][Hkv][max_tokens] fallback for the idx output
-  uint32_t* keys;         // [L][Hkv][max_tokens]
+  uint32_t* keys;         // [L][Hkv][topk_stride(max_tokens)]
+  // Split top-k (see topk_hist / topk_bin / topk_emit).
+  int* tk_hist;           // [L][Hkv][2][kTopkBins] first-digit histograms; all zero between calls
+  int* tk_seg;            // [L][Hkv][2][8] per modality: mode, bin, need, count, M, first slot, K
+  int* tk_slice;          // [L][Hkv][kTopkMaxSlices][2] per slice: keys above the bin, visual and audio
+  uint2* tk_cand;         // [L][Hkv][topk_stride(max_tokens)] candidates (key, row): visual from the
+                          // front, audio from the back
+  int* tk_ccount;         // [L][Hkv][2] candidates listed so far (cleared by each call's first kernel)
   float* layer_as;        // [2][L][max_tokens] layer-shared selection inputs (null without it)
   // In-place compaction (null / 0 unless the context reserves staging rows).
   int stage_rows;         // staging rows per (layer, KV head)
@@ -293,9 +311,10 @@ hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Wo
                                  const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
                                  float* stats, hipStream_t st);
 hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, int inplace,
-                                 int max_n, const LayerDesc* desc, const Workspace& ws, const float* a,
+                                 int max_n, bool split, const LayerDesc* desc, const Workspace& ws, const float* a,
                                  const float* s, const int32_t* budgets, int32_t* idx,
-                                 hipStream_t st);  // inplace: 0 none, 1 some, 2 all; max_n: largest N
+                                 hipStream_t st);  // inplace: 0 none, 1 some, 2 all; max_n: largest N;
+                                                   // split: the top-k over several workgroups per working set
 hipError_t launch_append(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws, int64_t max_rows,
                          hipStream_t st);
 

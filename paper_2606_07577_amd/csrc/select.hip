@@ -10,6 +10,10 @@
 //                  threshold and the first ones equal to it (ties to the
 //                  lower row), in ascending row order, placed by ballots and
 //                  block-wide scans.
+//  topk_hist, topk_bin, topk_emit
+//                  the same selection split over several workgroups per
+//                  (layer, KV head) for long working sets (described
+//                  where they are defined).
 //  gather_compact  k_out[g][i] = k[g][idx[g][i]] and the same for v, 16 bytes
 //                  per lane, whole rows per lane group.
 #include "common.h"
@@ -386,6 +390,587 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   }
 }
 
+// ---------------------------------------------------------------------------
+// Top-k split over several workgroups per (layer, KV head), for long working
+// sets.  A row's key is psi's order-preserving bits with its modality in bit
+// 31.  The M-th largest key of a modality is located by its first 12-bit
+// digit (key bits 30..19) in a histogram summed over the whole working set,
+// then among the keys in that bin (the "candidates", a small share of the
+// rows unless psi piles up in one narrow range) by the remaining 19 bits.
+//   topk_hist  4096 rows per workgroup: keys to `keys`; first-digit
+//              histograms of both modalities in LDS, added into the (layer,
+//              KV head)'s histograms in global memory.
+//   topk_bin   2048-row slices: every workgroup scans the histograms for the
+//              budgets as applied and each modality's threshold bin, counts
+//              its slice's keys above that bin (every member when all are
+//              kept) and writes the keys in it, in row order, to the slice's
+//              region of `cand` (visual from the front, audio from the back).
+//   topk_emit  per slice: the candidates of all slices, ranked in LDS by the
+//              two remaining digits, give the exact threshold key and how
+//              many keys equal to it are kept (the first ones in row order);
+//              the kept rows in front of the slice are counted and the
+//              slice's kept rows written in ascending order.  It also clears
+//              the histograms, which topk_bin has finished reading.
+// ---------------------------------------------------------------------------
+constexpr int kTkThreads = 1024;
+constexpr int kTkWaves = kTkThreads / 64;
+constexpr int kHistRows = 4096;                       // rows per topk_hist workgroup
+constexpr int kSliceSteps = kTopkSlice / kTkThreads;  // rows per lane of a slice
+constexpr int kCandLds = 4096;                        // candidates of a modality ranked in LDS
+constexpr int kShift1 = 19, kShift2 = 7;              // digits: key bits 30..19, 18..7, 6..0
+constexpr uint32_t kKeyBits = 0x7FFFFFFFu;
+static_assert(kTopkBins % (4 * kTkThreads) == 0 && kTopkSlice % kTkThreads == 0, "whole bins and rows per lane");
+static_assert(kTopkMaxSlices <= kTkThreads && (2 << kShift2) <= kTkThreads, "one slice and one bin per thread");
+
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+__device__ inline uint2 gload8(const void* p) {
+  const u32x2 v = gload<u32x2>(p);
+  return make_uint2(v[0], v[1]);
+}
+
+// Inclusive scans over the 256 threads in thread order (one barrier); wsum
+// holds kTkWaves ints per value and must not be reused before a later
+// barrier.  tot: the sums.
+template <int NV>
+__device__ inline void block_inclusive(int (&v)[NV], int (*wsum)[kTkWaves], int (&tot)[NV]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    v[i] = wave_inclusive(v[i]);
+    if (lane == 63) wsum[i][wave] = v[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    int base = 0, t = 0;
+#pragma unroll
+    for (int w = 0; w < kTkWaves; ++w) {
+      const int c = wsum[i][w];
+      base += w < wave ? c : 0;
+      t += c;
+    }
+    v[i] += base;
+    tot[i] = t;
+  }
+}
+
+// Of PER bins h[0..PER) taken from the highest down, with `above` keys in
+// the bins before them and above < need <= above + sum(h): the bin i that
+// holds the need-th largest key, how many of its keys are needed and its
+// count.  Branch-free: a selection per bin.
+template <int PER>
+__device__ inline void crossing_bin(const int (&h)[PER], int above, int need, int& bin, int& need_in, int& cnt) {
+  bin = 0;
+  need_in = 0;
+  cnt = 0;
+  bool found = false;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const bool hit = !found && need <= above + h[i];
+    bin = hit ? i : bin;
+    need_in = hit ? need - above : need_in;
+    cnt = hit ? h[i] : cnt;
+    found = found || hit;
+    above += h[i];
+  }
+}
+
+template <bool SHARED>
+__global__ __launch_bounds__(kTkThreads) void topk_hist(const LayerDesc* __restrict__ layers, Dims dm, float lambda,
+                                                         const float* __restrict__ a, const float* __restrict__ s,
+                                                         uint32_t* __restrict__ keys, int* __restrict__ hist,
+                                                         int* __restrict__ ccount, int* __restrict__ ctl) {
+  __shared__ int h[2 * kTopkBins];
+  const int l = blockIdx.z, g = blockIdx.y, r0 = blockIdx.x * kHistRows;
+  const int64_t unit = (int64_t)l * dm.Hkv + g;
+  const int64_t in_off = SHARED ? (int64_t)l * dm.max_tokens : unit * dm.max_tokens;
+  const float* ag = a + in_off;
+  const float* sg = s + in_off;
+  constexpr int R = kHistRows / kTkThreads;
+  // a and s are requested before the layer's descriptor arrives (indices
+  // kept inside the buffers' rows; rows past N are not used)
+  float av[R], sv[R];
+#pragma unroll
+  for (int u = 0; u < R; ++u) {
+    const int j = min(r0 + u * kTkThreads + (int)threadIdx.x, (int)dm.max_tokens - 1);
+    av[u] = gload<float>(ag + j);
+    sv[u] = gload<float>(sg + j);
+  }
+  if (ctl != nullptr && blockIdx.x == 0 && g == 0 && l == 0 && threadIdx.x == 0)
+    ctl[1] = 0;  // staging rows needed beyond the reserve, this call
+  if (blockIdx.x == 0 && threadIdx.x < 2) ccount[unit * 2 + threadIdx.x] = 0;  // topk_bin lists after this kernel
+  const int N = layers[l].n;
+  if (r0 >= N) return;
+  const uint8_t* mod = layers[l].mod;
+  uint32_t* kg = keys + unit * topk_stride(dm.max_tokens);
+  int* gh = hist + unit * 2 * kTopkBins;
+  int mv[R];
+#pragma unroll
+  for (int u = 0; u < R; ++u) mv[u] = gload<uint8_t>(mod + min(r0 + u * kTkThreads + (int)threadIdx.x, N - 1));
+  int4* h4 = reinterpret_cast<int4*>(h);
+  for (int i = threadIdx.x; i < 2 * kTopkBins / 4; i += kTkThreads) h4[i] = make_int4(0, 0, 0, 0);
+  __syncthreads();  // histograms cleared
+#pragma unroll
+  for (int u = 0; u < R; ++u) {
+    const int j = r0 + u * kTkThreads + (int)threadIdx.x;
+    if (j < N) {
+      const uint32_t key = psi_key(av[u], sv[u], lambda);
+      const uint32_t mu = mv[u] ? 1u : 0u;
+      kg[j] = key | (mu << 31);
+      atomicAdd(&h[mu * kTopkBins + (key >> kShift1)], 1);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 2 * kTopkBins / 4; i += kTkThreads) {
+    const int4 c = h4[i];
+    if (c.x) atomicAdd(gh + 4 * i, c.x);
+    if (c.y) atomicAdd(gh + 4 * i + 1, c.y);
+    if (c.z) atomicAdd(gh + 4 * i + 2, c.z);
+    if (c.w) atomicAdd(gh + 4 * i + 3, c.w);
+  }
+}
+
+// Segment record (tk_seg), per (layer, KV head, modality).
+enum { SEG_MODE, SEG_BIN, SEG_NEED, SEG_CNT, SEG_M, SEG_OUT0, SEG_K };
+enum { MODE_NONE = 0, MODE_ALL = 1, MODE_PICK = 2 };
+
+template <bool SHARED>
+__global__ __launch_bounds__(kTkThreads) void topk_bin(const LayerDesc* __restrict__ layers, Dims dm,
+                                                        const uint32_t* __restrict__ keys, const int* __restrict__ hist,
+                                                        const int32_t* __restrict__ budgets, int* __restrict__ seg,
+                                                        int* __restrict__ slice, uint2* __restrict__ cand,
+                                                        int* __restrict__ ccount, int* __restrict__ eff) {
+  __shared__ int wsum[2][kTkWaves];
+  __shared__ int s_bin[2], s_need[2], s_cnt[2], s_base[2];
+  __shared__ int wc[2][kSliceSteps][kTkWaves];  // candidates per (modality, step, wave)
+  __shared__ int wa[2][kTkWaves];               // keys above the bin per (modality, wave)
+  const int l = blockIdx.z, g = blockIdx.y, p = blockIdx.x;
+  const int r0 = p * kTopkSlice;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  const int64_t unit = (int64_t)l * dm.Hkv + g;
+  const int64_t stride = topk_stride(dm.max_tokens);
+  const uint32_t* kg = keys + unit * stride;
+  // Reads that need no descriptor first: the histograms (bins highest first:
+  // thread t holds bins btop - i, i < PER, of each modality) and the slice's
+  // keys (whole slices lie inside the key buffer; rows past N are not used).
+  constexpr int PER = kTopkBins / kTkThreads;
+  const int btop = kTopkBins - 1 - PER * (int)threadIdx.x;
+  int hb[2][PER];
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu) {
+#pragma unroll
+    for (int q = 0; q < PER / 4; ++q) {
+      const uint4 v = gload16(hist + unit * 2 * kTopkBins + mu * kTopkBins + btop - (PER - 1) + 4 * q);
+      hb[mu][PER - 1 - 4 * q] = (int)v.x;
+      hb[mu][PER - 2 - 4 * q] = (int)v.y;
+      hb[mu][PER - 3 - 4 * q] = (int)v.z;
+      hb[mu][PER - 4 - 4 * q] = (int)v.w;
+    }
+  }
+  uint32_t kk[kSliceSteps];
+#pragma unroll
+  for (int u = 0; u < kSliceSteps; ++u) kk[u] = gload<uint32_t>(kg + r0 + u * kTkThreads + (int)threadIdx.x);
+  const int bud_v = budgets[2 * l], bud_a = budgets[2 * l + 1];
+  const int N = layers[l].n;
+  if (r0 >= N && p > 0) return;  // slice 0 always writes the segment records
+  const int cap = layers[l].out_cap;
+  int mine[2] = {0, 0};
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    mine[0] += hb[0][i];
+    mine[1] += hb[1][i];
+  }
+  int incl[2] = {mine[0], mine[1]}, K[2];
+  block_inclusive<2>(incl, wsum, K);
+  // budgets as applied: each modality's within its rows, visual first within the output capacity
+  int M[2];
+  M[0] = min(min(max(bud_v, 0), K[0]), cap);
+  M[1] = min(min(max(bud_a, 0), K[1]), cap - M[0]);
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu) {
+    const int above = incl[mu] - mine[mu];
+    const int m = M[mu];
+    int i, need_in, cnt;
+    crossing_bin<PER>(hb[mu], above, m, i, need_in, cnt);
+    if (0 < m && m < K[mu] && above < m && m <= above + mine[mu]) { s_bin[mu] = btop - i; s_need[mu] = need_in; s_cnt[mu] = cnt; }
+  }
+  __syncthreads();
+  // (the same in every lane: kept in scalar registers, so that the flags
+  // below are plain lane arithmetic)
+  int mode[2], b1[2];
+  bool whole[2];  // the threshold's whole first-digit bin is kept: no candidates
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu) {
+    M[mu] = uniform(M[mu]);
+    K[mu] = uniform(K[mu]);
+    mode[mu] = M[mu] == 0 ? MODE_NONE : M[mu] >= K[mu] ? MODE_ALL : MODE_PICK;
+    b1[mu] = mode[mu] == MODE_PICK ? uniform(s_bin[mu]) : 0;
+    whole[mu] = mode[mu] == MODE_PICK && uniform(s_need[mu]) >= uniform(s_cnt[mu]);
+  }
+  if (p == 0 && threadIdx.x < 2) {
+    const int mu = threadIdx.x;
+    int* sr = seg + (unit * 2 + mu) * 8;
+    sr[SEG_MODE] = mode[mu];
+    sr[SEG_BIN] = b1[mu];
+    sr[SEG_NEED] = mode[mu] == MODE_PICK ? s_need[mu] : 0;
+    sr[SEG_CNT] = mode[mu] == MODE_PICK ? s_cnt[mu] : 0;
+    sr[SEG_M] = M[mu];
+    sr[SEG_OUT0] = mu ? M[0] : 0;
+    sr[SEG_K] = K[mu];
+    if (g == 0) eff[2 * l + mu] = M[mu];
+  }
+  if (r0 >= N) return;
+  int na[2] = {0, 0};
+  unsigned long long cb[2][kSliceSteps];
+#pragma unroll
+  for (int u = 0; u < kSliceSteps; ++u) {
+    const bool valid = r0 + u * kTkThreads + (int)threadIdx.x < N;
+    const int mu_u = (int)(kk[u] >> 31);
+    const int d1 = (int)((kk[u] & kKeyBits) >> kShift1);
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      const bool m = valid & (mu_u == mu);
+      const bool all = mode[mu] == MODE_ALL, pick = mode[mu] == MODE_PICK;
+      const bool above_f = m & (all | (pick & ((d1 > b1[mu]) | (whole[mu] & (d1 == b1[mu])))));
+      const bool cand_f = m & pick & !whole[mu] & (d1 == b1[mu]);
+      na[mu] += __popcll(__ballot(above_f));
+      cb[mu][u] = __ballot(cand_f);
+      if (lane == 0) wc[mu][u][wave] = __popcll(cb[mu][u]);
+    }
+  }
+  if (lane == 0) { wa[0][wave] = na[0]; wa[1][wave] = na[1]; }
+  __syncthreads();
+  // The slice's count above the bin, and room for its candidates in the
+  // (layer, KV head)'s list (one atomic per modality).
+  if (threadIdx.x < 2) {
+    const int mu = threadIdx.x;
+    int above = 0, n = 0;
+#pragma unroll
+    for (int w = 0; w < kTkWaves; ++w) {
+      above += wa[mu][w];
+#pragma unroll
+      for (int u = 0; u < kSliceSteps; ++u) n += wc[mu][u][w];
+    }
+    slice[(unit * kTopkMaxSlices + p) * 2 + mu] = above;
+    s_base[mu] = n ? atomicAdd(ccount + unit * 2 + mu, n) : 0;
+  }
+  __syncthreads();
+  uint2* cl = cand + unit * stride;
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu) {
+    int run = s_base[mu];
+#pragma unroll
+    for (int u = 0; u < kSliceSteps; ++u) {
+      int before = run, all = 0;
+#pragma unroll
+      for (int w = 0; w < kTkWaves; ++w) {
+        const int c = wc[mu][u][w];
+        before += w < wave ? c : 0;
+        all += c;
+      }
+      if ((cb[mu][u] >> lane) & 1ull) {
+        const int r = before + __popcll(cb[mu][u] & lt);
+        cl[mu ? stride - 1 - r : r] = make_uint2(kk[u] & kKeyBits, (uint32_t)(r0 + u * kTkThreads + (int)threadIdx.x));
+      }
+      run += all;
+    }
+  }
+}
+
+template <bool SHARED>
+__global__ __launch_bounds__(kTkThreads) void topk_emit(const LayerDesc* __restrict__ layers, Dims dm,
+                                                         const uint32_t* __restrict__ keys, int* __restrict__ hist,
+                                                         const int* __restrict__ seg, const int* __restrict__ slice,
+                                                         const uint2* __restrict__ cand, int32_t* __restrict__ idx,
+                                                         int* __restrict__ slot_of) {
+  __shared__ uint32_t ck[2][kCandLds];            // candidate keys of each modality; bit 31: row in front of the slice
+  __shared__ int hb[2][kTopkBins];                // digit histograms
+  __shared__ int apre[2][kTopkMaxSlices + 1];     // keys above the first-digit bin in front of slice i
+  __shared__ int wsum0[2][kTkWaves], wsum1[2][kTkWaves], wsum2[2][kTkWaves], wsum3[4][kTkWaves];
+  __shared__ int s_bin[2], s_need[2], s_cnt[2];
+  __shared__ int wc[2][kSliceSteps][kTkWaves];
+  const int l = blockIdx.z, g = blockIdx.y, p = blockIdx.x;
+  const int r0 = p * kTopkSlice;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  const int64_t unit = (int64_t)l * dm.Hkv + g;
+  const int64_t stride = topk_stride(dm.max_tokens);
+  const uint32_t* kg = keys + unit * stride;
+  const uint2* cl = cand + unit * stride;
+
+  // Reads that need no descriptor first: the slice's keys, the slice table
+  // (thread t: slice t) and the segment records.
+  uint32_t kk[kSliceSteps];
+#pragma unroll
+  for (int u = 0; u < kSliceSteps; ++u) kk[u] = gload<uint32_t>(kg + r0 + u * kTkThreads + (int)threadIdx.x);
+  uint2 st = make_uint2(0, 0);
+  if (threadIdx.x < gridDim.x) st = gload8(slice + (unit * kTopkMaxSlices + threadIdx.x) * 2);
+  int sr[2][7];
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu)
+#pragma unroll
+    for (int f = 0; f < 7; ++f) sr[mu][f] = uniform(seg[(unit * 2 + mu) * 8 + f]);
+  const LayerDesc& Ld = layers[l];
+  const int N = Ld.n;
+  if (r0 >= N) return;
+  const int P = (N + kTopkSlice - 1) / kTopkSlice;
+  if ((int)threadIdx.x >= P) st = make_uint2(0, 0);
+  // This slice's share of the histograms back to zero for the next call.
+  {
+    constexpr int V4 = 2 * kTopkBins / 4;
+    const int per = (V4 + P - 1) / P;
+    int4* h4 = reinterpret_cast<int4*>(hist + unit * 2 * kTopkBins);
+    for (int i = p * per + (int)threadIdx.x; i < min(V4, (p + 1) * per); i += kTkThreads) h4[i] = make_int4(0, 0, 0, 0);
+  }
+  // Keys above the first-digit bin in front of each slice.
+  {
+    int v[2] = {(int)st.x, (int)st.y}, tot[2];
+    block_inclusive<2>(v, wsum0, tot);
+    if ((int)threadIdx.x < P) {
+      apre[0][threadIdx.x + 1] = v[0];
+      apre[1][threadIdx.x + 1] = v[1];
+    }
+    if (threadIdx.x == 0) { apre[0][0] = 0; apre[1][0] = 0; }
+    __syncthreads();
+  }
+
+  // Exact threshold of each modality that ranks: keep the keys above thr
+  // and the first `take` keys equal to it.  Both modalities go through each
+  // phase together.
+  uint32_t thr[2] = {0u, 0u}, b1[2];
+  int take[2] = {0, 0}, n_eq[2] = {0, 0}, gtb[2], eqb[2] = {0, 0}, need1[2], C[2];
+  bool rank[2], whole[2], in_lds[2];
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu) {
+    b1[mu] = (uint32_t)sr[mu][SEG_BIN];
+    need1[mu] = sr[mu][SEG_NEED];
+    C[mu] = sr[mu][SEG_CNT];  // the keys in the first-digit bin: the listed candidates
+    gtb[mu] = apre[mu][p];
+    rank[mu] = sr[mu][SEG_MODE] == MODE_PICK && need1[mu] < C[mu];
+    whole[mu] = sr[mu][SEG_MODE] == MODE_PICK && !rank[mu];  // the whole first-digit bin is kept
+    in_lds[mu] = C[mu] <= kCandLds;
+    if (whole[mu]) thr[mu] = (b1[mu] << kShift1) - 1u;  // counted above the bin by topk_bin
+  }
+  if (rank[0] || rank[1]) {
+    // candidate i of modality mu as its key with bit 31 set when its row is
+    // in front of this slice
+    auto cand_at = [&](int mu, int i) {
+      const uint2 c = gload8(cl + (mu ? stride - 1 - i : i));
+      return c.x | (c.y < (uint32_t)r0 ? 0x80000000u : 0u);
+    };
+    // visit(key) over candidates [0, n) of modality mu, eight per lane in flight
+    auto for_cands = [&](int mu, int n, auto&& visit) {
+      for (int i0 = 0; i0 < n; i0 += 8 * kTkThreads) {
+        uint32_t v[8];
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const int i = i0 + b * kTkThreads + (int)threadIdx.x;
+          v[b] = i < n ? (in_lds[mu] ? ck[mu][i] : cand_at(mu, i)) : 0u;
+        }
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+          if (i0 + b * kTkThreads + (int)threadIdx.x < n) visit(v[b]);
+      }
+    };
+    {
+      int4* h4 = reinterpret_cast<int4*>(&hb[0][0]);
+      for (int i = threadIdx.x; i < 2 * kTopkBins / 4; i += kTkThreads) h4[i] = make_int4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      if (!rank[mu] || !in_lds[mu]) continue;
+      for (int i0 = 0; i0 < C[mu]; i0 += 8 * kTkThreads) {
+        uint32_t v[8];
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const int i = i0 + b * kTkThreads + (int)threadIdx.x;
+          v[b] = i < C[mu] ? cand_at(mu, i) : 0u;
+        }
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+          const int i = i0 + b * kTkThreads + (int)threadIdx.x;
+          if (i < C[mu]) ck[mu][i] = v[b];
+        }
+      }
+    }
+    __syncthreads();  // histograms cleared, candidates in LDS
+    // second digit (key bits 18..7)
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu)
+      if (rank[mu]) for_cands(mu, C[mu], [&](uint32_t key) { atomicAdd(&hb[mu][(key >> kShift2) & (kTopkBins - 1)], 1); });
+    __syncthreads();
+    {
+      constexpr int PER = kTopkBins / kTkThreads;
+      const int btop = kTopkBins - 1 - PER * (int)threadIdx.x;
+      int h[2][PER], mine[2] = {0, 0};
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu)
+#pragma unroll
+        for (int i = 0; i < PER; ++i) { h[mu][i] = hb[mu][btop - i]; mine[mu] += h[mu][i]; }
+      int v[2] = {mine[0], mine[1]}, tot[2];
+      block_inclusive<2>(v, wsum1, tot);
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) {
+        const int above = v[mu] - mine[mu];
+        const int need = need1[mu];
+        int i, need_in, cnt;
+        crossing_bin<PER>(h[mu], above, need, i, need_in, cnt);
+        if (rank[mu] && above < need && need <= above + mine[mu]) { s_bin[mu] = btop - i; s_need[mu] = need_in; s_cnt[mu] = cnt; }
+      }
+      __syncthreads();
+    }
+    uint32_t pre2[2];
+    int need2[2];
+    bool third[2];
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      pre2[mu] = (b1[mu] << (kShift1 - kShift2)) | (uint32_t)uniform(s_bin[mu]);  // key bits 30..7
+      need2[mu] = uniform(s_need[mu]);
+      third[mu] = rank[mu] && need2[mu] < uniform(s_cnt[mu]);
+      if (rank[mu] && !third[mu]) thr[mu] = (pre2[mu] << kShift2) - 1u;  // the whole second-digit bin is kept
+    }
+    if (third[0] || third[1]) {
+      __syncthreads();  // every thread has read the histograms and s_bin, s_need, s_cnt
+      if (threadIdx.x < 2u << kShift2) hb[threadIdx.x >> kShift2][threadIdx.x & ((1u << kShift2) - 1u)] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu)
+        if (third[mu])
+          for_cands(mu, C[mu], [&](uint32_t key) {
+            if (((key & kKeyBits) >> kShift2) == pre2[mu]) atomicAdd(&hb[mu][key & ((1u << kShift2) - 1u)], 1);
+          });
+      __syncthreads();
+      const int t = (int)threadIdx.x;
+      const int bin = (1 << kShift2) - 1 - t;
+      int c[2], v[2], tot[2];
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) c[mu] = v[mu] = t < (1 << kShift2) ? hb[mu][bin] : 0;
+      block_inclusive<2>(v, wsum2, tot);
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) {
+        const int above = v[mu] - c[mu];
+        if (third[mu] && c[mu] > 0 && above < need2[mu] && need2[mu] <= above + c[mu]) {
+          s_bin[mu] = bin; s_need[mu] = need2[mu] - above; s_cnt[mu] = c[mu];
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) {
+        if (!third[mu]) continue;
+        thr[mu] = (pre2[mu] << kShift2) | (uint32_t)uniform(s_bin[mu]);
+        take[mu] = uniform(s_need[mu]);
+        n_eq[mu] = uniform(s_cnt[mu]);
+      }
+    }
+    // kept candidates of the slices in front: above thr, or equal to it
+    int v[4] = {0, 0, 0, 0}, tot[4];
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      if (!rank[mu]) continue;
+      const uint32_t th = thr[mu];
+      int gt = 0, eq = 0;
+      for_cands(mu, C[mu], [&](uint32_t key) {
+        const bool front = (key >> 31) != 0;
+        key &= kKeyBits;
+        gt += front && key > th ? 1 : 0;
+        eq += front && key == th ? 1 : 0;
+      });
+      v[2 * mu] = gt;
+      v[2 * mu + 1] = eq;
+    }
+    block_inclusive<4>(v, wsum3, tot);
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      if (!rank[mu]) continue;
+      gtb[mu] += tot[2 * mu];
+      eqb[mu] = tot[2 * mu + 1];
+    }
+  }
+
+  // Emission: the slice's kept rows in ascending order.
+  const bool need_rank[2] = {rank[0] && take[0] > 0 && take[0] < n_eq[0], rank[1] && take[1] > 0 && take[1] < n_eq[1]};
+  bool keep_eq[kSliceSteps];
+#pragma unroll
+  for (int u = 0; u < kSliceSteps; ++u) keep_eq[u] = true;
+  if (need_rank[0] || need_rank[1]) {  // ranks among the keys equal to a threshold
+    unsigned long long eb[2][kSliceSteps];
+#pragma unroll
+    for (int u = 0; u < kSliceSteps; ++u) {
+      const bool valid = r0 + u * kTkThreads + (int)threadIdx.x < N;
+      const int mu_u = (int)(kk[u] >> 31);
+      const uint32_t k = kk[u] & kKeyBits;
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) {
+        eb[mu][u] = __ballot(valid & (mu_u == mu) & need_rank[mu] & (k == thr[mu]));
+        if (lane == 0) wc[mu][u][wave] = __popcll(eb[mu][u]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      int run = 0;
+#pragma unroll
+      for (int u = 0; u < kSliceSteps; ++u) {
+        int before = run, all = 0;
+#pragma unroll
+        for (int w = 0; w < kTkWaves; ++w) {
+          const int c = wc[mu][u][w];
+          before += w < wave ? c : 0;
+          all += c;
+        }
+        if ((eb[mu][u] >> lane) & 1ull) keep_eq[u] = eqb[mu] + before + __popcll(eb[mu][u] & lt) < take[mu];
+        run += all;
+      }
+    }
+    __syncthreads();  // before wc is reused
+  }
+  unsigned long long sb[2][kSliceSteps];
+#pragma unroll
+  for (int u = 0; u < kSliceSteps; ++u) {
+    const bool valid = r0 + u * kTkThreads + (int)threadIdx.x < N;
+    const int mu_u = (int)(kk[u] >> 31);
+    const uint32_t k = kk[u] & kKeyBits;
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      const bool all = sr[mu][SEG_MODE] == MODE_ALL, pick = sr[mu][SEG_MODE] == MODE_PICK;
+      const bool sel = valid & (mu_u == mu) & (all | (pick & ((k > thr[mu]) | ((k == thr[mu]) & (take[mu] > 0) & keep_eq[u]))));
+      sb[mu][u] = __ballot(sel);
+      if (lane == 0) wc[mu][u][wave] = __popcll(sb[mu][u]);
+    }
+  }
+  __syncthreads();
+  const bool want_slots = Ld.inplace != 0 && slot_of != nullptr;
+  const int heads = SHARED ? dm.Hkv : 1;
+  int32_t* ig = idx + unit * dm.max_tokens;
+  int* so = want_slots ? slot_of + unit * dm.max_tokens : nullptr;
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu) {
+    int run = sr[mu][SEG_OUT0] + gtb[mu] + min(eqb[mu], take[mu]);
+#pragma unroll
+    for (int u = 0; u < kSliceSteps; ++u) {
+      int before = run, all = 0;
+#pragma unroll
+      for (int w = 0; w < kTkWaves; ++w) {
+        const int c = wc[mu][u][w];
+        before += w < wave ? c : 0;
+        all += c;
+      }
+      const int row = r0 + u * kTkThreads + (int)threadIdx.x;
+      if ((sb[mu][u] >> lane) & 1ull) {
+        const int slot = before + __popcll(sb[mu][u] & lt);
+        for (int h = 0; h < heads; ++h) {
+          ig[(int64_t)h * dm.max_tokens + slot] = row;
+          if (so) so[(int64_t)h * dm.max_tokens + row] = slot;
+        }
+      } else if (so && row < N && (int)(kk[u] >> 31) == mu) {
+        for (int h = 0; h < heads; ++h) so[(int64_t)h * dm.max_tokens + row] = -1;
+      }
+      run += all;
+    }
+  }
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void gather_compact(const LayerDesc* __restrict__ layers, Dims dm,
                                                       const int32_t* __restrict__ idx, const int* __restrict__ eff,
@@ -697,10 +1282,36 @@ void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, c
   }
 }
 
+template <bool SHARED>
+void launch_topk(const Dims& dm, float lambda, int max_n, bool split, const LayerDesc* desc, const Workspace& ws,
+                 const float* a, const float* s, const int32_t* budgets, int32_t* ix, int* slot_of, int* ctl,
+                 hipStream_t st) {
+  const unsigned heads = SHARED ? 1u : (unsigned)dm.Hkv;
+  if (!split) {
+    OMNIMEM_LAUNCH(ws, K_TOPK, st,
+                   psi_topk<SHARED><<<dim3(2, heads, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets,
+                                                                                  ws.keys, ix, ws.eff, slot_of, ctl));
+    return;
+  }
+  const unsigned hx = (unsigned)((max_n + kHistRows - 1) / kHistRows);
+  const unsigned sx = (unsigned)((max_n + kTopkSlice - 1) / kTopkSlice);
+  OMNIMEM_LAUNCH(ws, K_TOPK_HIST, st,
+                 topk_hist<SHARED><<<dim3(hx, heads, dm.L), kTkThreads, 0, st>>>(desc, dm, lambda, a, s, ws.keys,
+                                                                                ws.tk_hist, ws.tk_ccount, ctl));
+  OMNIMEM_LAUNCH(ws, K_TOPK_BIN, st,
+                 topk_bin<SHARED><<<dim3(sx, heads, dm.L), kTkThreads, 0, st>>>(desc, dm, ws.keys, ws.tk_hist, budgets,
+                                                                               ws.tk_seg, ws.tk_slice, ws.tk_cand,
+                                                                               ws.tk_ccount, ws.eff));
+  OMNIMEM_LAUNCH(ws, K_TOPK_EMIT, st,
+                 topk_emit<SHARED><<<dim3(sx, heads, dm.L), kTkThreads, 0, st>>>(desc, dm, ws.keys, ws.tk_hist,
+                                                                                ws.tk_seg, ws.tk_slice, ws.tk_cand,
+                                                                                ix, slot_of));
+}
+
 }  // namespace
 
 hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, int inplace,
-                                 int max_n, const LayerDesc* desc, const Workspace& ws, const float* a,
+                                 int max_n, bool split, const LayerDesc* desc, const Workspace& ws, const float* a,
                                  const float* s, const int32_t* budgets, int32_t* idx, hipStream_t st) {
   int32_t* ix = idx ? idx : ws.idx;
   int* slot_of = inplace ? ws.slot_of : nullptr;
@@ -710,13 +1321,10 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int sh
     float* ls = ws.layer_as + (size_t)dm.L * dm.max_tokens;
     const dim3 gtok((unsigned)((dm.max_tokens + 255) / 256), dm.L);
     OMNIMEM_LAUNCH(ws, K_LAYER_IN, st, layer_inputs<<<gtok, 256, 0, st>>>(desc, dm, a, s, la, ls));
-    OMNIMEM_LAUNCH(ws, K_TOPK, st,
-                   psi_topk<true><<<dim3(2, 1, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, la, ls, budgets, ws.keys,
-                                                                            ix, ws.eff, slot_of, ctl));
-  } else
-    OMNIMEM_LAUNCH(ws, K_TOPK, st,
-                   psi_topk<false><<<dim3(2, dm.Hkv, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets,
-                                                                                  ws.keys, ix, ws.eff, slot_of, ctl));
+    launch_topk<true>(dm, lambda, max_n, split, desc, ws, la, ls, budgets, ix, slot_of, ctl, st);
+  } else {
+    launch_topk<false>(dm, lambda, max_n, split, desc, ws, a, s, budgets, ix, slot_of, ctl, st);
+  }
   if (dtype == 0) {
     if (dm.d == 128) launch_gather<uint16_t, 128>(dm, desc, ws, ix, inplace, max_n, st);
     else launch_gather<uint16_t, 64>(dm, desc, ws, ix, inplace, max_n, st);

@@ -26,7 +26,7 @@ EXPORTED = [
     "omnimem_score", "omnimem_redundancy", "omnimem_allocate", "omnimem_select_compact",
     "omnimem_calibrate", "omnimem_calibration_reset", "omnimem_calibration_budgets",
     "omnimem_allocate_fixed", "omnimem_profile", "omnimem_profile_report", "omnimem_inplace_status",
-    "omnimem_append", "omnimem_allocate_noalloc",
+    "omnimem_append", "omnimem_allocate_noalloc", "omnimem_set_topk_split",
 ]
 
 
@@ -113,6 +113,8 @@ def load_library(path=LIB_PATH):
     lib.omnimem_inplace_status.restype = i32
     lib.omnimem_append.argtypes = [vp, ctypes.POINTER(Layer), ctypes.POINTER(Chunk), vp]
     lib.omnimem_append.restype = i32
+    lib.omnimem_set_topk_split.argtypes = [vp, i64]
+    lib.omnimem_set_topk_split.restype = i32
     lib.omnimem_profile.argtypes = [vp, ctypes.c_int32]
     lib.omnimem_profile.restype = i32
     lib.omnimem_profile_report.argtypes = [vp, ctypes.POINTER(KernelTime), ctypes.c_int32,
@@ -273,6 +275,12 @@ class Context:
             raise ValueError(f"expected {self.cfg.n_layers} chunk descriptors")
         arr = chunks if isinstance(chunks, ctypes.Array) else (Chunk * len(chunks))(*chunks)
         self._check(self._lib.omnimem_append(self.handle, self._layers(layers), arr, _stream(stream)))
+
+    def omnimem_set_topk_split(self, rows):
+        """Split the top-k over several workgroups per (layer, KV head) when
+        the longest working set has more than `rows` rows (0: always, -1:
+        never)."""
+        self._check(self._lib.omnimem_set_topk_split(self.handle, int(rows)))
 
     def omnimem_profile(self, on):
         self._check(self._lib.omnimem_profile(self.handle, int(bool(on))))
