@@ -321,18 +321,29 @@ omnimem_status omnimem_inplace_status(omnimem_ctx* ctx, int64_t* rows_needed);
 omnimem_status omnimem_append(omnimem_ctx* ctx, const omnimem_layer* layers, const omnimem_chunk* chunks,
                               hipStream_t stream);
 
-/* How omnimem_select_compact ranks (Eq. 8 keys, top-M per modality): a
- * call whose longest working set has more than `rows` rows splits each
- * (layer, KV head) over several workgroups (2048-row slices: keys and a
- * global first-digit histogram, then the threshold bin's keys ranked
- * exactly; three launches); shorter ones take one workgroup per (layer, KV
- * head, modality) in one launch.  0: always split; negative: never.  Both
- * give the same kept rows (top M by psi, ties to the lower row).  Default
- * 16384: below it the one launch is faster.  Working sets of more than 256
- * slices (524288 rows) always take the one-workgroup ranking.  The setting
- * applies to later calls on the context.
- * Errors: INVALID_ARG (null context). */
-omnimem_status omnimem_set_topk_split(omnimem_ctx* ctx, int64_t rows);
+/* How omnimem_select_compact ranks the rows (Eq. 8 keys, top M per
+ * modality).  Every path keeps the same rows (the top M by psi, ties to the
+ * lower row); they differ in speed only.
+ *   REGISTERS     one workgroup per (layer, KV head, modality) holding every
+ *                 key in registers; working sets of at most 8192 rows.
+ *   ONE_WORKGROUP one workgroup per (layer, KV head, modality), keys in LDS
+ *                 (in global memory past 32768 rows of a modality).
+ *   SPLIT         several workgroups per (layer, KV head) in 2048-row
+ *                 slices, three launches: keys and a global first-digit
+ *                 histogram, the threshold bin's keys listed, then ranked
+ *                 exactly and the rows emitted; at most 524288 rows.
+ *   AUTO          REGISTERS up to 8192 rows, ONE_WORKGROUP up to 16384,
+ *                 SPLIT beyond (by the call's longest working set).
+ * A call whose sizes a chosen path cannot take uses ONE_WORKGROUP.  The
+ * setting applies to later calls on the context.
+ * Errors: INVALID_ARG (null context, unknown path). */
+typedef enum {
+  OMNIMEM_TOPK_AUTO = 0,
+  OMNIMEM_TOPK_REGISTERS = 1,
+  OMNIMEM_TOPK_ONE_WORKGROUP = 2,
+  OMNIMEM_TOPK_SPLIT = 3
+} omnimem_topk_path;
+omnimem_status omnimem_set_topk_path(omnimem_ctx* ctx, int32_t path);
 
 /* Kernel timing for measurement.  While on, every kernel the context
  * launches is bracketed by two HIP events recorded on its launch stream

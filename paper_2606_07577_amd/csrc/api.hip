@@ -18,7 +18,7 @@ using namespace omnimem;
 namespace {
 
 constexpr int kSlots = 16;        // descriptor ring depth
-constexpr int64_t kDefaultTopkSplitRows = 16384;  // longest working set still ranked by one workgroup
+constexpr int64_t kTopkAutoSplitRows = 16384;  // longest working set AUTO ranks in one workgroup
 constexpr int kProfEvents = 2 * 16384;
 constexpr int kMaxLayers = 1024;  // bound of the allocation kernel's tables
 
@@ -58,7 +58,7 @@ void prof_mark(Profiler* p, int kid, hipStream_t st, bool begin) {
 static const char* kKernelNames[K_COUNT] = {
     "lse_pass", "lse_merge", "colsum_pass", "head_sum", "modality_lists", "lists_norms", "gram_pass", "gram_finish", "adjacent_cos", "avba_partials", "avba_allocate", "psi_topk", "gather_compact",
     "gather_hidden", "adjacent_cos_hidden", "hidden_norms", "gram_wide", "hidden_finish", "layer_inputs",
-    "stage_moved_back", "gather_inplace", "append_chunk", "gram_sym", "topk_hist", "topk_bin", "topk_emit"};
+    "stage_moved_back", "gather_inplace", "append_chunk", "gram_sym", "topk_hist", "topk_bin", "topk_emit", "psi_topk_reg"};
 
 struct omnimem_ctx {
   omnimem_config cfg;
@@ -74,7 +74,7 @@ struct omnimem_ctx {
   PassPlan lse_plan{0, 0}, cs_plan{0, 0};  // score-pass plans of the last table
   int max_workgroups = 512;               // persistent score-pass grid: 2 per compute unit
   int calib_steps = 0;                    // steps in the calibration sums since the last reset
-  int64_t topk_split_rows = kDefaultTopkSplitRows;  // split top-k when some working set is longer
+  int topk_path = OMNIMEM_TOPK_AUTO;
   std::string err;
   std::vector<void*> allocations;
   Profiler prof;
@@ -729,10 +729,17 @@ omnimem_status omnimem_select_compact(omnimem_ctx* ctx, const omnimem_layer* lay
   if ((st = set_device(ctx)) != OMNIMEM_OK) return st;
   const LayerDesc* dev = nullptr;
   if ((st = upload(ctx, layers, stream, &dev)) != OMNIMEM_OK) return st;
-  const bool split = ctx->topk_split_rows >= 0 && max_n > ctx->topk_split_rows &&
-                     (max_n + kTopkSlice - 1) / kTopkSlice <= kTopkMaxSlices;
+  // the ranking path: AUTO by the longest working set; a path that cannot
+  // take these sizes falls back to the one-workgroup ranking
+  int path = ctx->topk_path;
+  if (path == OMNIMEM_TOPK_AUTO)
+    path = max_n <= kTopkRegRows ? OMNIMEM_TOPK_REGISTERS
+           : max_n > kTopkAutoSplitRows ? OMNIMEM_TOPK_SPLIT : OMNIMEM_TOPK_ONE_WORKGROUP;
+  if ((path == OMNIMEM_TOPK_REGISTERS && max_n > kTopkRegRows) ||
+      (path == OMNIMEM_TOPK_SPLIT && max_n > kTopkSplitMaxRows))
+    path = OMNIMEM_TOPK_ONE_WORKGROUP;
   return finish(ctx, launch_select_compact(ctx->dm, ctx->cfg.dtype, ctx->cfg.lambda, ctx->cfg.shared_selection ? 1 : 0,
-                                           hidden, inplace, (int)max_n, split, dev, ctx->ws, a, s, budgets, idx,
+                                           hidden, inplace, (int)max_n, path, dev, ctx->ws, a, s, budgets, idx,
                                            stream),
                 stream, "omnimem_select_compact launch");
 }
@@ -775,9 +782,11 @@ omnimem_status omnimem_append(omnimem_ctx* ctx, const omnimem_layer* layers, con
                 "omnimem_append launch");
 }
 
-omnimem_status omnimem_set_topk_split(omnimem_ctx* ctx, int64_t rows) {
+omnimem_status omnimem_set_topk_path(omnimem_ctx* ctx, int32_t path) {
   if (!ctx) return fail(nullptr, OMNIMEM_ERR_INVALID_ARG, "null context");
-  ctx->topk_split_rows = rows < 0 ? -1 : rows;
+  if (path < OMNIMEM_TOPK_AUTO || path > OMNIMEM_TOPK_SPLIT)
+    return fail(ctx, OMNIMEM_ERR_INVALID_ARG, "top-k path %d is not an omnimem_topk_path", path);
+  ctx->topk_path = path;
   return OMNIMEM_OK;
 }
 

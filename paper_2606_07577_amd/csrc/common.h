@@ -237,7 +237,7 @@ __host__ __device__ inline int64_t topk_stride(int64_t max_tokens) {
 enum KernelId {
   K_LSE, K_LSE_MERGE, K_COLSUM, K_HEADSUM, K_LISTS, K_NORMS, K_GRAM, K_GRAM_FINISH, K_ADJ,
   K_AVBA_PART, K_AVBA_ALLOC, K_TOPK, K_GATHER, K_GATHER_H, K_ADJ_H, K_NORMS_H, K_GRAM_H, K_FINISH_H, K_LAYER_IN,
-  K_STAGE, K_GATHER_IP, K_APPEND, K_GRAM_SYM, K_TOPK_HIST, K_TOPK_BIN, K_TOPK_EMIT, K_COUNT
+  K_STAGE, K_GATHER_IP, K_APPEND, K_GRAM_SYM, K_TOPK_HIST, K_TOPK_BIN, K_TOPK_EMIT, K_TOPK_REG, K_COUNT
 };
 struct Profiler;
 void prof_mark(Profiler* p, int kernel, hipStream_t st, bool begin);
@@ -311,10 +311,14 @@ hipError_t launch_allocate_fixed(const Dims& dm, const LayerDesc* desc, const Wo
                                  const float* s, const int32_t* layer_budgets, float ratio_r, int32_t* budgets,
                                  float* stats, hipStream_t st);
 hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, int inplace,
-                                 int max_n, bool split, const LayerDesc* desc, const Workspace& ws, const float* a,
-                                 const float* s, const int32_t* budgets, int32_t* idx,
+                                 int max_n, int topk_path, const LayerDesc* desc, const Workspace& ws,
+                                 const float* a, const float* s, const int32_t* budgets, int32_t* idx,
                                  hipStream_t st);  // inplace: 0 none, 1 some, 2 all; max_n: largest N;
-                                                   // split: the top-k over several workgroups per working set
+                                                   // topk_path: an omnimem_topk_path other than AUTO
+// Rows up to which the top-k can keep every key in registers, and the
+// largest working set the split top-k takes.
+constexpr int kTopkRegRows = 8192;
+constexpr int64_t kTopkSplitMaxRows = (int64_t)kTopkMaxSlices * kTopkSlice;
 hipError_t launch_append(const Dims& dm, int dtype, const LayerDesc* desc, const Workspace& ws, int64_t max_rows,
                          hipStream_t st);
 

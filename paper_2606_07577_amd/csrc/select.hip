@@ -16,6 +16,7 @@
 //                  where they are defined).
 //  gather_compact  k_out[g][i] = k[g][idx[g][i]] and the same for v, 16 bytes
 //                  per lane, whole rows per lane group.
+#include "../../include/omnimem.h"
 #include "common.h"
 
 namespace omnimem {
@@ -66,6 +67,53 @@ __device__ inline int wave_scan(int v, int* wave_tot, int* total) {
   }
   *total = tot;
   return base;
+}
+
+// Inclusive scans over the workgroup's threads in thread order (one
+// barrier); wsum holds kSelWaves ints per value and must not be reused before a later
+// barrier.  tot: the sums.
+template <int NV>
+__device__ inline void block_inclusive(int (&v)[NV], int (*wsum)[kSelWaves], int (&tot)[NV]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    v[i] = wave_inclusive(v[i]);
+    if (lane == 63) wsum[i][wave] = v[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    int base = 0, t = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+      const int c = wsum[i][w];
+      base += w < wave ? c : 0;
+      t += c;
+    }
+    v[i] += base;
+    tot[i] = t;
+  }
+}
+
+// Of PER bins h[0..PER) taken from the highest down, with `above` keys in
+// the bins before them and above < need <= above + sum(h): the bin i that
+// holds the need-th largest key, how many of its keys are needed and its
+// count.  Branch-free: a selection per bin.
+template <int PER>
+__device__ inline void crossing_bin(const int (&h)[PER], int above, int need, int& bin, int& need_in, int& cnt) {
+  bin = 0;
+  need_in = 0;
+  cnt = 0;
+  bool found = false;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const bool hit = !found && need <= above + h[i];
+    bin = hit ? i : bin;
+    need_in = hit ? need - above : need_in;
+    cnt = hit ? h[i] : cnt;
+    found = found || hit;
+    above += h[i];
+  }
 }
 
 // Rows are dealt to waves in contiguous spans: wave w owns rows
@@ -390,6 +438,198 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
   }
 }
 
+// psi_topk for working sets of at most kRegRows rows: each lane keeps the
+// keys of its rows (wave w owns rows 512 w .. 512 w + 511, step i the 64
+// rows from 512 w + 64 i) in registers from the one round of reads to the
+// emission.  The radix select runs on them directly, 12-bit digits below
+// the bits all keys share, two LDS histograms taking turns (one is cleared
+// while the other is scanned), and stops at the first digit whose bin is
+// kept whole.
+constexpr int kRegSteps = 8;
+constexpr int kRegRows = kRegSteps * kSelThreads;
+
+template <bool SHARED>
+__global__ __launch_bounds__(kSelThreads) void psi_topk_reg(const LayerDesc* __restrict__ layers, Dims dm, float lambda,
+                                                            const float* __restrict__ a, const float* __restrict__ s,
+                                                            const int32_t* __restrict__ budgets,
+                                                            int32_t* __restrict__ idx, int* __restrict__ eff,
+                                                            int* __restrict__ slot_of, int* __restrict__ ctl) {
+  __shared__ int hist[2][kBins];
+  __shared__ int wsum[1][kSelWaves];
+  __shared__ int s_bin, s_need, s_cnt;
+  __shared__ int wt_mem[kSelWaves], wt_eq[kSelWaves], wt_sel[kSelWaves];
+  __shared__ uint32_t wmin[kSelWaves], wmax[kSelWaves];
+  const int mu = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  const int64_t off = ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
+  const float* ag = a + (SHARED ? (int64_t)l * dm.max_tokens : off);
+  const float* sg = s + (SHARED ? (int64_t)l * dm.max_tokens : off);
+  const int row0 = wave * 64 * kRegSteps + lane;
+  // a, s and the budgets are requested before the layer's descriptor arrives
+  // (indices kept inside the buffers' rows; rows past N are not used)
+  float av[kRegSteps], sv[kRegSteps];
+#pragma unroll
+  for (int i = 0; i < kRegSteps; ++i) {
+    const int j = min(row0 + 64 * i, (int)dm.max_tokens - 1);
+    av[i] = gload<float>(ag + j);
+    sv[i] = gload<float>(sg + j);
+  }
+  const int bud_mu = budgets[2 * l + mu], bud_v = budgets[2 * l];
+  if (ctl != nullptr && blockIdx.x == 0 && g == 0 && l == 0 && threadIdx.x == 0)
+    ctl[1] = 0;  // staging rows needed beyond the reserve, this call
+  const LayerDesc& Ld = layers[l];
+  const int N = Ld.n;
+  const uint8_t* mod = Ld.mod;
+  const int cap = Ld.out_cap;
+  int mv[kRegSteps];
+#pragma unroll
+  for (int i = 0; i < kRegSteps; ++i) mv[i] = gload<uint8_t>(mod + max(0, min(row0 + 64 * i, N - 1)));
+  for (int i = threadIdx.x; i < kBins; i += kSelThreads) hist[0][i] = 0;
+  // keys of the member rows, their count and range
+  bool mb[kRegSteps];
+  uint32_t kk[kRegSteps];
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  int wcount = 0;
+#pragma unroll
+  for (int i = 0; i < kRegSteps; ++i) {
+    mb[i] = (row0 + 64 * i < N) & ((mv[i] ? 1 : 0) == mu);
+    kk[i] = psi_key(av[i], sv[i], lambda);
+    wcount += __popcll(__ballot(mb[i]));
+    kmin = mb[i] ? min(kmin, kk[i]) : kmin;
+    kmax = mb[i] ? max(kmax, kk[i]) : kmax;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, 64));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
+  }
+  if (lane == 0) { wt_mem[wave] = wcount; wmin[wave] = kmin; wmax[wave] = kmax; }
+  __syncthreads();  // counts and ranges of the waves; histogram 0 cleared
+  int K = 0;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) {
+    K += wt_mem[w];
+    kmin = min(kmin, wmin[w]);
+    kmax = max(kmax, wmax[w]);
+  }
+  K = uniform(K);
+  kmin = (uint32_t)uniform((int)kmin);
+  kmax = (uint32_t)uniform((int)kmax);
+  // Budgets as applied: each modality's within its rows, visual first
+  // within the output capacity, audio in what remains.
+  const int Kv = mu ? N - K : K;
+  const int Mv = min(min(max(bud_v, 0), Kv), cap);
+  const int M = mu ? min(min(max(bud_mu, 0), K), cap - Mv) : Mv;
+  if (g == 0 && threadIdx.x == 0) eff[2 * l + mu] = M;
+  const int out0 = mu ? Mv : 0;
+  const bool all = M >= K, pick = !all && M > 0;
+
+  // Radix select of the M-th largest key: keep the keys above thr and the
+  // first take_eq keys equal to it.
+  uint32_t thr = 0;
+  int take_eq = 0, n_eq = 0;
+  if (pick) {
+    const int width = (kmin ^ kmax) ? 32 - __clz(kmin ^ kmax) : 0;  // low bits in which keys differ
+    const uint32_t low = width < 32 ? (1u << width) - 1u : 0xFFFFFFFFu;
+    uint32_t prefix = kmin & ~low, mask = ~low;
+    int need = M, cnt = K, buf = 0;
+    bool whole = false;
+    for (int top = width; top > 0 && !whole;) {
+      const int shift = max(0, top - kDigit);
+      const uint32_t dmask = (1u << (top - shift)) - 1u;
+#pragma unroll
+      for (int i = 0; i < kRegSteps; ++i)
+        if (mb[i] && (kk[i] & mask) == prefix) atomicAdd(&hist[buf][(kk[i] >> shift) & dmask], 1);
+      __syncthreads();
+      // bins from the top: thread t holds bins btop - q, q < PER; the other
+      // histogram is cleared for the next digit meanwhile
+      constexpr int PER = kBins / kSelThreads;
+      const int btop = kBins - 1 - PER * (int)threadIdx.x;
+      int h[PER], mine = 0;
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        h[q] = hist[buf][btop - q];
+        hist[buf ^ 1][btop - q] = 0;
+        mine += h[q];
+      }
+      int v[1] = {mine}, tot[1];
+      block_inclusive<1>(v, wsum, tot);
+      const int above = v[0] - mine;
+      int bi, need_in, cnt_in;
+      crossing_bin<PER>(h, above, need, bi, need_in, cnt_in);
+      if (above < need && need <= above + mine) { s_bin = btop - bi; s_need = need_in; s_cnt = cnt_in; }
+      __syncthreads();
+      prefix |= (uint32_t)uniform(s_bin) << shift;
+      mask |= dmask << shift;
+      need = uniform(s_need);
+      cnt = uniform(s_cnt);
+      whole = need >= cnt;
+      top = shift;
+      buf ^= 1;
+      __syncthreads();  // every thread has read s_bin, s_need, s_cnt
+    }
+    if (whole) {
+      thr = prefix - 1u;  // the keys from prefix up: the whole bin and every bin above it
+    } else {
+      thr = prefix;       // every bit resolved: the threshold key itself
+      take_eq = need;
+      n_eq = cnt;
+    }
+  }
+
+  // Ordered emission: rows above thr and the first take_eq rows equal to it
+  // (ties to the lower row), in ascending row order.
+  const bool eq_ranks = pick && take_eq > 0 && take_eq < n_eq;
+  bool keep_eq[kRegSteps];
+#pragma unroll
+  for (int i = 0; i < kRegSteps; ++i) keep_eq[i] = take_eq > 0;
+  if (eq_ranks) {
+    unsigned long long eb[kRegSteps];
+    int weq = 0;
+#pragma unroll
+    for (int i = 0; i < kRegSteps; ++i) {
+      eb[i] = __ballot(mb[i] & (kk[i] == thr));
+      weq += __popcll(eb[i]);
+    }
+    int eq_tot;
+    int run = wave_scan(weq, wt_eq, &eq_tot);
+#pragma unroll
+    for (int i = 0; i < kRegSteps; ++i) {
+      if ((eb[i] >> lane) & 1ull) keep_eq[i] = run + __popcll(eb[i] & lt) < take_eq;
+      run += __popcll(eb[i]);
+    }
+  }
+  unsigned long long sb[kRegSteps];
+  int wsel = 0;
+#pragma unroll
+  for (int i = 0; i < kRegSteps; ++i) {
+    const bool sel = mb[i] & (all | (pick & ((kk[i] > thr) | ((kk[i] == thr) & keep_eq[i]))));
+    sb[i] = __ballot(sel);
+    wsel += __popcll(sb[i]);
+  }
+  int sel_tot;
+  int o = wave_scan(wsel, wt_sel, &sel_tot) + out0;
+  const bool want_slots = Ld.inplace != 0 && slot_of != nullptr;
+  int32_t* ig = idx + off;
+  int* so = want_slots ? slot_of + off : nullptr;
+  const int heads = SHARED ? dm.Hkv : 1;
+#pragma unroll
+  for (int i = 0; i < kRegSteps; ++i) {
+    const int row = row0 + 64 * i;
+    if ((sb[i] >> lane) & 1ull) {
+      const int slot = o + __popcll(sb[i] & lt);
+      for (int h = 0; h < heads; ++h) {
+        ig[(int64_t)h * dm.max_tokens + slot] = row;
+        if (so) so[(int64_t)h * dm.max_tokens + row] = slot;
+      }
+    } else if (so && mb[i]) {
+      for (int h = 0; h < heads; ++h) so[(int64_t)h * dm.max_tokens + row] = -1;
+    }
+    o += __popcll(sb[i]);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Top-k split over several workgroups per (layer, KV head), for long working
 // sets.  A row's key is psi's order-preserving bits with its modality in bit
@@ -414,6 +654,7 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk(const LayerDesc* __restr
 // ---------------------------------------------------------------------------
 constexpr int kTkThreads = 1024;
 constexpr int kTkWaves = kTkThreads / 64;
+static_assert(kTkWaves == kSelWaves, "the scans are sized for one workgroup size");
 constexpr int kHistRows = 4096;                       // rows per topk_hist workgroup
 constexpr int kSliceSteps = kTopkSlice / kTkThreads;  // rows per lane of a slice
 constexpr int kCandLds = 4096;                        // candidates of a modality ranked in LDS
@@ -426,53 +667,6 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 __device__ inline uint2 gload8(const void* p) {
   const u32x2 v = gload<u32x2>(p);
   return make_uint2(v[0], v[1]);
-}
-
-// Inclusive scans over the 256 threads in thread order (one barrier); wsum
-// holds kTkWaves ints per value and must not be reused before a later
-// barrier.  tot: the sums.
-template <int NV>
-__device__ inline void block_inclusive(int (&v)[NV], int (*wsum)[kTkWaves], int (&tot)[NV]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    v[i] = wave_inclusive(v[i]);
-    if (lane == 63) wsum[i][wave] = v[i];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    int base = 0, t = 0;
-#pragma unroll
-    for (int w = 0; w < kTkWaves; ++w) {
-      const int c = wsum[i][w];
-      base += w < wave ? c : 0;
-      t += c;
-    }
-    v[i] += base;
-    tot[i] = t;
-  }
-}
-
-// Of PER bins h[0..PER) taken from the highest down, with `above` keys in
-// the bins before them and above < need <= above + sum(h): the bin i that
-// holds the need-th largest key, how many of its keys are needed and its
-// count.  Branch-free: a selection per bin.
-template <int PER>
-__device__ inline void crossing_bin(const int (&h)[PER], int above, int need, int& bin, int& need_in, int& cnt) {
-  bin = 0;
-  need_in = 0;
-  cnt = 0;
-  bool found = false;
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const bool hit = !found && need <= above + h[i];
-    bin = hit ? i : bin;
-    need_in = hit ? need - above : need_in;
-    cnt = hit ? h[i] : cnt;
-    found = found || hit;
-    above += h[i];
-  }
 }
 
 template <bool SHARED>
@@ -1283,11 +1477,18 @@ void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, c
 }
 
 template <bool SHARED>
-void launch_topk(const Dims& dm, float lambda, int max_n, bool split, const LayerDesc* desc, const Workspace& ws,
+void launch_topk(const Dims& dm, float lambda, int max_n, int path, const LayerDesc* desc, const Workspace& ws,
                  const float* a, const float* s, const int32_t* budgets, int32_t* ix, int* slot_of, int* ctl,
                  hipStream_t st) {
   const unsigned heads = SHARED ? 1u : (unsigned)dm.Hkv;
-  if (!split) {
+  if (path == OMNIMEM_TOPK_REGISTERS) {
+    static_assert(kRegRows == kTopkRegRows, "the register path's rows");
+    OMNIMEM_LAUNCH(ws, K_TOPK_REG, st,
+                   psi_topk_reg<SHARED><<<dim3(2, heads, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets,
+                                                                                      ix, ws.eff, slot_of, ctl));
+    return;
+  }
+  if (path != OMNIMEM_TOPK_SPLIT) {
     OMNIMEM_LAUNCH(ws, K_TOPK, st,
                    psi_topk<SHARED><<<dim3(2, heads, dm.L), kSelThreads, 0, st>>>(desc, dm, lambda, a, s, budgets,
                                                                                   ws.keys, ix, ws.eff, slot_of, ctl));
@@ -1311,8 +1512,9 @@ void launch_topk(const Dims& dm, float lambda, int max_n, bool split, const Laye
 }  // namespace
 
 hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int shared, bool hidden, int inplace,
-                                 int max_n, bool split, const LayerDesc* desc, const Workspace& ws, const float* a,
-                                 const float* s, const int32_t* budgets, int32_t* idx, hipStream_t st) {
+                                 int max_n, int topk_path, const LayerDesc* desc, const Workspace& ws,
+                                 const float* a, const float* s, const int32_t* budgets, int32_t* idx,
+                                 hipStream_t st) {
   int32_t* ix = idx ? idx : ws.idx;
   int* slot_of = inplace ? ws.slot_of : nullptr;
   int* ctl = ws.stage_rows > 0 ? ws.ctl : nullptr;
@@ -1321,9 +1523,9 @@ hipError_t launch_select_compact(const Dims& dm, int dtype, float lambda, int sh
     float* ls = ws.layer_as + (size_t)dm.L * dm.max_tokens;
     const dim3 gtok((unsigned)((dm.max_tokens + 255) / 256), dm.L);
     OMNIMEM_LAUNCH(ws, K_LAYER_IN, st, layer_inputs<<<gtok, 256, 0, st>>>(desc, dm, a, s, la, ls));
-    launch_topk<true>(dm, lambda, max_n, split, desc, ws, la, ls, budgets, ix, slot_of, ctl, st);
+    launch_topk<true>(dm, lambda, max_n, topk_path, desc, ws, la, ls, budgets, ix, slot_of, ctl, st);
   } else {
-    launch_topk<false>(dm, lambda, max_n, split, desc, ws, a, s, budgets, ix, slot_of, ctl, st);
+    launch_topk<false>(dm, lambda, max_n, topk_path, desc, ws, a, s, budgets, ix, slot_of, ctl, st);
   }
   if (dtype == 0) {
     if (dm.d == 128) launch_gather<uint16_t, 128>(dm, desc, ws, ix, inplace, max_n, st);

@@ -20,13 +20,14 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_INFEASIBLE, ERR_CAPACITY, ERR_HIP = ra
 BF16, F32 = 0, 1
 SIM_MAX, SIM_ADJ = 0, 1
 SRC_VALUES, SRC_KEYS, SRC_HIDDEN = 0, 1, 2
+TOPK_AUTO, TOPK_REGISTERS, TOPK_ONE_WORKGROUP, TOPK_SPLIT = 0, 1, 2, 3
 
 EXPORTED = [
     "omnimem_config_default", "omnimem_create", "omnimem_destroy", "omnimem_last_error",
     "omnimem_score", "omnimem_redundancy", "omnimem_allocate", "omnimem_select_compact",
     "omnimem_calibrate", "omnimem_calibration_reset", "omnimem_calibration_budgets",
     "omnimem_allocate_fixed", "omnimem_profile", "omnimem_profile_report", "omnimem_inplace_status",
-    "omnimem_append", "omnimem_allocate_noalloc", "omnimem_set_topk_split",
+    "omnimem_append", "omnimem_allocate_noalloc", "omnimem_set_topk_path",
 ]
 
 
@@ -113,8 +114,8 @@ def load_library(path=LIB_PATH):
     lib.omnimem_inplace_status.restype = i32
     lib.omnimem_append.argtypes = [vp, ctypes.POINTER(Layer), ctypes.POINTER(Chunk), vp]
     lib.omnimem_append.restype = i32
-    lib.omnimem_set_topk_split.argtypes = [vp, i64]
-    lib.omnimem_set_topk_split.restype = i32
+    lib.omnimem_set_topk_path.argtypes = [vp, i32]
+    lib.omnimem_set_topk_path.restype = i32
     lib.omnimem_profile.argtypes = [vp, ctypes.c_int32]
     lib.omnimem_profile.restype = i32
     lib.omnimem_profile_report.argtypes = [vp, ctypes.POINTER(KernelTime), ctypes.c_int32,
@@ -276,11 +277,10 @@ class Context:
         arr = chunks if isinstance(chunks, ctypes.Array) else (Chunk * len(chunks))(*chunks)
         self._check(self._lib.omnimem_append(self.handle, self._layers(layers), arr, _stream(stream)))
 
-    def omnimem_set_topk_split(self, rows):
-        """Split the top-k over several workgroups per (layer, KV head) when
-        the longest working set has more than `rows` rows (0: always, -1:
-        never)."""
-        self._check(self._lib.omnimem_set_topk_split(self.handle, int(rows)))
+    def omnimem_set_topk_path(self, path):
+        """Ranking path of later select_compact calls (TOPK_AUTO,
+        TOPK_REGISTERS, TOPK_ONE_WORKGROUP or TOPK_SPLIT)."""
+        self._check(self._lib.omnimem_set_topk_path(self.handle, int(path)))
 
     def omnimem_profile(self, on):
         self._check(self._lib.omnimem_profile(self.handle, int(bool(on))))

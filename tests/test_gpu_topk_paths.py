@@ -1,17 +1,20 @@
-"""The top-k split over several workgroups per (layer, KV head) (topk_hist,
-topk_bin, topk_emit) against the one-workgroup top-k (psi_topk) and the
-oracle's top-M (Eqs. 4, 5 and 8), through the C ABI.
+"""The three ranking paths of the selection (Eqs. 4, 5 and 8) against each
+other and against the oracle's top-M, through the C ABI: one workgroup per
+(layer, KV head, modality) with keys in LDS (psi_topk), the same with every
+key in registers for working sets of at most 8192 rows (psi_topk_reg), and
+several workgroups per (layer, KV head) (topk_hist, topk_bin, topk_emit).
 
-Both rankings must keep exactly the same rows (the top M of each modality
-by the fp32 psi key, ties to the lower row), so idx and the compacted K/V
-must agree bit for bit; the kept rows are also checked against the
-oracle's psi.  Inputs: the synthetic a, s of the selection stage on small
-ragged layers (one slice), a 6144-token layer (three slices) and a
-20001-token layer (ten slices, the last ragged), plus a, s built to stress
-the ranking: psi quantised to a few values (ties across slices), one psi
-for every row (the threshold bin's candidates exceed what LDS holds), and
-zero and NaN scores; budgets of 0, 1, all rows, beyond the rows and beyond
-the output capacity; layer-shared selection and compaction in place.
+All paths must keep exactly the same rows (the top M of each modality by
+the fp32 psi key, ties to the lower row), so idx and the compacted K/V must
+agree bit for bit; the kept rows are also checked against the oracle's psi.
+Inputs: the synthetic a, s of the selection stage on small ragged layers
+(one slice), a 6144-token layer (three slices) and a 20001-token layer (ten
+slices, the last ragged; the register path does not take it and falls back
+to one workgroup), plus a, s built to stress the ranking: psi quantised to
+a few values (ties across slices), one psi for every row (the threshold
+bin's candidates exceed what LDS holds), and zero and NaN scores; budgets
+of 0, 1, all rows, beyond the rows and beyond the output capacity;
+layer-shared selection and compaction in place.
 """
 import numpy as np
 import pytest
@@ -26,7 +29,8 @@ from tests.test_gpu_parity import ragged_layers
 
 pytestmark = pytest.mark.gpu
 
-NEVER, ALWAYS = -1, 0
+PATHS = (omnimem.TOPK_ONE_WORKGROUP, omnimem.TOPK_REGISTERS, omnimem.TOPK_SPLIT)
+ONE, REG, SPLIT = PATHS
 
 
 def _long_layer(seed=500, n_cache_v=12000, n_cache_a=4001, frames=(4, 900, 100), h_kv=2):
@@ -80,8 +84,8 @@ def _budgets(layers, which):
     return out
 
 
-def _run(step, a, s, budgets, split):
-    step.ctx.omnimem_set_topk_split(split)
+def _run(step, a, s, budgets, path):
+    step.ctx.omnimem_set_topk_path(path)
     for t in step.k_out + step.v_out:
         t.zero_()
     step.idx.fill_(-1)
@@ -92,14 +96,16 @@ def _run(step, a, s, budgets, split):
 
 def _check(step, layers, a_h, s_h, budgets, shared=False):
     a, s = step.to_device_f32(a_h), step.to_device_f32(s_h)
-    one = _run(step, a, s, budgets, NEVER)
-    split = _run(step, a, s, budgets, ALWAYS)
+    one = _run(step, a, s, budgets, ONE)
+    others = [_run(step, a, s, budgets, path) for path in (REG, SPLIT)]
+    split = others[1]
     for l, lay in enumerate(layers):
         n = len(lay["modality"])
         mv, ma = _applied(budgets[l], lay["modality"], n)
         m = mv + ma
-        assert torch.equal(one[0][l, :, :m], split[0][l, :, :m]), f"layer {l}: kept rows differ"
-        assert torch.equal(one[1][l][:, :m], split[1][l][:, :m]) and torch.equal(one[2][l][:, :m], split[2][l][:, :m])
+        for path, res in zip((REG, SPLIT), others):
+            assert torch.equal(one[0][l, :, :m], res[0][l, :, :m]), f"path {path}, layer {l}: kept rows differ"
+            assert torch.equal(one[1][l][:, :m], res[1][l][:, :m]) and torch.equal(one[2][l][:, :m], res[2][l][:, :m])
         a64 = np.asarray(a_h[l], dtype=np.float64)
         s64 = np.asarray(s_h[l], dtype=np.float64)
         if shared:   # one ranking per layer: a summed over the heads, s averaged (fp32, head order)
@@ -117,7 +123,7 @@ def _check(step, layers, a_h, s_h, budgets, shared=False):
 
 @pytest.mark.parametrize("name", ["ragged-3layer", "qwen-layer", "long-20001"])
 @pytest.mark.parametrize("kind", ["synthetic", "ties", "constant", "zeros-nans"])
-def test_split_topk_equals_one_workgroup(name, kind):
+def test_paths_keep_the_same_rows(name, kind):
     layers = _workload(name)
     h_kv = layers[0]["k"].shape[0]
     step = DeviceStep(layers, 1000)
@@ -128,7 +134,7 @@ def test_split_topk_equals_one_workgroup(name, kind):
     step.close()
 
 
-def test_split_topk_output_capacity():
+def test_paths_output_capacity():
     layers = _workload("qwen-layer")
     n = len(layers[0]["modality"])
     cap = 2500
@@ -141,8 +147,8 @@ def test_split_topk_output_capacity():
                                None, k_small, v_small, out_rows=cap)]
     bud = torch.tensor([(2000, 1500)], dtype=torch.int32, device=step.device)
     res = []
-    for split in (NEVER, ALWAYS):
-        step.ctx.omnimem_set_topk_split(split)
+    for path in PATHS:
+        step.ctx.omnimem_set_topk_path(path)
         step.idx.fill_(-1)
         k_small.zero_()
         v_small.zero_()
@@ -151,13 +157,14 @@ def test_split_topk_output_capacity():
         res.append((step.idx.clone(), k_small.clone(), v_small.clone()))
     mv, ma = _applied((2000, 1500), layers[0]["modality"], cap)
     assert (mv, ma) == (2000, 500) and n > cap
-    assert torch.equal(res[0][0][0, :, :cap], res[1][0][0, :, :cap])
-    assert torch.equal(res[0][1], res[1][1]) and torch.equal(res[0][2], res[1][2])
+    for r in res[1:]:
+        assert torch.equal(res[0][0][0, :, :cap], r[0][0, :, :cap])
+        assert torch.equal(res[0][1], r[1]) and torch.equal(res[0][2], r[2])
     step.close()
 
 
 @pytest.mark.parametrize("kind", ["synthetic", "ties"])
-def test_split_topk_shared_selection(kind):
+def test_paths_shared_selection(kind):
     layers = _workload("long-20001") if kind == "synthetic" else _workload("ragged-3layer")
     step = DeviceStep(layers, 1000, shared_selection=1)
     a_h, s_h = _scores(layers, step.h_kv, kind)
@@ -168,23 +175,23 @@ def test_split_topk_shared_selection(kind):
     step.close()
 
 
+@pytest.mark.parametrize("path", [REG, SPLIT])
 @pytest.mark.parametrize("budget", [(260, 90), (150, 50), (0, 116), (323, 0), (300, 1)])
-def test_split_topk_in_place(budget):
+def test_paths_in_place(budget, path):
     layers = ragged_layers(seed=200)
     step = DeviceStep(layers, 300, inplace_stage_rows=128)
     a, s = synth.make_scores([l["modality"] for l in layers], step.h_kv, 1)
     a, s = step.to_device_f32(a), step.to_device_f32(s)
-    step.ctx.omnimem_set_topk_split(NEVER)
-    ref = _run(step, a, s, [budget], NEVER)[0]
-    step.ctx.omnimem_set_topk_split(ALWAYS)
+    ref = _run(step, a, s, [budget], ONE)[0]
+    step.ctx.omnimem_set_topk_path(path)
     _compare(step, layers, [budget], a, s)
     m = sum(_applied(budget, layers[0]["modality"], len(layers[0]["modality"])))
-    split = _run(step, a, s, [budget], ALWAYS)[0]
-    assert torch.equal(ref[0, :, :m], split[0, :, :m])
+    got = _run(step, a, s, [budget], path)[0]
+    assert torch.equal(ref[0, :, :m], got[0, :, :m])
     step.close()
 
 
-def test_split_topk_repeated_calls_leave_no_state():
+def test_split_path_repeated_calls_leave_no_state():
     # The global histograms are cleared by each call: the same inputs give
     # the same rows on every call, and a call on other inputs in between
     # does not leak into the next one.
@@ -195,9 +202,17 @@ def test_split_topk_repeated_calls_leave_no_state():
     d1 = step.to_device_f32(a1), step.to_device_f32(s1)
     d2 = step.to_device_f32(a2), step.to_device_f32(s2)
     bud = _budgets(layers, "half")
-    first = _run(step, *d1, bud, ALWAYS)[0]
+    first = _run(step, *d1, bud, SPLIT)[0]
     for _ in range(3):
-        _run(step, *d2, bud, ALWAYS)
-        again = _run(step, *d1, bud, ALWAYS)[0]
+        _run(step, *d2, bud, SPLIT)
+        again = _run(step, *d1, bud, SPLIT)[0]
         assert torch.equal(first, again)
+    step.close()
+
+
+def test_unknown_path_is_refused():
+    step = DeviceStep(_workload("ragged-3layer"), 300)
+    with pytest.raises(omnimem.OmnimemError):
+        step.ctx.omnimem_set_topk_path(7)
+    step.ctx.omnimem_set_topk_path(omnimem.TOPK_AUTO)
     step.close()
