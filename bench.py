@@ -31,30 +31,37 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
-        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
-        "append_chunk": 235255686, "lse_pass": 604414862, "lse_merge": 19381020, "colsum_pass": 622617905,
-        "head_sum": 21741403, "lists_norms": 181331651, "gram_sym": 816381184, "gram_finish": 6206193,
-        "avba_partials": 6040922, "avba_allocate": 180771, "psi_topk": 17178582, "stage_moved_back": 15209435,
-        "gather_inplace": 417910033,
+        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
+        "append_chunk": 235255316, "lse_pass": 604361225, "lse_merge": 19381020, "colsum_pass": 622594095,
+        "head_sum": 21741394, "lists_norms": 181331549, "gram_sym": 816667465, "gram_finish": 6206188,
+        "avba_partials": 6040923, "avba_allocate": 180771, "psi_topk_reg": 20836413, "stage_moved_back": 15204357,
+        "gather_inplace": 417901335
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
-        "lse_pass": 608607492, "lse_merge": 19381168, "colsum_pass": 613155300, "head_sum": 22114184,
-        "lists_norms": 184701051, "gram_sym": 822267402, "gram_finish": 6248421, "avba_partials": 6078432,
-        "avba_allocate": 123709, "psi_topk": 14666015, "gather_compact": 471798186,
+        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
+        "lse_pass": 608518137, "lse_merge": 19381249, "colsum_pass": 613578672, "head_sum": 22114129,
+        "lists_norms": 184700838, "gram_sym": 824524066, "gram_finish": 6248350, "avba_partials": 6078433,
+        "avba_allocate": 123709, "psi_topk_reg": 14469402, "gather_compact": 471793444
     },
     "qwen7b-layer-6144": {
-        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
-        "lse_pass": 31059193, "lse_merge": 1738838, "colsum_pass": 33068509, "head_sum": 1292309,
-        "lists_norms": 6740159, "gram_sym": 14033861, "gram_finish": 245756, "avba_partials": 300160,
-        "avba_allocate": 36063, "psi_topk": 861627, "gather_compact": 16889831,
+        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
+        "lse_pass": 31045097, "lse_merge": 1738838, "colsum_pass": 33079534, "head_sum": 1292311,
+        "lists_norms": 6740160, "gram_sym": 14033859, "gram_finish": 245756, "avba_partials": 300160,
+        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889834
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "3d1fe966a96eba485413dcb0d3bbc76102346fc02ec45760e248bf22936cd2a5",
-        "lse_pass": 31060948, "lse_merge": 1738710, "colsum_pass": 33071501, "head_sum": 1292280,
-        "modality_lists": 65787, "hidden_norms": 44175419, "gram_wide": 188161894, "hidden_finish": 138273,
-        "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 265346, "psi_topk": 271034,
-        "gather_compact": 16889947, "gather_hidden": 58879344,
+        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
+        "lse_pass": 31046405, "lse_merge": 1738710, "colsum_pass": 33079966, "head_sum": 1292317,
+        "modality_lists": 65832, "hidden_norms": 44175423, "gram_wide": 188161912, "hidden_finish": 138239,
+        "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 272514, "psi_topk_reg": 218044,
+        "gather_compact": 16889857, "gather_hidden": 58875388
+    },
+    "qwen7b-longcache-40960": {
+        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
+        "lse_pass": 5075300489, "lse_merge": 3850240, "colsum_pass": 380318796, "head_sum": 5296188,
+        "lists_norms": 44062563, "gram_sym": 957379805, "gram_finish": 1499112, "avba_partials": 1460429,
+        "avba_allocate": 53471, "topk_hist": 2205441, "topk_bin": 1949050, "topk_emit": 2722502,
+        "gather_compact": 134816419
     },
 }
 
