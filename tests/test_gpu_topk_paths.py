@@ -216,3 +216,17 @@ def test_unknown_path_is_refused():
         step.ctx.omnimem_set_topk_path(7)
     step.ctx.omnimem_set_topk_path(omnimem.TOPK_AUTO)
     step.close()
+
+
+def test_paths_single_modality_layers_and_tiny_working_sets():
+    # A visual-only layer, an audio-only layer and a 3-row layer in one call:
+    # one modality's segment is empty, budgets reach past it, and the split
+    # path's only slice is nearly empty.
+    layers = [ragged_layers(seed=106, caches=((150, 0),), frames=(2, 30, 0))[0],
+              ragged_layers(seed=107, caches=((0, 90),), frames=(2, 0, 20))[0],
+              ragged_layers(seed=108, caches=((1, 1),), frames=(1, 1, 0))[0]]
+    step = DeviceStep(layers, 200)
+    a_h, s_h = _scores(layers, step.h_kv, "synthetic")
+    for budgets in ([(100, 5), (5, 60), (1, 1)], [(500, 500), (500, 500), (500, 500)], [(0, 0), (0, 1), (2, 0)]):
+        _check(step, layers, a_h, s_h, budgets)
+    step.close()
