@@ -32,36 +32,36 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
         "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "append_chunk": 235255316, "lse_pass": 604361225, "lse_merge": 19381020, "colsum_pass": 622594095,
-        "head_sum": 21741394, "lists_norms": 181331549, "gram_sym": 816667465, "gram_finish": 6206188,
-        "avba_partials": 6040923, "avba_allocate": 180771, "psi_topk_reg": 20836413, "stage_moved_back": 15204357,
-        "gather_inplace": 417901335
+        "append_chunk": 235255483, "lse_pass": 604352514, "lse_merge": 19381025, "colsum_pass": 622752439,
+        "head_sum": 21741411, "lists_norms": 181331544, "gram_sym": 816356564, "gram_finish": 6206189,
+        "avba_partials": 6040924, "avba_allocate": 180771, "psi_topk_reg": 20836428, "stage_moved_back": 15204375,
+        "gather_inplace": 417902347
     },
     "qwen7b-28layer-6144": {
         "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 608518137, "lse_merge": 19381249, "colsum_pass": 613578672, "head_sum": 22114129,
-        "lists_norms": 184700838, "gram_sym": 824524066, "gram_finish": 6248350, "avba_partials": 6078433,
-        "avba_allocate": 123709, "psi_topk_reg": 14469402, "gather_compact": 471793444
+        "lse_pass": 608261853, "lse_merge": 19381200, "colsum_pass": 613581644, "head_sum": 22114177,
+        "lists_norms": 184700833, "gram_sym": 824972350, "gram_finish": 6248351, "avba_partials": 6078434,
+        "avba_allocate": 123709, "psi_topk_reg": 14469370, "gather_compact": 471796146
     },
     "qwen7b-layer-6144": {
         "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 31045097, "lse_merge": 1738838, "colsum_pass": 33079534, "head_sum": 1292311,
-        "lists_norms": 6740160, "gram_sym": 14033859, "gram_finish": 245756, "avba_partials": 300160,
-        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889834
+        "lse_pass": 31046025, "lse_merge": 1738861, "colsum_pass": 33088850, "head_sum": 1292309,
+        "lists_norms": 6740160, "gram_sym": 14033821, "gram_finish": 245756, "avba_partials": 300160,
+        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889847
     },
     "qwen7b-layer-6144-hidden": {
         "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 31046405, "lse_merge": 1738710, "colsum_pass": 33079966, "head_sum": 1292317,
-        "modality_lists": 65832, "hidden_norms": 44175423, "gram_wide": 188161912, "hidden_finish": 138239,
+        "lse_pass": 31045922, "lse_merge": 1738710, "colsum_pass": 33079026, "head_sum": 1292417,
+        "modality_lists": 65832, "hidden_norms": 44175363, "gram_wide": 188161935, "hidden_finish": 138239,
         "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 272514, "psi_topk_reg": 218044,
-        "gather_compact": 16889857, "gather_hidden": 58875388
+        "gather_compact": 16889935, "gather_hidden": 58875443
     },
     "qwen7b-longcache-40960": {
         "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 5075300489, "lse_merge": 3850240, "colsum_pass": 380318796, "head_sum": 5296188,
-        "lists_norms": 44062563, "gram_sym": 957379805, "gram_finish": 1499112, "avba_partials": 1460429,
-        "avba_allocate": 53471, "topk_hist": 2205441, "topk_bin": 1949050, "topk_emit": 2722502,
-        "gather_compact": 134816419
+        "lse_pass": 5088958436, "lse_merge": 3850240, "colsum_pass": 380478253, "head_sum": 5296260,
+        "lists_norms": 44062901, "gram_sym": 955946068, "gram_finish": 1499112, "avba_partials": 1460512,
+        "avba_allocate": 53471, "topk_hist": 2205605, "topk_bin": 1949125, "topk_emit": 2722502,
+        "gather_compact": 134817497
     },
 }
 
