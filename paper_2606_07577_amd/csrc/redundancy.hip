@@ -596,6 +596,10 @@ constexpr int kWideChunk = 64;  // d elements per LDS stage row
 // for fp32 (four waves of 64 x 64; a 256-row fp32 stage would not fit LDS).
 template <typename T> constexpr int wide_block() { return sizeof(T) == 2 ? 256 : 128; }
 template <typename T> constexpr int wide_threads() { return wide_block<T>() / 32 * 64; }
+// Waves per SIMD the register budget is sized for: two for bf16 (eight
+// waves in the one workgroup of a compute unit); one for fp32 (four waves,
+// and the stage leaves room for one workgroup).
+template <typename T> constexpr int wide_waves_per_simd() { return sizeof(T) == 2 ? 2 : 1; }
 
 __device__ inline float swz_xor(float v, int m) {
   // ds_swizzle bit mode (and-mask 0x1F, xor-mask m): within groups of 32 lanes
@@ -651,7 +655,7 @@ __global__ __launch_bounds__(256) void hidden_norms(const LayerDesc* __restrict_
 }
 
 template <typename T>
-__global__ __launch_bounds__(wide_threads<T>(), 2) void gram_wide(
+__global__ __launch_bounds__(wide_threads<T>(), wide_waves_per_simd<T>()) void gram_wide(
     const LayerDesc* __restrict__ layers, Dims dm, const int* __restrict__ pos, const int* __restrict__ counts,
     const float* __restrict__ inv, int* __restrict__ best) {
   using M = Mfma<T>;
