@@ -31,37 +31,37 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
-        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "append_chunk": 235255483, "lse_pass": 604352514, "lse_merge": 19381025, "colsum_pass": 622752439,
-        "head_sum": 21741411, "lists_norms": 181331544, "gram_sym": 816356564, "gram_finish": 6206189,
-        "avba_partials": 6040924, "avba_allocate": 180771, "psi_topk_reg": 20836428, "stage_moved_back": 15204375,
-        "gather_inplace": 417902347
+        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
+        "append_chunk": 235255223, "lse_pass": 604356467, "lse_merge": 19381024, "colsum_pass": 622677118,
+        "head_sum": 21741399, "lists_norms": 181331508, "gram_sym": 816339141, "gram_finish": 6206188,
+        "avba_partials": 6040922, "avba_allocate": 180771, "psi_topk_reg": 20836432, "stage_moved_back": 15204399,
+        "gather_inplace": 417905968
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 608261853, "lse_merge": 19381200, "colsum_pass": 613581644, "head_sum": 22114177,
-        "lists_norms": 184700833, "gram_sym": 824972350, "gram_finish": 6248351, "avba_partials": 6078434,
-        "avba_allocate": 123709, "psi_topk_reg": 14469370, "gather_compact": 471796146
+        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
+        "lse_pass": 608220340, "lse_merge": 19381194, "colsum_pass": 613970961, "head_sum": 22114178,
+        "lists_norms": 184701193, "gram_sym": 825564684, "gram_finish": 6248350, "avba_partials": 6078432,
+        "avba_allocate": 123709, "psi_topk_reg": 14469367, "gather_compact": 471796909
     },
     "qwen7b-layer-6144": {
-        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 31046025, "lse_merge": 1738861, "colsum_pass": 33088850, "head_sum": 1292309,
-        "lists_norms": 6740160, "gram_sym": 14033821, "gram_finish": 245756, "avba_partials": 300160,
-        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889847
+        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
+        "lse_pass": 31065607, "lse_merge": 1738838, "colsum_pass": 33068992, "head_sum": 1292306,
+        "lists_norms": 6740136, "gram_sym": 14033841, "gram_finish": 245756, "avba_partials": 300160,
+        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889839
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 31045922, "lse_merge": 1738710, "colsum_pass": 33079026, "head_sum": 1292417,
-        "modality_lists": 65832, "hidden_norms": 44175363, "gram_wide": 188161935, "hidden_finish": 138239,
+        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
+        "lse_pass": 31064187, "lse_merge": 1738710, "colsum_pass": 33074063, "head_sum": 1292371,
+        "modality_lists": 65832, "hidden_norms": 44175353, "gram_wide": 188161890, "hidden_finish": 138239,
         "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 272514, "psi_topk_reg": 218044,
-        "gather_compact": 16889935, "gather_hidden": 58875443
+        "gather_compact": 16889919, "gather_hidden": 58875453
     },
     "qwen7b-longcache-40960": {
-        "sources_sha256": "c00c9217ae32b00b88313bc97abb1fe3498b361aabd561da608439d839194638",
-        "lse_pass": 5088958436, "lse_merge": 3850240, "colsum_pass": 380478253, "head_sum": 5296260,
-        "lists_norms": 44062901, "gram_sym": 955946068, "gram_finish": 1499112, "avba_partials": 1460512,
-        "avba_allocate": 53471, "topk_hist": 2205605, "topk_bin": 1949125, "topk_emit": 2722502,
-        "gather_compact": 134817497
+        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
+        "lse_pass": 5088207845, "lse_merge": 3850239, "colsum_pass": 380773118, "head_sum": 5296172,
+        "lists_norms": 44062563, "gram_sym": 955931456, "gram_finish": 1499112, "avba_partials": 1460429,
+        "avba_allocate": 53470, "topk_hist": 2205441, "topk_bin": 1949072, "topk_emit": 2722502,
+        "gather_compact": 134817184
     },
 }
 
