@@ -1282,25 +1282,45 @@ struct RowCopy {
 };
 
 // Zero the read flags and ticket counters, and stage the slots that take a
-// row in front of them.
+// row in front of them.  Grid: (ceil(stage_rows / 64), H_kv, L); tile x
+// stages audio slots M_v + 64x .. + 63 (the run that moves back is a prefix
+// of the audio slots, so it lies in the first stage_rows of them unless it
+// is too long) and zeroes every gridDim.x-th read flag.  Workgroup 0 also
+// checks the first slot past the staging rows; if that one moves back too,
+// it counts the whole run (the shortfall) for the status word.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void stage_moved_back(const LayerDesc* __restrict__ layers, Dims dm,
                                                         const int32_t* __restrict__ idx, const int* __restrict__ eff,
-                                                        Workspace ws) {
+                                                        Workspace ws, int active) {
   using RC = RowCopy<T, D>;
-  const int l = blockIdx.z, g = blockIdx.y, tile = blockIdx.x;
+  const int l = blockIdx.z, g = blockIdx.y;
   const int u = l * dm.Hkv + g;
+  // (rotated by the unit, so that the few workgroups with rows to stage,
+  // the first of each unit, spread over the XCDs)
+  const int x = (int)((blockIdx.x + (unsigned)u) % gridDim.x);
   const int tiles = (int)((dm.max_tokens + kGatherRows - 1) / kGatherRows);
-  if (threadIdx.x == 0) {
-    ws.read_flags[(int64_t)u * tiles + tile] = 0;
-    if (tile == 0) ws.tickets[u * kTicketStride] = 0;
-  }
+  for (int t = x * 256 + (int)threadIdx.x; t < active; t += (int)gridDim.x * 256) ws.read_flags[(int64_t)u * tiles + t] = 0;
+  if (x == 0 && threadIdx.x == 0) ws.tickets[u * kTicketStride] = 0;
   const LayerDesc Ld = layers[l];
   if (!Ld.inplace) return;
   const int Mv = eff[2 * l], M = Mv + eff[2 * l + 1];
-  const int i0 = tile * kGatherRows;
-  if (i0 >= M || i0 + kGatherRows <= Mv) return;
   const int32_t* ig = idx + (int64_t)u * dm.max_tokens;
+  auto moves_back = [&](int i) {
+    const int row = ig[i];
+    return row >= 0 && row < i;
+  };
+  if (x == 0 && Mv + ws.stage_rows < M && moves_back(Mv + ws.stage_rows)) {  // (uniform)
+    int run = ws.stage_rows;
+    for (int i0 = Mv + ws.stage_rows; i0 < M; i0 += 256) {
+      const int i = i0 + (int)threadIdx.x;
+      run += __syncthreads_count(i < M && moves_back(i));
+    }
+    if (threadIdx.x == 0) atomicMax(&ws.ctl[1], run);
+    return;
+  }
+  const int j0 = x * kGatherRows;
+  const int jend = min(ws.stage_rows, M - Mv);
+  if (j0 >= jend) return;
   const T* k = reinterpret_cast<const T*>(Ld.k) + (int64_t)g * Ld.kv_hs;
   const T* v = reinterpret_cast<const T*>(Ld.v) + (int64_t)g * Ld.kv_hs;
   const int64_t stage_len = (int64_t)dm.L * dm.Hkv * ws.stage_rows * D;
@@ -1309,15 +1329,11 @@ __global__ __launch_bounds__(256) void stage_moved_back(const LayerDesc* __restr
   const int sub = threadIdx.x % RC::CPR;
 #pragma unroll
   for (int p = 0; p < RC::NP; ++p) {
-    const int i = i0 + (int)threadIdx.x / RC::CPR + p * RC::RPP;
-    if (i < Mv || i >= M) continue;
+    const int j = j0 + (int)threadIdx.x / RC::CPR + p * RC::RPP;
+    if (j >= jend) continue;
+    const int i = Mv + j;
     const int row = ig[i];
     if (row >= i || row < 0) continue;  // moves to the front or stays
-    const int j = i - Mv;
-    if (j >= ws.stage_rows) {
-      if (sub == 0) atomicMax(&ws.ctl[1], j + 1);
-      continue;
-    }
     const int64_t e = (int64_t)row * Ld.kv_rs + sub * RC::EPC;
     const uint4 kx = gload16(k + e), vx = gload16(v + e);
     *reinterpret_cast<uint4*>(sk + (int64_t)j * D + sub * RC::EPC) = kx;
@@ -1469,7 +1485,8 @@ void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, c
     OMNIMEM_LAUNCH(ws, K_GATHER, st, gather_compact<T, D><<<grid, 256, 0, st>>>(desc, dm, idx, ws.eff, ctl));
   if (inplace > 0) {
     const int units = dm.L * dm.Hkv;
-    OMNIMEM_LAUNCH(ws, K_STAGE, st, stage_moved_back<T, D><<<grid, 256, 0, st>>>(desc, dm, idx, ws.eff, ws));
+    const dim3 gstage((unsigned)max(1, (ws.stage_rows + kGatherRows - 1) / kGatherRows), dm.Hkv, dm.L);
+    OMNIMEM_LAUNCH(ws, K_STAGE, st, stage_moved_back<T, D><<<gstage, 256, 0, st>>>(desc, dm, idx, ws.eff, ws, active));
     OMNIMEM_LAUNCH(ws, K_GATHER_IP, st,
                    gather_inplace<T, D><<<(unsigned)(units * active), 256, 0, st>>>(desc, dm, idx, ws.eff, ws,
                                                                                      units, tiles, active));

@@ -168,6 +168,10 @@ def test_inplace_staging_shortfall_moves_nothing():
     assert torch.equal(step.k[0], k0) and torch.equal(step.v[0], v0) and torch.equal(step.mod[0], m0)
     idx = step.idx[0, :, :350].cpu().numpy()
     assert (np.diff(idx[:, :260], axis=1) > 0).all() and (np.diff(idx[:, 260:], axis=1) > 0).all()
+    # the reported need is the longest run of audio slots whose row lies in front of them
+    slots = np.arange(260, 350)
+    need = max(int(((idx[g, 260:] >= 0) & (idx[g, 260:] < slots)).sum()) for g in range(idx.shape[0]))
+    assert need > 4 and f"needed {need} staging rows" in str(e.value), (need, str(e.value))
     assert step.ctx.omnimem_inplace_status() == 0      # the record was cleared
     # A call that needs no staging rows still runs on the same context.
     bud = torch.tensor([[150, 50]], dtype=torch.int32, device=step.device)
@@ -177,6 +181,32 @@ def test_inplace_staging_shortfall_moves_nothing():
     idx = step.idx[0, :, :200].long()
     for g in range(2):
         assert torch.equal(step.k[0][g, :200], k0[g, idx[g]])
+    step.close()
+
+
+def test_inplace_long_shortfall_is_counted_whole():
+    # A full-size layer whose visual budget exceeds the 3072 visual cache
+    # rows: the kept audio cache rows all land behind their row, a run of
+    # hundreds of slots against 100 staging rows (two staging tiles).  Nothing
+    # moves, and the status reports the whole run.
+    layers = synth.make_workload("qwen7b-layer-6144")
+    step = DeviceStep(layers, 4096, inplace_stage_rows=100)
+    a, s = _scores(step, layers, 8)
+    k0, v0 = step.k[0].clone(), step.v[0].clone()
+    desc = omnimem.make_layer(step.q[0], step.k[0], step.v[0], step.mod[0], step.n_cache[0], step.sm_scale[0], None,
+                              step.k[0], step.v[0])
+    mv, ma = 3900, 900
+    bud = torch.tensor([[mv, ma]], dtype=torch.int32, device=step.device)
+    step.ctx.omnimem_select_compact([desc], a, s, bud, step.idx)
+    torch.cuda.synchronize()
+    with pytest.raises(omnimem.OmnimemError) as e:
+        step.ctx.omnimem_inplace_status()
+    assert e.value.status == omnimem.ERR_CAPACITY
+    assert torch.equal(step.k[0], k0) and torch.equal(step.v[0], v0)
+    idx = step.idx[0, :, mv:mv + ma].cpu().numpy()
+    slots = np.arange(mv, mv + ma)
+    need = max(int(((idx[g] >= 0) & (idx[g] < slots)).sum()) for g in range(idx.shape[0]))
+    assert need > 100 + 256 and f"needed {need} staging rows" in str(e.value), (need, str(e.value))
     step.close()
 
 
