@@ -31,37 +31,37 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
-        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
-        "append_chunk": 235255223, "lse_pass": 604356467, "lse_merge": 19381024, "colsum_pass": 622677118,
-        "head_sum": 21741399, "lists_norms": 181331508, "gram_sym": 816339141, "gram_finish": 6206188,
-        "avba_partials": 6040922, "avba_allocate": 180771, "psi_topk_reg": 20836432, "stage_moved_back": 15204399,
-        "gather_inplace": 417905968
+        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
+        "append_chunk": 235255492, "lse_pass": 604356378, "lse_merge": 19381018, "colsum_pass": 622604979,
+        "head_sum": 21741411, "lists_norms": 181331502, "gram_sym": 816088659, "gram_finish": 6206187,
+        "avba_partials": 6040922, "avba_allocate": 180771, "psi_topk_reg": 20837236,
+        "stage_moved_back": 15224540, "gather_inplace": 417907096,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
-        "lse_pass": 608220340, "lse_merge": 19381194, "colsum_pass": 613970961, "head_sum": 22114178,
-        "lists_norms": 184701193, "gram_sym": 825564684, "gram_finish": 6248350, "avba_partials": 6078432,
-        "avba_allocate": 123709, "psi_topk_reg": 14469367, "gather_compact": 471796909
+        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
+        "lse_pass": 608194360, "lse_merge": 19381199, "colsum_pass": 613584219, "head_sum": 22114162,
+        "lists_norms": 184700662, "gram_sym": 825225593, "gram_finish": 6248349, "avba_partials": 6078432,
+        "avba_allocate": 123709, "psi_topk_reg": 14469363, "gather_compact": 471796838,
     },
     "qwen7b-layer-6144": {
-        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
-        "lse_pass": 31065607, "lse_merge": 1738838, "colsum_pass": 33068992, "head_sum": 1292306,
-        "lists_norms": 6740136, "gram_sym": 14033841, "gram_finish": 245756, "avba_partials": 300160,
-        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889839
+        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
+        "lse_pass": 31045848, "lse_merge": 1738709, "colsum_pass": 33089347, "head_sum": 1292314,
+        "lists_norms": 6740158, "gram_sym": 14033866, "gram_finish": 245756, "avba_partials": 300160,
+        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889835,
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
-        "lse_pass": 31064187, "lse_merge": 1738710, "colsum_pass": 33074063, "head_sum": 1292371,
-        "modality_lists": 65832, "hidden_norms": 44175353, "gram_wide": 188161890, "hidden_finish": 138239,
-        "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 272514, "psi_topk_reg": 218044,
-        "gather_compact": 16889919, "gather_hidden": 58875453
+        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
+        "lse_pass": 31047056, "lse_merge": 1738709, "colsum_pass": 33082506, "head_sum": 1292280,
+        "modality_lists": 65838, "hidden_norms": 44175367, "gram_wide": 188161876, "hidden_finish": 138259,
+        "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 272514, "psi_topk_reg": 220348,
+        "gather_compact": 16889926, "gather_hidden": 58879555,
     },
     "qwen7b-longcache-40960": {
-        "sources_sha256": "c86014ed2e63d9852e2a922ec436b1f3a709fda0273c3fae541c91775dab7ff9",
-        "lse_pass": 5088207845, "lse_merge": 3850239, "colsum_pass": 380773118, "head_sum": 5296172,
-        "lists_norms": 44062563, "gram_sym": 955931456, "gram_finish": 1499112, "avba_partials": 1460429,
-        "avba_allocate": 53470, "topk_hist": 2205441, "topk_bin": 1949072, "topk_emit": 2722502,
-        "gather_compact": 134817184
+        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
+        "lse_pass": 5094183208, "lse_merge": 3850239, "colsum_pass": 380412203, "head_sum": 5296176,
+        "lists_norms": 44062565, "gram_sym": 962458843, "gram_finish": 1499112, "avba_partials": 1460429,
+        "avba_allocate": 53470, "topk_hist": 2190081, "topk_bin": 1949101, "topk_emit": 2738885,
+        "gather_compact": 134817374,
     },
 }
 
