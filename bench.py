@@ -171,7 +171,9 @@ def roof_probe(torch):
     one of them).  Returns MFMA-flop rates as fractions of the bf16 peak:
     MFMA alone, and the per-MFMA mix of the passes (one 32x32x16 bf16 MFMA,
     two exp2, two FMA, two adds) with and without its LDS fragment reads;
-    the mix is the ceiling of a pass that does this work per MFMA."""
+    the mix is the ceiling of a pass that does this work per MFMA.  Also the
+    Gram pass's mix (one MFMA, two cosines: four multiplies, two running
+    maxima, one v_max3; LDS fragments and a barrier per tile)."""
     import ctypes
 
     from paper_2606_07577_amd import build
@@ -205,7 +207,7 @@ def roof_probe(torch):
         res[f"mfma_only_{waves}w"] = blocks * 4 * 4 * 20000 * mfma_flop / (ms / 1e3) / 1e12
         ms = best_ms(1, blocks, 20000)
         res[f"exp2_per_ns_{waves}w"] = blocks * 4 * 64 * 16 * 20000 / (ms * 1e6)
-    for kind, name in ((2, "mix"), (3, "mix_lds"), (4, "mix_lds_barrier")):
+    for kind, name in ((2, "mix"), (3, "mix_lds"), (4, "mix_lds_barrier"), (5, "gram_mix")):
         blocks = cus * 2                        # the passes' occupancy: two 4-wave workgroups per compute unit
         ms = best_ms(kind, blocks, 2500)
         res[name] = blocks * 4 * 32 * 2500 * mfma_flop / (ms / 1e3) / 1e12
@@ -213,9 +215,9 @@ def roof_probe(torch):
     out_d = {"unit": "TFLOP/s of MFMA work", "peak": peak,
              "mfma_only": round(max(res["mfma_only_2w"], res["mfma_only_4w"]), 1),
              "mix": round(res["mix"], 1), "mix_lds": round(res["mix_lds"], 1),
-             "mix_lds_barrier": round(res["mix_lds_barrier"], 1),
+             "mix_lds_barrier": round(res["mix_lds_barrier"], 1), "gram_mix": round(res["gram_mix"], 1),
              "exp2_per_ns": round(max(res["exp2_per_ns_2w"], res["exp2_per_ns_4w"]), 1)}
-    for k in ("mfma_only", "mix", "mix_lds", "mix_lds_barrier"):
+    for k in ("mfma_only", "mix", "mix_lds", "mix_lds_barrier", "gram_mix"):
         out_d[k + "_frac"] = round(out_d[k] / peak, 4)
     return out_d
 
@@ -641,6 +643,8 @@ def main():
         for name in ("lse_pass", "colsum_pass"):
             if name in per_kernel and "frac" in per_kernel[name]:
                 ceiling[name + "_vs_mix"] = round(per_kernel[name]["frac"] / ceiling["mix_frac"], 4)
+        if "gram_sym" in per_kernel and "frac" in per_kernel["gram_sym"]:
+            ceiling["gram_sym_vs_gram_mix"] = round(per_kernel["gram_sym"]["frac"] / ceiling["gram_mix_frac"], 4)
         out["score_pass_ceiling"] = ceiling
     print(json.dumps(out))
 

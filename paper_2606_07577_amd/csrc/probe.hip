@@ -15,6 +15,13 @@
 //                   (one ds_read_b128 per k-step and phase), as in the pass
 //   probe_mix_bar   probe_mix_lds with one workgroup barrier every two
 //                   phases (one per 64-key tile, as in the pass)
+//   probe_gram      the per-MFMA work of the bf16 Gram pass at head_dim 128:
+//                   per phase, 16 MFMAs (two register row blocks, k-step
+//                   fragments of the tile rows read from LDS two k-steps
+//                   ahead) while the 32 products per lane of the other
+//                   accumulator pair become cosines (two multiplies) and
+//                   enter a running row maximum and a column maximum
+//                   (v_max3 over pairs); one barrier every two phases
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -138,24 +145,105 @@ __global__ __launch_bounds__(256, 2) void probe_mix(int iters, float* out, int f
   if (flag) out[blockIdx.x * blockDim.x + threadIdx.x] = lsum[0] + lsum[1] + acc0[0][0] + acc1[1][1];
 }
 
+// v_max_f32 / v_max3_f32 written out, as the Gram pass writes them.
+__device__ inline float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ inline float vmax3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// One phase of the Gram mix: MFMAs into `o` (two register row blocks x NKS
+// k-steps against one tile fragment per k-step) interleaved with the
+// cosines and maxima of the products in `in`, as the Gram pass schedules it.
+__device__ inline void gram_phase(floatx16 (&o)[2], bf16x8 (&a)[2][NKS], const bf16x8* lds, int lane,
+                                  const floatx16 (&in)[2], float invj, float (&iv)[2][16], float (&rmax)[2][16],
+                                  float& cm) {
+  constexpr int NG = 2 * NKS;
+  constexpr int PER = 32 / NG;
+  static_assert(PER == 2, "two products per MFMA");
+  bf16x8 f[NKS];
+  f[0] = lds[lane & 511];
+  f[1] = lds[(64 + lane) & 511];
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int ks = g >> 1, rb = g & 1;
+    if (rb == 0 && ks + 2 < NKS) f[ks + 2] = lds[((ks + 2) * 64 + lane) & 511];
+    pin(a[rb][ks]);
+    o[rb] = mma(a[rb][ks], f[ks], ks ? o[rb] : floatx16{});
+    float c[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = g * PER + i, erb = e >> 4, r = e & 15;
+      c[i] = in[erb][r] * invj * iv[erb][r];
+      rmax[erb][r] = vmax(rmax[erb][r], c[i]);
+      pin(rmax[erb][r]);
+    }
+    cm = vmax3(cm, c[0], c[1]);
+    pin(cm);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+__global__ __launch_bounds__(256, 2) void probe_gram(int iters, float* out, int flag) {
+  __shared__ bf16x8 tile[512];  // 8 KB of tile-row fragments
+  const int lane = threadIdx.x & 63;
+  for (int i = threadIdx.x; i < 512; i += blockDim.x) tile[i] = frag_of(i);
+  __syncthreads();
+  bf16x8 a[2][NKS];
+  float iv[2][16], rmax[2][16];
+#pragma unroll
+  for (int k = 0; k < NKS; ++k) {
+    a[0][k] = frag_of(threadIdx.x + 2 * k);
+    a[1][k] = frag_of(threadIdx.x + 3 * k);
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    iv[0][r] = 1.0f + 0.01f * (float)r;
+    iv[1][r] = 1.0f - 0.01f * (float)r;
+    rmax[0][r] = rmax[1][r] = -1.0f;
+  }
+  floatx16 acc0[2] = {}, acc1[2] = {};
+  const float invj = 0.9f + 0.001f * (float)lane;
+  float cm = -1.0f, cms = 0.0f;
+  for (int it = 0; it < iters; ++it) {
+    gram_phase(acc1, a, tile, lane, acc0, invj, iv, rmax, cm);
+    cms += cm;
+    __syncthreads();  // the pass hands each tile to the workgroup's waves with one barrier
+    gram_phase(acc0, a, tile, lane, acc1, invj, iv, rmax, cm);
+    cms += cm;
+  }
+  float t = cms + acc0[0][0] + acc1[1][1];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) t += rmax[0][r] + rmax[1][r];
+  if (flag) out[blockIdx.x * blockDim.x + threadIdx.x] = t;
+}
+
 }  // namespace
 
 extern "C" {
 
 // Launch probe `kind` (0 MFMA, 1 exp2, 2 mix, 3 mix with LDS fragments, 4 the
-// same with a barrier per tile) on
+// same with a barrier per tile, 5 the Gram mix) on
 // `blocks` workgroups of 256 threads for `iters` iterations on `stream`.
 // Work per launch, per wave: kind 0: 4 * iters MFMAs; kind 1: 16 * iters
-// exp2; kinds 2-4: 32 * iters MFMAs and 64 * iters exp2.  `out` receives
-// nothing unless `flag` is set.  Returns a hipError_t.
+// exp2; kinds 2-4: 32 * iters MFMAs and 64 * iters exp2; kind 5: 32 * iters
+// MFMAs and 64 * iters cosines.  `out` receives nothing unless `flag` is
+// set.  Returns a hipError_t.
 int omnimem_probe_run(int kind, int blocks, int iters, float* out, int flag, hipStream_t stream) {
-  if (blocks < 1 || iters < 1 || kind < 0 || kind > 4) return (int)hipErrorInvalidValue;
+  if (blocks < 1 || iters < 1 || kind < 0 || kind > 5) return (int)hipErrorInvalidValue;
   switch (kind) {
     case 0: probe_mfma<<<blocks, 256, 0, stream>>>(iters, out, flag); break;
     case 1: probe_exp<<<blocks, 256, 0, stream>>>(iters, out, flag); break;
     case 2: probe_mix<false><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
     case 3: probe_mix<true><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
-    default: probe_mix<true, true><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
+    case 4: probe_mix<true, true><<<blocks, 256, 0, stream>>>(iters, out, flag); break;
+    default: probe_gram<<<blocks, 256, 0, stream>>>(iters, out, flag); break;
   }
   return (int)hipGetLastError();
 }
