@@ -221,6 +221,13 @@ __global__ __launch_bounds__(256) void lists_norms(const LayerDesc* __restrict__
     }
   }
   __syncthreads();
+  // Pass p's row sum ends up in every lane of the row's group; lane sub = p
+  // keeps it, so one fp64 square root and division per lane serves all NP
+  // rows of the group (each is a long instruction sequence, paid per wave).
+  static_assert(NP <= LPR, "a lane of the group for every pass");
+  double mine = 0.0;
+  int64_t omine = 0;
+  bool in_mine = false;
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
     const int r = p * RPP + (int)threadIdx.x / LPR;
@@ -244,10 +251,15 @@ __global__ __launch_bounds__(256) void lists_norms(const LayerDesc* __restrict__
     }
 #pragma unroll
     for (int x = LPR / 2; x > 0; x >>= 1) acc += __shfl_xor(acc, x, 64);
-    if (in && sub == 0) {
-      inv[o] = acc > 0.0 ? (float)(1.0 / sqrt(acc)) : 0.0f;
-      best[o] = kNoPartner;  // the Gram pass merges maxima into this
+    if (sub == p) {
+      mine = acc;
+      omine = o;
+      in_mine = in;
     }
+  }
+  if (in_mine) {
+    inv[omine] = mine > 0.0 ? (float)(1.0 / sqrt(mine)) : 0.0f;
+    best[omine] = kNoPartner;  // the Gram pass merges maxima into this
   }
 }
 
