@@ -739,17 +739,25 @@ __global__ void head_sum(const LayerDesc* __restrict__ layers, Dims dm, PassPlan
   if (Ld.cs_th > 0 && tiles > 0) {
     int64_t start = Ld.cs_base;
     for (int bb = 0; bb < b; ++bb) start += cs_row_tiles(Ld.n, Ld.n_cache, Ld.n_chunk, bb, dm.causal);
-    // per query head, all its segment partials requested at once
-    for (int hh = 0; hh < dm.G; ++hh) {
-      const int h = g * dm.G + hh;
-      const int64_t s0 = start + (int64_t)h * Ld.cs_th;
-      const int nseg = plan_seg(pl, s0, s0 + tiles - 1) + 1;
-      const float* p = part + ((((int64_t)l * dm.Hq + h) * dm.kb + b) * kMaxSeg) * kBlockRows + (j - b * kBlockRows);
-      float v[kMaxSeg];
+    // the segment partials of up to kHeadsAtOnce query heads requested at
+    // once, then added in head and segment order
+    constexpr int kHeadsAtOnce = 8;
+    for (int h0 = 0; h0 < dm.G; h0 += kHeadsAtOnce) {
+      float v[kHeadsAtOnce][kMaxSeg];
 #pragma unroll
-      for (int sg = 0; sg < kMaxSeg; ++sg) v[sg] = sg < nseg ? p[sg * kBlockRows] : 0.0f;
+      for (int u = 0; u < kHeadsAtOnce; ++u) {
+        const int h = g * dm.G + min(h0 + u, dm.G - 1);  // (heads past G load nothing)
+        const int64_t s0 = start + (int64_t)h * Ld.cs_th;
+        const int nseg = h0 + u < dm.G ? plan_seg(pl, s0, s0 + tiles - 1) + 1 : 0;
+        const float* p =
+            part + ((((int64_t)l * dm.Hq + h) * dm.kb + b) * kMaxSeg) * kBlockRows + (j - b * kBlockRows);
 #pragma unroll
-      for (int sg = 0; sg < kMaxSeg; ++sg) sum += v[sg];
+        for (int sg = 0; sg < kMaxSeg; ++sg) v[u][sg] = sg < nseg ? p[sg * kBlockRows] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < kHeadsAtOnce; ++u)
+#pragma unroll
+        for (int sg = 0; sg < kMaxSeg; ++sg) sum += v[u][sg];
     }
   }
   a[((int64_t)l * dm.Hkv + g) * dm.max_tokens + j] = sum;
