@@ -44,12 +44,26 @@ __global__ __launch_bounds__(kPartThreads) void avba_partials(const LayerDesc* _
   const float* sg = s + ((int64_t)l * dm.Hkv + g) * dm.max_tokens;
   double acc[kStatSets * 4] = {};
   const int j1 = min(N, (chunk + 1) * kPartRows);
-  for (int j = chunk * kPartRows + threadIdx.x; j < j1; j += blockDim.x) {
-    const int o = mod[j] ? 4 : 0;
-    const double x = ag[j];
+  // the thread's rows (j, j + 256, ...), all requested before the first sum
+  constexpr int kPer = kPartRows / kPartThreads;
+  static_assert(kPer * kPartThreads == kPartRows, "whole rows per thread");
+  float xa[kPer], xs[kPer];
+  int xm[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int j = chunk * kPartRows + u * kPartThreads + (int)threadIdx.x;
+    xa[u] = j < j1 ? ag[j] : 0.0f;
+    xs[u] = j < j1 ? sg[j] : 0.0f;
+    xm[u] = j < j1 ? (int)mod[j] : -1;
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    if (xm[u] < 0) continue;
+    const int o = xm[u] ? 4 : 0;
+    const double x = xa[u];
     acc[o + 0] += x;
     acc[o + 1] += x > 0.0 ? x * log(x) : 0.0;
-    acc[o + 2] += sg[j];
+    acc[o + 2] += xs[u];
     acc[o + 3] += 1.0;
   }
   // all eight sums reduced together: wave shuffles, then one LDS round
