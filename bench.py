@@ -31,37 +31,37 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
-        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
-        "append_chunk": 235255492, "lse_pass": 604356378, "lse_merge": 19381018, "colsum_pass": 622604979,
-        "head_sum": 21741411, "lists_norms": 181331502, "gram_sym": 816088659, "gram_finish": 6206187,
-        "avba_partials": 6040922, "avba_allocate": 180771, "psi_topk_reg": 20837236,
-        "stage_moved_back": 15224540, "gather_inplace": 417907096,
+        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
+        "append_chunk": 235255846, "lse_pass": 604451542, "lse_merge": 19381016, "colsum_pass": 622682255,
+        "head_sum": 21864298, "lists_norms": 181315154, "gram_sym": 816394218, "gram_finish": 6206187,
+        "avba_partials": 6072665, "avba_allocate": 181106, "psi_topk_reg": 20837261,
+        "stage_moved_back": 15224553, "gather_inplace": 417907189,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
-        "lse_pass": 608194360, "lse_merge": 19381199, "colsum_pass": 613584219, "head_sum": 22114162,
-        "lists_norms": 184700662, "gram_sym": 825225593, "gram_finish": 6248349, "avba_partials": 6078432,
-        "avba_allocate": 123709, "psi_topk_reg": 14469363, "gather_compact": 471796838,
+        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
+        "lse_pass": 608579822, "lse_merge": 19381162, "colsum_pass": 613599376, "head_sum": 22237031,
+        "lists_norms": 184687152, "gram_sym": 824156891, "gram_finish": 6248350, "avba_partials": 6110175,
+        "avba_allocate": 123965, "psi_topk_reg": 14469369, "gather_compact": 471795467,
     },
     "qwen7b-layer-6144": {
-        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
-        "lse_pass": 31045848, "lse_merge": 1738709, "colsum_pass": 33089347, "head_sum": 1292314,
-        "lists_norms": 6740158, "gram_sym": 14033866, "gram_finish": 245756, "avba_partials": 300160,
-        "avba_allocate": 36063, "psi_topk_reg": 665024, "gather_compact": 16889835,
+        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
+        "lse_pass": 31196227, "lse_merge": 1738710, "colsum_pass": 32973636, "head_sum": 1460231,
+        "lists_norms": 6721682, "gram_sym": 14042058, "gram_finish": 245756, "avba_partials": 331903,
+        "avba_allocate": 36191, "psi_topk_reg": 665024, "gather_compact": 16889853,
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
-        "lse_pass": 31047056, "lse_merge": 1738709, "colsum_pass": 33082506, "head_sum": 1292280,
-        "modality_lists": 65838, "hidden_norms": 44175367, "gram_wide": 188161876, "hidden_finish": 138259,
-        "avba_partials": 300160, "avba_allocate": 36063, "layer_inputs": 272514, "psi_topk_reg": 220348,
-        "gather_compact": 16889926, "gather_hidden": 58879555,
+        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
+        "lse_pass": 31197464, "lse_merge": 1738710, "colsum_pass": 32975126, "head_sum": 1460208,
+        "modality_lists": 65838, "hidden_norms": 44175368, "gram_wide": 188161881, "hidden_finish": 138262,
+        "avba_partials": 331903, "avba_allocate": 36191, "layer_inputs": 272514, "psi_topk_reg": 220348,
+        "gather_compact": 16890009, "gather_hidden": 58879559,
     },
     "qwen7b-longcache-40960": {
-        "sources_sha256": "d9b05f1ac80359c4d2a2c40d2bd2ce58ec2e9f351a232b950de290fff35b662d",
-        "lse_pass": 5094183208, "lse_merge": 3850239, "colsum_pass": 380412203, "head_sum": 5296176,
-        "lists_norms": 44062565, "gram_sym": 962458843, "gram_finish": 1499112, "avba_partials": 1460429,
-        "avba_allocate": 53470, "topk_hist": 2190081, "topk_bin": 1949101, "topk_emit": 2738885,
-        "gather_compact": 134817374,
+        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
+        "lse_pass": 5085325129, "lse_merge": 3850239, "colsum_pass": 380154079, "head_sum": 5419053,
+        "lists_norms": 44044135, "gram_sym": 953912024, "gram_finish": 1499112, "avba_partials": 1492172,
+        "avba_allocate": 53598, "topk_hist": 2190081, "topk_bin": 1949118, "topk_emit": 2738885,
+        "gather_compact": 134818712,
     },
 }
 
