@@ -1165,13 +1165,16 @@ __global__ __launch_bounds__(kTkThreads) void topk_emit(const LayerDesc* __restr
   }
 }
 
+constexpr int kCompactRows = 32;  // output rows per workgroup of the out-of-place gather
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void gather_compact(const LayerDesc* __restrict__ layers, Dims dm,
                                                       const int32_t* __restrict__ idx, const int* __restrict__ eff,
                                                       const int* __restrict__ ctl) {
   constexpr int CPR = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
   constexpr int RPP = 256 / CPR;                // rows per pass
-  constexpr int ROWS = 64;                      // rows per workgroup
+  constexpr int ROWS = kCompactRows;            // rows per workgroup
+  static_assert(ROWS % RPP == 0 && ROWS <= 256, "whole passes; one modality byte per thread");
   const int l = blockIdx.z, g = blockIdx.y;
   const LayerDesc Ld = layers[l];
   if (Ld.inplace || (ctl && ctl[1] != 0)) return;  // in-place layer, or a call that moves nothing
@@ -1483,10 +1486,11 @@ void launch_gather(const Dims& dm, const LayerDesc* desc, const Workspace& ws, c
                    int max_n, hipStream_t st) {
   const int tiles = (int)((dm.max_tokens + kGatherRows - 1) / kGatherRows);
   const int active = (max_n + kGatherRows - 1) / kGatherRows;
-  const dim3 grid((unsigned)active, dm.Hkv, dm.L);
   const int* ctl = ws.stage_rows > 0 ? ws.ctl : nullptr;
-  if (inplace < 2)
+  if (inplace < 2) {
+    const dim3 grid((unsigned)((max_n + kCompactRows - 1) / kCompactRows), dm.Hkv, dm.L);
     OMNIMEM_LAUNCH(ws, K_GATHER, st, gather_compact<T, D><<<grid, 256, 0, st>>>(desc, dm, idx, ws.eff, ctl));
+  }
   if (inplace > 0) {
     const int units = dm.L * dm.Hkv;
     const dim3 gstage((unsigned)max(1, (ws.stage_rows + kGatherRows - 1) / kGatherRows), dm.Hkv, dm.L);
