@@ -529,7 +529,7 @@ omnimem_status omnimem_create(const omnimem_config* cfg, omnimem_ctx** out) {
        ((e = dalloc(ctx, reinterpret_cast<char**>(&ws.stage),
                     2 * L * Hkv * (size_t)c.inplace_stage_rows * (size_t)c.head_dim * elt)) != hipSuccess ||
         (e = dalloc(ctx, &ws.slot_of, L * Hkv * T)) != hipSuccess ||
-        (e = dalloc(ctx, &ws.read_flags, L * Hkv * (size_t)((T + 63) / 64))) != hipSuccess ||
+        (e = dalloc(ctx, &ws.read_flags, L * Hkv * (size_t)((T + kGatherRows - 1) / kGatherRows))) != hipSuccess ||
         (e = dalloc(ctx, &ws.tickets, L * Hkv * 32)) != hipSuccess))) {
     omnimem_destroy(ctx);
     return fail(nullptr, OMNIMEM_ERR_HIP, "workspace allocation: %s", hipGetErrorString(e));

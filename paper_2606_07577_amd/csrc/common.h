@@ -76,6 +76,7 @@ struct Dims {
 constexpr int kScoreBlock = 256;  // rows a workgroup keeps in registers
 constexpr int kScoreTile = 64;    // rows per streamed tile
 constexpr int kMaxSeg = 4;
+constexpr int kGatherRows = 64;   // slots per tile (and workgroup) of the in-place gather and its staging
 struct PassPlan {
   int64_t W;  // tiles
   int P;      // workgroups
@@ -282,7 +283,7 @@ struct Workspace {
   int stage_rows;         // staging rows per (layer, KV head)
   void* stage;            // [2][L][Hkv][stage_rows][d] staged K, then V rows
   int* slot_of;           // [L][Hkv][max_tokens] slot that reads row j (-1: dropped)
-  int* read_flags;        // [L][Hkv][tiles] 1 once a 64-slot tile has read its rows
+  int* read_flags;        // [L][Hkv][tiles] 1 once a kGatherRows-slot tile has read its rows
   int* ctl;               // [1] this call's staging need beyond the reserve (0: none), [2] largest need
                           // and [3] wait time-outs since the last query ([0] unused)
   int* tickets;           // [L * Hkv][32] tile tickets of the in-place gather, one 128-byte line each

@@ -1261,7 +1261,7 @@ __global__ __launch_bounds__(256) void gather_hidden(const LayerDesc* __restrict
 // fewer than M_v visual rows in front of it (M_v + j - p_j does not grow
 // with j, so these are the first ones).  That run is copied out to the
 // staging rows first (stage_moved_back); every other slot is then filled
-// in one pass in which the 64-slot tile t writes its rows only after each
+// in one pass in which the kGatherRows-slot tile t writes its rows only after each
 // earlier tile that reads one of those rows has loaded it (flags set after
 // the loads).  The workgroups of one (layer, KV head) take its tiles as
 // tickets from a counter of their own, in their order of starting, and the
@@ -1270,7 +1270,6 @@ __global__ __launch_bounds__(256) void gather_hidden(const LayerDesc* __restrict
 // counter per (layer, KV head), each on a cache line of its own, keeps the
 // ticket atomics from queueing on one address.
 // ---------------------------------------------------------------------------
-constexpr int kGatherRows = 64;      // slots per workgroup of the gathers
 constexpr int kSpinLimit = 1 << 22;  // polls before a wait gives up (never reached when the order holds)
 constexpr int kTicketStride = 32;    // ints between two ticket counters (one 128-byte line each)
 
@@ -1281,14 +1280,16 @@ struct RowCopy {
   static constexpr int CPR = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
   static constexpr int RPP = 256 / CPR;                // rows per pass
   static constexpr int NP = kGatherRows / RPP;         // passes
+  static_assert(NP >= 1 && NP * RPP == kGatherRows, "whole passes of rows");
   static constexpr int EPC = 16 / (int)sizeof(T);
 };
 
 // Zero the read flags and ticket counters, and stage the slots that take a
-// row in front of them.  Grid: (ceil(stage_rows / 64), H_kv, L); tile x
-// stages audio slots M_v + 64x .. + 63 (the run that moves back is a prefix
-// of the audio slots, so it lies in the first stage_rows of them unless it
-// is too long) and zeroes every gridDim.x-th read flag.  Workgroup 0 also
+// row in front of them.  Grid: (ceil(stage_rows / kGatherRows), H_kv, L);
+// tile x stages the kGatherRows audio slots from M_v + kGatherRows x (the
+// run that moves back is a prefix of the audio slots, so it lies in the
+// first stage_rows of them unless it is too long) and zeroes every
+// gridDim.x-th read flag.  Workgroup 0 also
 // checks the first slot past the staging rows; if that one moves back too,
 // it counts the whole run (the shortfall) for the status word.
 template <typename T, int D>
