@@ -31,37 +31,37 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
-        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
-        "append_chunk": 235255846, "lse_pass": 604451542, "lse_merge": 19381016, "colsum_pass": 622682255,
-        "head_sum": 21864298, "lists_norms": 181315154, "gram_sym": 816394218, "gram_finish": 6206187,
-        "avba_partials": 6072665, "avba_allocate": 181106, "psi_topk_reg": 20837261,
-        "stage_moved_back": 15224553, "gather_inplace": 417907189,
+        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
+        "append_chunk": 235384765, "lse_pass": 604420165, "lse_merge": 19380995, "colsum_pass": 622653050,
+        "head_sum": 21864259, "lists_norms": 181313766, "gram_sym": 816681520, "gram_finish": 6206180,
+        "avba_partials": 6072654, "avba_allocate": 181106, "psi_topk_reg": 20837219,
+        "stage_moved_back": 15224528, "gather_inplace": 417904406,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
-        "lse_pass": 608579822, "lse_merge": 19381162, "colsum_pass": 613599376, "head_sum": 22237031,
-        "lists_norms": 184687152, "gram_sym": 824156891, "gram_finish": 6248350, "avba_partials": 6110175,
-        "avba_allocate": 123965, "psi_topk_reg": 14469369, "gather_compact": 471795467,
+        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
+        "lse_pass": 608420332, "lse_merge": 19381809, "colsum_pass": 613441828, "head_sum": 22237023,
+        "lists_norms": 184685265, "gram_sym": 822364608, "gram_finish": 6248343, "avba_partials": 6110164,
+        "avba_allocate": 123964, "psi_topk_reg": 14469365, "gather_compact": 471725701,
     },
     "qwen7b-layer-6144": {
-        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
-        "lse_pass": 31196227, "lse_merge": 1738710, "colsum_pass": 32973636, "head_sum": 1460231,
-        "lists_norms": 6721682, "gram_sym": 14042058, "gram_finish": 245756, "avba_partials": 331903,
-        "avba_allocate": 36191, "psi_topk_reg": 665024, "gather_compact": 16889853,
+        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
+        "lse_pass": 31151882, "lse_merge": 1738835, "colsum_pass": 32956155, "head_sum": 1460183,
+        "lists_norms": 6721692, "gram_sym": 14042051, "gram_finish": 245756, "avba_partials": 331903,
+        "avba_allocate": 36191, "psi_topk_reg": 665023, "gather_compact": 16865199,
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
-        "lse_pass": 31197464, "lse_merge": 1738710, "colsum_pass": 32975126, "head_sum": 1460208,
-        "modality_lists": 65838, "hidden_norms": 44175368, "gram_wide": 188161881, "hidden_finish": 138262,
-        "avba_partials": 331903, "avba_allocate": 36191, "layer_inputs": 272514, "psi_topk_reg": 220348,
-        "gather_compact": 16890009, "gather_hidden": 58879559,
+        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
+        "lse_pass": 31151666, "lse_merge": 1738707, "colsum_pass": 32953211, "head_sum": 1460229,
+        "modality_lists": 65832, "hidden_norms": 44175244, "gram_wide": 188161532, "hidden_finish": 138239,
+        "avba_partials": 331903, "avba_allocate": 36191, "layer_inputs": 272514, "psi_topk_reg": 220347,
+        "gather_compact": 16865316, "gather_hidden": 58879430,
     },
     "qwen7b-longcache-40960": {
-        "sources_sha256": "89e62b6864723746ae5356865c9710ce5e7e3822da5aa694ee2ccac13ef6c7ca",
-        "lse_pass": 5085325129, "lse_merge": 3850239, "colsum_pass": 380154079, "head_sum": 5419053,
-        "lists_norms": 44044135, "gram_sym": 953912024, "gram_finish": 1499112, "avba_partials": 1492172,
-        "avba_allocate": 53598, "topk_hist": 2190081, "topk_bin": 1949118, "topk_emit": 2738885,
-        "gather_compact": 134818712,
+        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
+        "lse_pass": 5089254032, "lse_merge": 3850234, "colsum_pass": 380593524, "head_sum": 5419044,
+        "lists_norms": 44044040, "gram_sym": 954667961, "gram_finish": 1499111, "avba_partials": 1492170,
+        "avba_allocate": 53598, "topk_hist": 2190078, "topk_bin": 1949117, "topk_emit": 2738882,
+        "gather_compact": 134765416,
     },
 }
 
