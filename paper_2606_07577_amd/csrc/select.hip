@@ -456,7 +456,8 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk_reg(const LayerDesc* __r
                                                             int* __restrict__ slot_of, int* __restrict__ ctl) {
   __shared__ int hist[2][kBins];
   __shared__ int wsum[1][kSelWaves];
-  __shared__ int s_bin, s_need, s_cnt;
+  __shared__ int s_bin, s_need, s_cnt, s_lcnt;
+  __shared__ uint32_t s_thr;
   __shared__ int wt_mem[kSelWaves], wt_eq[kSelWaves], wt_sel[kSelWaves];
   __shared__ uint32_t wmin[kSelWaves], wmax[kSelWaves];
   const int mu = blockIdx.x, g = blockIdx.y, l = blockIdx.z;
@@ -486,6 +487,7 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk_reg(const LayerDesc* __r
 #pragma unroll
   for (int i = 0; i < kRegSteps; ++i) mv[i] = gload<uint8_t>(mod + max(0, min(row0 + 64 * i, N - 1)));
   for (int i = threadIdx.x; i < kBins; i += kSelThreads) hist[0][i] = 0;
+  if (threadIdx.x == 0) s_lcnt = 0;
   // keys of the member rows, their count and range
   bool mb[kRegSteps];
   uint32_t kk[kRegSteps];
@@ -534,7 +536,7 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk_reg(const LayerDesc* __r
     const uint32_t low = width < 32 ? (1u << width) - 1u : 0xFFFFFFFFu;
     uint32_t prefix = kmin & ~low, mask = ~low;
     int need = M, cnt = K, buf = 0;
-    bool whole = false;
+    bool whole = false, ranked = false;
     for (int top = width; top > 0 && !whole;) {
       const int shift = max(0, top - kDigit);
       const uint32_t dmask = (1u << (top - shift)) - 1u;
@@ -568,8 +570,49 @@ __global__ __launch_bounds__(kSelThreads) void psi_topk_reg(const LayerDesc* __r
       top = shift;
       buf ^= 1;
       __syncthreads();  // every thread has read s_bin, s_need, s_cnt
+      if (!whole && top > 0 && cnt <= kListMax) {
+        // Few keys left in the threshold's bin: collect them into the next
+        // digit's (unused) histogram and rank each against the others, four
+        // threads per key, instead of further digits.  The key with fewer
+        // than `need` keys strictly above it and at least `need` counting
+        // its equals is the threshold.
+        int* cand = hist[buf];
+#pragma unroll
+        for (int i = 0; i < kRegSteps; ++i) {
+          const bool m = mb[i] & ((kk[i] & mask) == prefix);
+          const unsigned long long b = __ballot(m);
+          int base = 0;
+          if (lane == 0 && b) base = atomicAdd(&s_lcnt, __popcll(b));
+          base = __shfl(base, 0, 64);
+          if (m) cand[base + __popcll(b & lt)] = (int)kk[i];
+        }
+        __syncthreads();
+        static_assert(4 * kListMax <= kSelThreads, "four threads per candidate");
+        const int ci = (int)threadIdx.x >> 2, part = (int)threadIdx.x & 3;
+        const uint32_t c = ci < cnt ? (uint32_t)cand[ci] : 0u;
+        int gt = 0, eq = 0;
+        for (int u = part; u < cnt; u += 4) {
+          const uint32_t x = (uint32_t)cand[u];
+          gt += x > c ? 1 : 0;
+          eq += x == c ? 1 : 0;
+        }
+        gt += __shfl_xor(gt, 1, 64);
+        eq += __shfl_xor(eq, 1, 64);
+        gt += __shfl_xor(gt, 2, 64);
+        eq += __shfl_xor(eq, 2, 64);
+        // every candidate equal to the threshold writes the same values
+        if (ci < cnt && part == 0 && gt < need && need <= gt + eq) { s_thr = c; s_need = need - gt; s_cnt = eq; }
+        __syncthreads();
+        thr = (uint32_t)uniform((int)s_thr);
+        take_eq = uniform(s_need);
+        n_eq = uniform(s_cnt);
+        ranked = true;
+        break;
+      }
     }
-    if (whole) {
+    if (ranked) {
+      // thr, take_eq and n_eq set by the ranking
+    } else if (whole) {
       thr = prefix - 1u;  // the keys from prefix up: the whole bin and every bin above it
     } else {
       thr = prefix;       // every bit resolved: the threshold key itself
