@@ -31,37 +31,37 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
     "common.h", "api.hip", "score.hip", "redundancy.hip", "allocate.hip", "select.hip")]
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
-        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
-        "append_chunk": 235384765, "lse_pass": 604420165, "lse_merge": 19380995, "colsum_pass": 622653050,
-        "head_sum": 21864259, "lists_norms": 181313766, "gram_sym": 816681520, "gram_finish": 6206180,
-        "avba_partials": 6072654, "avba_allocate": 181106, "psi_topk_reg": 20837219,
-        "stage_moved_back": 15224528, "gather_inplace": 417904406,
+        "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
+        "append_chunk": 235384574, "lse_pass": 604409478, "lse_merge": 19381029, "colsum_pass": 622708577,
+        "head_sum": 21864327, "lists_norms": 181314043, "gram_sym": 816754841, "gram_finish": 6206187,
+        "avba_partials": 6072666, "avba_allocate": 181106, "psi_topk_reg": 20871094,
+        "stage_moved_back": 15224542, "gather_inplace": 417907944,
     },
     "qwen7b-28layer-6144": {
-        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
-        "lse_pass": 608420332, "lse_merge": 19381809, "colsum_pass": 613441828, "head_sum": 22237023,
-        "lists_norms": 184685265, "gram_sym": 822364608, "gram_finish": 6248343, "avba_partials": 6110164,
-        "avba_allocate": 123964, "psi_topk_reg": 14469365, "gather_compact": 471725701,
+        "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
+        "lse_pass": 608236263, "lse_merge": 19381182, "colsum_pass": 613598545, "head_sum": 22237024,
+        "lists_norms": 184685801, "gram_sym": 823377808, "gram_finish": 6248350, "avba_partials": 6110176,
+        "avba_allocate": 123965, "psi_topk_reg": 14505233, "gather_compact": 471744760,
     },
     "qwen7b-layer-6144": {
-        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
-        "lse_pass": 31151882, "lse_merge": 1738835, "colsum_pass": 32956155, "head_sum": 1460183,
-        "lists_norms": 6721692, "gram_sym": 14042051, "gram_finish": 245756, "avba_partials": 331903,
-        "avba_allocate": 36191, "psi_topk_reg": 665023, "gather_compact": 16865199,
+        "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
+        "lse_pass": 31054550, "lse_merge": 1738778, "colsum_pass": 33071890, "head_sum": 1460231,
+        "lists_norms": 6721683, "gram_sym": 14042020, "gram_finish": 245756, "avba_partials": 331903,
+        "avba_allocate": 36191, "psi_topk_reg": 697023, "gather_compact": 16881677,
     },
     "qwen7b-layer-6144-hidden": {
-        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
-        "lse_pass": 31151666, "lse_merge": 1738707, "colsum_pass": 32953211, "head_sum": 1460229,
-        "modality_lists": 65832, "hidden_norms": 44175244, "gram_wide": 188161532, "hidden_finish": 138239,
-        "avba_partials": 331903, "avba_allocate": 36191, "layer_inputs": 272514, "psi_topk_reg": 220347,
-        "gather_compact": 16865316, "gather_hidden": 58879430,
+        "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
+        "lse_pass": 31055949, "lse_merge": 1738710, "colsum_pass": 33073676, "head_sum": 1460362,
+        "modality_lists": 65832, "hidden_norms": 44175380, "gram_wide": 188161921, "hidden_finish": 138239,
+        "avba_partials": 331903, "avba_allocate": 36191, "layer_inputs": 272514, "psi_topk_reg": 227003,
+        "gather_compact": 16881674, "gather_hidden": 58879388,
     },
     "qwen7b-longcache-40960": {
-        "sources_sha256": "0f052fae6179b412348843b6cea5f00d5e58c7505dd654677c08b1a25907d41b",
-        "lse_pass": 5089254032, "lse_merge": 3850234, "colsum_pass": 380593524, "head_sum": 5419044,
-        "lists_norms": 44044040, "gram_sym": 954667961, "gram_finish": 1499111, "avba_partials": 1492170,
-        "avba_allocate": 53598, "topk_hist": 2190078, "topk_bin": 1949117, "topk_emit": 2738882,
-        "gather_compact": 134765416,
+        "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
+        "lse_pass": 5087891386, "lse_merge": 3850240, "colsum_pass": 379964935, "head_sum": 5419044,
+        "lists_norms": 44044149, "gram_sym": 946629536, "gram_finish": 1499112, "avba_partials": 1492173,
+        "avba_allocate": 53599, "topk_hist": 2205441, "topk_bin": 1948936, "topk_emit": 2727622,
+        "gather_compact": 134783860,
     },
 }
 
