@@ -1304,8 +1304,8 @@ __global__ __launch_bounds__(256) void gather_hidden(const LayerDesc* __restrict
 // fewer than M_v visual rows in front of it (M_v + j - p_j does not grow
 // with j, so these are the first ones).  That run is copied out to the
 // staging rows first (stage_moved_back); every other slot is then filled
-// in one pass in which the kGatherRows-slot tile t writes its rows only after each
-// earlier tile that reads one of those rows has loaded it (flags set after
+// in one pass in which tile t (kGatherRows slots) writes its rows only after
+// each earlier tile that reads one of those rows has loaded it (flags set after
 // the loads).  The workgroups of one (layer, KV head) take its tiles as
 // tickets from a counter of their own, in their order of starting, and the
 // wait of a tile is only on tiles of the same (layer, KV head) with smaller
@@ -1332,9 +1332,9 @@ struct RowCopy {
 // tile x stages the kGatherRows audio slots from M_v + kGatherRows x (the
 // run that moves back is a prefix of the audio slots, so it lies in the
 // first stage_rows of them unless it is too long) and zeroes every
-// gridDim.x-th read flag.  Workgroup 0 also
-// checks the first slot past the staging rows; if that one moves back too,
-// it counts the whole run (the shortfall) for the status word.
+// gridDim.x-th read flag.  The workgroup of tile 0 also checks the first
+// slot past the staging rows; if that one moves back too, it counts the
+// whole run (the shortfall) for the status word.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void stage_moved_back(const LayerDesc* __restrict__ layers, Dims dm,
                                                         const int32_t* __restrict__ idx, const int* __restrict__ eff,
