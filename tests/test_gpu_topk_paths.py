@@ -14,7 +14,10 @@ to one workgroup), plus a, s built to stress the ranking: psi quantised to
 a few values (ties across slices), one psi for every row (the threshold
 bin's candidates exceed what LDS holds), and zero and NaN scores; budgets
 of 0, 1, all rows, beyond the rows and beyond the output capacity;
-layer-shared selection and compaction in place.
+layer-shared selection and compaction in place.  With the "half" budgets
+most segments of the 6144-token and ragged layers end the register path's
+select by ranking a threshold bin of at most 256 keys directly, with equal
+keys among them in the quantised case.
 """
 import numpy as np
 import pytest
