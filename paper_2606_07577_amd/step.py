@@ -190,23 +190,28 @@ class StreamRunner:
         self._layers = (om.Layer * n_layers)()
         self._chunks = (om.Chunk * n_layers)()
         self._budget_ready = torch.cuda.Event()
+        self._pending, self._pending_stream = False, None   # a pushed step whose budgets are unread
         self.timing = timing       # per step: events before the append, before score, after select_compact
         self.events = []
 
     # buffers ------------------------------------------------------------
     def cache_k(self, l):
         """Device view of layer l's kept keys [H_kv, n_cache, d]."""
+        self.finish()
         return self.kbuf[self.cur][l][:, : self.n_cache[l]]
 
     def cache_v(self, l):
+        self.finish()
         return self.vbuf[self.cur][l][:, : self.n_cache[l]]
 
     def cache_modality(self, l):
+        self.finish()
         return self.mbuf[self.cur][l][: self.n_cache[l]]
 
     def set_cache(self, l, k, v, m_v, m_a):
         """Replace layer l's retained cache: k, v [H_kv, m_v + m_a, d] (host or
         device), visual rows first."""
+        self.finish()
         m = int(m_v) + int(m_a)
         if m > self.cache_cap:
             raise ValueError(f"cache of {m} rows exceeds the capacity {self.cache_cap}")
@@ -218,11 +223,12 @@ class StreamRunner:
         self.n_cache[l] = m
 
     # one step ----------------------------------------------------------
-    def _describe(self, chunk, qs):
-        """Fill the persistent descriptor arrays for this step's working sets."""
-        other = self.cur if self.in_place else 1 - self.cur
+    def _describe(self, chunk, qs, cur):
+        """Fill the persistent descriptor arrays for a step's working sets in
+        buffer set `cur`, all but the kept-row counts (_set_cache_rows)."""
+        other = cur if self.in_place else 1 - cur
         for l, ch in enumerate(chunk):
-            kb, vb, mb = self.kbuf[self.cur][l], self.vbuf[self.cur][l], self.mbuf[self.cur][l]
+            kb, vb, mb = self.kbuf[cur][l], self.vbuf[cur][l], self.mbuf[cur][l]
             ko, vo, mo = self.kbuf[other][l], self.vbuf[other][l], self.mbuf[other][l]
             lay = self._layers[l]
             q = qs[l]
@@ -230,7 +236,7 @@ class StreamRunner:
             lay.k, lay.v = kb.data_ptr(), vb.data_ptr()
             lay.kv_head_stride, lay.kv_row_stride = kb.stride(0), kb.stride(1)
             lay.modality = mb.data_ptr()
-            lay.n_cache, lay.n_chunk = self.n_cache[l], self.C
+            lay.n_chunk = self.C
             lay.sm_scale = float(ch["sm_scale"])
             lay.k_out, lay.v_out = ko.data_ptr(), vo.data_ptr()
             lay.out_head_stride, lay.out_row_stride = ko.stride(0), ko.stride(1)
@@ -240,6 +246,10 @@ class StreamRunner:
             ck, cv, cm = ch["k"], ch["v"], ch["modality"]
             c.k, c.v, c.modality = ck.data_ptr(), cv.data_ptr(), cm.data_ptr()
             c.head_stride, c.row_stride, c.n_rows = ck.stride(0), ck.stride(1), ck.shape[1]
+
+    def _set_cache_rows(self):
+        for l in range(self.L):
+            self._layers[l].n_cache = self.n_cache[l]
 
     def _on_device(self, chunk):
         dev, td = self.device, self.tdtype
@@ -253,15 +263,21 @@ class StreamRunner:
             out.append(x)
         return out
 
-    def push(self, chunk, stream=None):
+    def push(self, chunk, stream=None, wait=True):
         """Append one chunk (list of per-layer dicts from synth.StreamSource:
         q [H_q, C, d], k, v [H_kv, C, d], modality [C], sm_scale) and run the
-        step.  Returns the budgets [L, 2] as a host array; the compaction may
-        still be running on the stream when it returns."""
+        step.  With wait, returns the budgets [L, 2] as a host array (the
+        compaction may still be running on the stream).  Without, returns
+        None at once: the step's budgets are read by the next push (after it
+        has described its chunk, so the host's work overlaps the GPU's) or
+        by finish()."""
         stream = stream if stream is not None else torch.cuda.current_stream()
         chunk = self._on_device(chunk)
+        cur = self.cur if self.in_place or not self._pending else 1 - self.cur
+        self._describe(chunk, [ch["q"] for ch in chunk], cur)
+        self.finish()              # the previous step's budgets give this step's kept rows
         self._chunk_refs = chunk   # keep the inputs alive while the stream uses them
-        self._describe(chunk, [ch["q"] for ch in chunk])
+        self._set_cache_rows()
         ctx, lays = self.ctx, self._layers
         ev = None
         if self.timing:
@@ -293,10 +309,20 @@ class StreamRunner:
             self.events.append(ev)
         for l in range(self.L):
             self.tokens += self.n_cache[l] + self.C
+        self._pending, self._pending_stream = True, stream
+        return self.finish() if wait else None
+
+    def finish(self):
+        """Wait for the last pushed step's budgets and take its kept-row
+        counts as the caches' sizes; returns the budgets [L, 2] (None when no
+        step is pending)."""
+        if not self._pending:
+            return None
+        self._pending = False
         self._budget_ready.synchronize()
         budgets = self.budgets_host.numpy().copy()
         if self.in_place and int(budgets[:, 1].max()) > self.stage_rows:
-            self._check_staging(stream)
+            self._check_staging(self._pending_stream)
         for l in range(self.L):
             self.n_cache[l] = int(budgets[l, 0]) + int(budgets[l, 1])
         if not self.in_place:
@@ -341,9 +367,11 @@ class StreamRunner:
 
     def freeze_budgets(self, stream=None):
         """Layer budgets from the steps calibrated so far; later steps split them."""
+        self.finish()
         self.ctx.omnimem_calibration_budgets(self.total_budget, self.layer_budgets, stream)
         self.calibrating = False
         self.fixed = True
 
     def close(self):
+        self.finish()
         self.ctx.close()

@@ -330,6 +330,32 @@ def test_stream_in_place_equals_out_of_place(name, chunks, stage_rows):
     oop.close()
 
 
+@pytest.mark.parametrize("in_place,stage_rows", [(True, None), (True, 1), (False, None)])
+def test_stream_without_waiting_equals_waiting(in_place, stage_rows):
+    # push(wait=False) reads a step's budgets only when the next chunk has
+    # been described (or at finish()): the same steps, the same caches.
+    src = synth.StreamSource("small-stream", backend="torch")
+    waiting = _runner(src, keep_working_set=False, in_place=in_place, stage_rows=stage_rows)
+    pipelined = _runner(src, keep_working_set=False, in_place=in_place, stage_rows=stage_rows)
+    L = src.spec["n_layers"]
+    chunks = [src.chunk(t) for t in range(10)]
+    for t, chunk in enumerate(chunks):
+        b = waiting.push(chunk)
+        assert pipelined.push(chunk, wait=False) is None
+        if t == 4:   # finish() gives the step's budgets
+            np.testing.assert_array_equal(pipelined.finish(), b)
+            _same_caches(waiting, pipelined, L)
+        if t == 7:   # so does a read of a cache
+            pipelined.cache_k(0)
+            _same_caches(waiting, pipelined, L)
+    np.testing.assert_array_equal(pipelined.finish(), waiting.budgets_host.numpy())
+    assert pipelined.finish() is None
+    _same_caches(waiting, pipelined, L)
+    assert (pipelined.steps, pipelined.tokens, pipelined.fallbacks) == (waiting.steps, waiting.tokens, waiting.fallbacks)
+    waiting.close()
+    pipelined.close()
+
+
 def test_small_stream_with_offline_budgets():
     # Offline budgets (end of Sec. 3.2; reading R21) on a stream: the first
     # four chunks calibrate (their steps allocate online), the layer budgets
