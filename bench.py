@@ -32,36 +32,36 @@ KERNEL_SOURCES = ["include/omnimem.h"] + [f"paper_2606_07577_amd/csrc/{f}" for f
 MEASURED_TRAFFIC = {
     "qwen7b-stream-64x28": {
         "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
-        "append_chunk": 235384574, "lse_pass": 604409478, "lse_merge": 19381029, "colsum_pass": 622708577,
-        "head_sum": 21864327, "lists_norms": 181314043, "gram_sym": 816754841, "gram_finish": 6206187,
-        "avba_partials": 6072666, "avba_allocate": 181106, "psi_topk_reg": 20871094,
-        "stage_moved_back": 15224542, "gather_inplace": 417907944,
+        "append_chunk": 235384164, "lse_pass": 604350999, "lse_merge": 19381020, "colsum_pass": 622659771,
+        "head_sum": 21864299, "lists_norms": 181314004, "gram_sym": 816413190, "gram_finish": 6206188,
+        "avba_partials": 6072666, "avba_allocate": 181106, "psi_topk_reg": 20871092,
+        "stage_moved_back": 15224527, "gather_inplace": 417904305,
     },
     "qwen7b-28layer-6144": {
         "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
-        "lse_pass": 608236263, "lse_merge": 19381182, "colsum_pass": 613598545, "head_sum": 22237024,
-        "lists_norms": 184685801, "gram_sym": 823377808, "gram_finish": 6248350, "avba_partials": 6110176,
-        "avba_allocate": 123965, "psi_topk_reg": 14505233, "gather_compact": 471744760,
+        "lse_pass": 608507806, "lse_merge": 19381186, "colsum_pass": 613571541, "head_sum": 22237014,
+        "lists_norms": 184685541, "gram_sym": 823118569, "gram_finish": 6248350, "avba_partials": 6110176,
+        "avba_allocate": 123965, "psi_topk_reg": 14505207, "gather_compact": 471744325,
     },
     "qwen7b-layer-6144": {
         "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
-        "lse_pass": 31054550, "lse_merge": 1738778, "colsum_pass": 33071890, "head_sum": 1460231,
-        "lists_norms": 6721683, "gram_sym": 14042020, "gram_finish": 245756, "avba_partials": 331903,
-        "avba_allocate": 36191, "psi_topk_reg": 697023, "gather_compact": 16881677,
+        "lse_pass": 31056374, "lse_merge": 1738778, "colsum_pass": 33076993, "head_sum": 1460231,
+        "lists_norms": 6721705, "gram_sym": 14042062, "gram_finish": 245756, "avba_partials": 331903,
+        "avba_allocate": 36191, "psi_topk_reg": 697023, "gather_compact": 16881639,
     },
     "qwen7b-layer-6144-hidden": {
         "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
-        "lse_pass": 31055949, "lse_merge": 1738710, "colsum_pass": 33073676, "head_sum": 1460362,
-        "modality_lists": 65832, "hidden_norms": 44175380, "gram_wide": 188161921, "hidden_finish": 138239,
+        "lse_pass": 31055225, "lse_merge": 1738710, "colsum_pass": 33082548, "head_sum": 1460345,
+        "modality_lists": 65832, "hidden_norms": 44175417, "gram_wide": 188173558, "hidden_finish": 138239,
         "avba_partials": 331903, "avba_allocate": 36191, "layer_inputs": 272514, "psi_topk_reg": 227003,
-        "gather_compact": 16881674, "gather_hidden": 58879388,
+        "gather_compact": 16881708, "gather_hidden": 58879398,
     },
     "qwen7b-longcache-40960": {
         "sources_sha256": "24c825019fb7279f0410ec26c325d4a26aea536854ca8f7aa8afde88e6a5ded8",
-        "lse_pass": 5087891386, "lse_merge": 3850240, "colsum_pass": 379964935, "head_sum": 5419044,
-        "lists_norms": 44044149, "gram_sym": 946629536, "gram_finish": 1499112, "avba_partials": 1492173,
-        "avba_allocate": 53599, "topk_hist": 2205441, "topk_bin": 1948936, "topk_emit": 2727622,
-        "gather_compact": 134783860,
+        "lse_pass": 5085468639, "lse_merge": 3850240, "colsum_pass": 380252009, "head_sum": 5419069,
+        "lists_norms": 44044125, "gram_sym": 947909492, "gram_finish": 1499112, "avba_partials": 1492173,
+        "avba_allocate": 53599, "topk_hist": 2205441, "topk_bin": 1948912, "topk_emit": 2727622,
+        "gather_compact": 134783809,
     },
 }
 
